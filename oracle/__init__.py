@@ -1,0 +1,162 @@
+"""PrunePath sparse-FFN forward: CPU oracle (fp64) -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The HIP library never calls it and it
+never calls the HIP library; the two share only the seeded bf16 inputs.
+
+The arithmetic lives in ``prunepath_oracle.c`` (fp64, per token, following the
+paper's Sec. 3.1 equations in order); this module only marshals numpy arrays.
+
+Readings taken where the paper is open are stated in the C file's header.
+Every function here is pinned by ``tests/test_oracle_pins.py`` against closed
+forms, library routines, brute force and the paper's all-expert identity
+(Eq. moefication_decomp).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+SELECT_NUCLEUS = 0
+SELECT_STRICT = 1
+AGG_SUM = 0
+AGG_SIGMOID = 2
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB) or (
+                os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC)):
+            _build.build()
+        lib = ctypes.CDLL(_build.LIB)
+        P = ctypes.c_void_p
+        I64 = ctypes.c_int64
+        lib.ppo_route.argtypes = [I64, I64, I64, P, P, P, P, ctypes.c_double, ctypes.c_uint,
+                                  P, P, P, P]
+        lib.ppo_route.restype = ctypes.c_int
+        lib.ppo_ffn.argtypes = [I64, I64, I64, I64, P, P, P, P, P, P, P, P, ctypes.c_uint, P]
+        lib.ppo_ffn.restype = ctypes.c_int
+        lib.ppo_softmax.argtypes = [I64, P, P]
+        lib.ppo_softmax.restype = None
+        lib.ppo_order.argtypes = [I64, P, P]
+        lib.ppo_order.restype = None
+        lib.ppo_cut.argtypes = [I64, P, ctypes.c_double, ctypes.c_uint, P]
+        lib.ppo_cut.restype = I64
+        lib.ppo_num_threads.argtypes = []
+        lib.ppo_num_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def num_threads() -> int:
+    return _load().ppo_num_threads()
+
+
+def softmax(g):
+    g = _c(g, np.float64)
+    p = np.empty_like(g)
+    _load().ppo_softmax(g.size, _ptr(g), _ptr(p))
+    return p
+
+
+def order(g):
+    g = _c(g, np.float64)
+    pi = np.empty(g.size, np.int32)
+    _load().ppo_order(g.size, _ptr(g), _ptr(pi))
+    return pi
+
+
+def cut(p_sorted, tau, flags=0):
+    """Returns (k, C) for probabilities already in descending order."""
+    p = _c(p_sorted, np.float64)
+    C = np.empty_like(p)
+    k = _load().ppo_cut(p.size, _ptr(p), float(tau), int(flags), _ptr(C))
+    return int(k), C
+
+
+def route(x, W_r, tau, flags=0, bias=None, inv_temp=None):
+    """Routing of T tokens.  x: [T,d] uint16 (bf16 bits), W_r: [E,d] uint16.
+
+    Returns dict(idx [T,E] int32 (-1 padded), count [T] int32, g [T,E] fp64
+    logits, cum [T,E] fp64 cumulative mass in selection order)."""
+    x = _c(x, np.uint16)
+    W_r = _c(W_r, np.uint16)
+    T, d = x.shape
+    E = W_r.shape[0]
+    assert W_r.shape[1] == d
+    bias = _c(bias, np.float32)
+    inv_temp = _c(inv_temp, np.float32)
+    idx = np.empty((T, E), np.int32)
+    count = np.empty(T, np.int32)
+    g = np.empty((T, E), np.float64)
+    cum = np.empty((T, E), np.float64)
+    rc = _load().ppo_route(T, d, E, _ptr(x), _ptr(W_r), _ptr(bias), _ptr(inv_temp), float(tau),
+                           int(flags), _ptr(idx), _ptr(count), _ptr(g), _ptr(cum))
+    if rc != 0:
+        raise ValueError("oracle route: bad arguments")
+    return dict(idx=idx, count=count, g=g, cum=cum)
+
+
+def ffn(x, W_gate, W_up, W_down, idx, count, flags=0, g=None, perm=None):
+    """y [T,d] fp64 for a given selection (idx [T,E] -1 padded, count [T])."""
+    x = _c(x, np.uint16)
+    T, d = x.shape
+    d_ff = W_gate.shape[0]
+    E = idx.shape[1]
+    assert W_gate.shape == (d_ff, d) and W_up.shape == (d_ff, d) and W_down.shape == (d, d_ff)
+    y = np.empty((T, d), np.float64)
+    rc = _load().ppo_ffn(T, d, d_ff, E, _ptr(x), _ptr(_c(W_gate, np.uint16)),
+                         _ptr(_c(W_up, np.uint16)), _ptr(_c(W_down, np.uint16)),
+                         _ptr(_c(perm, np.int32)), _ptr(_c(idx, np.int32)),
+                         _ptr(_c(count, np.int32)), _ptr(_c(g, np.float64)), int(flags), _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle ffn: bad arguments")
+    return y
+
+
+def forward(x, W_r, W_gate, W_up, W_down, tau, flags=0, bias=None, inv_temp=None, perm=None):
+    """Routing followed by the selected experts' outputs; returns (route dict, y)."""
+    r = route(x, W_r, tau, flags=flags, bias=bias, inv_temp=inv_temp)
+    y = ffn(x, W_gate, W_up, W_down, r["idx"], r["count"], flags=flags, g=r["g"], perm=perm)
+    return r, y
+
+
+def near_tie(cum, tau, band=1e-5, flags=0):
+    """Tokens whose cumulative mass lies within `band` of tau at some cut
+    position (C_1..C_{E-1}); for these the count may legitimately differ
+    between fp32 and fp64 evaluation.  Nothing is near a tie when the rule
+    keeps every expert regardless of C (nucleus with tau >= 1, strict with
+    tau > 1)."""
+    cum = np.asarray(cum)
+    if (flags & SELECT_STRICT and tau > 1.0) or (not flags & SELECT_STRICT and tau >= 1.0):
+        return np.zeros(cum.shape[0], bool)
+    return (np.abs(cum[:, :-1] - tau) <= band).any(axis=1)
+
+
+def order_tie(g, idx, count, band=1e-5):
+    """Tokens whose logits at the cut (last kept vs first dropped) or inside
+    the kept prefix differ by at most `band`; their expert order (and, at the
+    cut, their set) is not unique under fp32 evaluation."""
+    g = np.asarray(g)
+    T, E = g.shape
+    out = np.zeros(T, bool)
+    for t in range(T):
+        k = int(count[t])
+        srt = np.sort(g[t])[::-1]
+        m = min(k + 1, E)
+        if m >= 2 and (np.diff(srt[:m]) >= -band).any():
+            out[t] = True
+    return out

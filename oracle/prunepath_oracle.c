@@ -1,0 +1,227 @@
+/*
+ * PrunePath sparse-FFN forward -- CPU oracle in fp64.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may call, link or
+ * load this file; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark use it.  It shares no code, header, table or helper with the
+ * HIP library: the two meet only at the seeded bf16 input arrays.
+ *
+ * Every quantity is computed in double precision from the exact values of the
+ * same bf16 bit patterns the GPU path consumes.  The code follows the paper's
+ * equations in their own order and notation (Sec. 2.1 and Sec. 3.1):
+ *
+ *   g = W_r^T x                         Eq. (routing_logits)
+ *   p = softmax(g)                      Eq. (softmax_prob)
+ *   pi = descending order of p          Sec. 3.1, text after Eq. (softmax_prob)
+ *   C_i = sum_{r<=i} p_{pi_r}
+ *   A_tau(x) from C and tau             Eq. (tau_thresh_activate), nucleus reading
+ *   y = sum_{e in A} [sigmoid(g_e)] FFN_e(x)   Eqs. (moefication_decomp), (moe_output)
+ *   FFN_e(x) = (phi(x Wg^(e)) . x Wu^(e)) Wd^(e), phi = SiLU   Eq. (ffn)
+ *
+ * Readings of points the paper leaves open (each is listed in the design notes):
+ *  - Selection rule.  Default (nucleus): the smallest prefix of pi whose mass
+ *    reaches tau; tau >= 1 keeps all E experts (exact-arithmetic result: every
+ *    softmax probability is positive).  Flag PPO_SELECT_STRICT: the rule as
+ *    printed, {pi_1} U {pi_i : C_i < tau}, with C_E = 1 by definition.
+ *  - Ties in the ordering: the lower expert index comes first.  The order is
+ *    taken on g, which is equivalent to ordering p (softmax is monotone).
+ *  - Aggregation.  Default: plain sum (Eq. moefication_decomp, whose all-expert
+ *    case is the dense FFN).  Flag PPO_AGG_SIGMOID: Eq. (moe_output).
+ *  - Router extras for the skewed workload: g = (W_r x + b) * inv_temp_t.
+ *  - Layouts follow the API: W_r [E,d], W_gate/W_up [d_ff,d], W_down [d,d_ff]
+ *    (the paper's matrices transposed).  Expert e owns neurons
+ *    perm[e*de .. e*de+de-1] (identity when perm is NULL), de = d_ff / E.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define PPO_SELECT_STRICT 1u
+#define PPO_AGG_SIGMOID 2u
+
+/* Exact value of a bf16 bit pattern: its bits are the top half of an IEEE
+ * binary32 number. */
+static double bf16_value(uint16_t h) {
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+int ppo_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* Eq. (routing_logits), one token: g_e = sum_j W_r[e,j] x_j, then the optional
+ * per-expert bias and per-token inverse temperature of the skewed workload. */
+static void logits_one(int64_t d, int64_t E, const uint16_t *x, const uint16_t *Wr,
+                       const float *bias, double inv_temp, double *g) {
+    for (int64_t e = 0; e < E; ++e) {
+        double s = 0.0;
+        const uint16_t *w = Wr + e * d;
+        for (int64_t j = 0; j < d; ++j) s += bf16_value(w[j]) * bf16_value(x[j]);
+        if (bias) s += (double)bias[e];
+        g[e] = s * inv_temp;
+    }
+}
+
+/* Eq. (softmax_prob).  Subtracting max g leaves the value unchanged. */
+void ppo_softmax(int64_t E, const double *g, double *p) {
+    double m = g[0];
+    for (int64_t e = 1; e < E; ++e)
+        if (g[e] > m) m = g[e];
+    double z = 0.0;
+    for (int64_t e = 0; e < E; ++e) {
+        p[e] = exp(g[e] - m);
+        z += p[e];
+    }
+    for (int64_t e = 0; e < E; ++e) p[e] /= z;
+}
+
+/* pi: experts in descending order of probability (equivalently of logit);
+ * equal logits keep ascending expert index.  Insertion sort, E <= a few
+ * hundred. */
+void ppo_order(int64_t E, const double *g, int32_t *pi) {
+    for (int64_t i = 0; i < E; ++i) {
+        int32_t e = (int32_t)i;
+        int64_t j = i;
+        while (j > 0 && g[pi[j - 1]] < g[e]) {
+            pi[j] = pi[j - 1];
+            --j;
+        }
+        pi[j] = e;
+    }
+}
+
+/* Eq. (tau_thresh_activate): given p already in the order pi, form the
+ * cumulative masses C_1..C_E (written to C) and return the number k of
+ * selected experts; the selection is always the prefix pi_1..pi_k.
+ *
+ *  nucleus (default): k = min{i : C_i >= tau}; all E when tau >= 1.
+ *  strict:            k = max(1, #{i : C_i < tau}) with C_E taken as exactly 1.
+ */
+int64_t ppo_cut(int64_t E, const double *p_sorted, double tau, unsigned flags, double *C) {
+    double c = 0.0;
+    for (int64_t i = 0; i < E; ++i) {
+        c += p_sorted[i];
+        C[i] = c;
+    }
+    if (flags & PPO_SELECT_STRICT) {
+        int64_t m = 0;
+        for (int64_t i = 0; i < E - 1; ++i)
+            if (C[i] < tau) ++m;
+        if (1.0 < tau) ++m; /* C_E = 1 */
+        return m < 1 ? 1 : m;
+    }
+    if (tau >= 1.0) return E;
+    for (int64_t i = 0; i < E; ++i)
+        if (C[i] >= tau) return i + 1;
+    return E;
+}
+
+/* Routing for T tokens.  Outputs per token t (row-major [T,E]):
+ *   idx[t, 0..k-1] = pi_1..pi_k (rest -1), count[t] = k,
+ *   g[t, e] logits, cum[t, i] = C_{i+1} in the order pi.
+ * Returns 0, or -1 on bad arguments. */
+int ppo_route(int64_t T, int64_t d, int64_t E, const uint16_t *x, const uint16_t *Wr,
+              const float *bias, const float *inv_temp, double tau, unsigned flags,
+              int32_t *idx, int32_t *count, double *g, double *cum) {
+    if (T < 0 || d < 1 || E < 1 || !x || !Wr || !idx || !count || !g || !cum) return -1;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (int64_t t = 0; t < T; ++t) {
+        double *gt = g + t * E;
+        double *p = (double *)malloc(sizeof(double) * (size_t)E * 2);
+        int32_t *pi = (int32_t *)malloc(sizeof(int32_t) * (size_t)E);
+        if (!p || !pi) {
+            bad = 1;
+            free(p);
+            free(pi);
+            continue;
+        }
+        double *ps = p + E;
+        logits_one(d, E, x + t * d, Wr, bias, inv_temp ? (double)inv_temp[t] : 1.0, gt);
+        ppo_softmax(E, gt, p);
+        ppo_order(E, gt, pi);
+        for (int64_t i = 0; i < E; ++i) ps[i] = p[pi[i]];
+        int64_t k = ppo_cut(E, ps, tau, flags, cum + t * E);
+        count[t] = (int32_t)k;
+        for (int64_t i = 0; i < E; ++i) idx[t * E + i] = i < k ? pi[i] : -1;
+        free(p);
+        free(pi);
+    }
+    return bad ? -1 : 0;
+}
+
+/* Expert outputs summed over a given selection, Eqs. (moefication_decomp) and
+ * (moe_output), with FFN_e from Eq. (ffn) restricted to expert e's neurons:
+ *   a_n = Wg[n,:] . x,  b_n = Wu[n,:] . x,  h_n = SiLU(a_n) b_n [* sigmoid(g_e)]
+ *   y_i = sum over selected neurons n of Wd[i, n] h_n.
+ * idx/count use the layout written by ppo_route (any order of experts is
+ * accepted).  g is needed only with PPO_AGG_SIGMOID.  y is [T,d], overwritten.
+ * Returns 0, or -1 on bad arguments. */
+int ppo_ffn(int64_t T, int64_t d, int64_t d_ff, int64_t E, const uint16_t *x,
+            const uint16_t *Wg, const uint16_t *Wu, const uint16_t *Wd, const int32_t *perm,
+            const int32_t *idx, const int32_t *count, const double *g, unsigned flags,
+            double *y) {
+    if (T < 0 || d < 1 || E < 1 || d_ff % E != 0 || !x || !Wg || !Wu || !Wd || !idx || !count ||
+        !y)
+        return -1;
+    if ((flags & PPO_AGG_SIGMOID) && !g) return -1;
+    const int64_t de = d_ff / E;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (int64_t t = 0; t < T; ++t) {
+        const uint16_t *xt = x + t * d;
+        double *yt = y + t * d;
+        int64_t k = count[t];
+        int32_t *nsel = (int32_t *)malloc(sizeof(int32_t) * (size_t)(k * de + 1));
+        double *h = (double *)malloc(sizeof(double) * (size_t)(k * de + 1));
+        double *xv = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!nsel || !h || !xv || k < 0 || k > E) {
+            bad = 1;
+            free(nsel);
+            free(h);
+            free(xv);
+            continue;
+        }
+        for (int64_t j = 0; j < d; ++j) xv[j] = bf16_value(xt[j]);
+        /* intermediate activations of the selected neurons */
+        for (int64_t s = 0; s < k; ++s) {
+            int64_t e = idx[t * E + s];
+            double scale = 1.0;
+            if (flags & PPO_AGG_SIGMOID) scale = 1.0 / (1.0 + exp(-g[t * E + e]));
+            for (int64_t r = 0; r < de; ++r) {
+                int64_t n = perm ? perm[e * de + r] : e * de + r;
+                const uint16_t *wg = Wg + n * d;
+                const uint16_t *wu = Wu + n * d;
+                double a = 0.0, b = 0.0;
+                for (int64_t j = 0; j < d; ++j) {
+                    a += bf16_value(wg[j]) * xv[j];
+                    b += bf16_value(wu[j]) * xv[j];
+                }
+                nsel[s * de + r] = (int32_t)n;
+                h[s * de + r] = a / (1.0 + exp(-a)) * b * scale;
+            }
+        }
+        /* down projection over the selected neurons */
+        for (int64_t i = 0; i < d; ++i) {
+            const uint16_t *wd = Wd + i * d_ff;
+            double acc = 0.0;
+            for (int64_t q = 0; q < k * de; ++q) acc += bf16_value(wd[nsel[q]]) * h[q];
+            yt[i] = acc;
+        }
+        free(nsel);
+        free(h);
+        free(xv);
+    }
+    return bad ? -1 : 0;
+}

@@ -1,0 +1,140 @@
+"""Seeded synthetic inputs for the sparse-FFN forward.
+
+This module only draws random numbers and rounds them to bf16; it holds none
+of the method's arithmetic.  Both the oracle-based tests and the HIP path
+consume exactly the arrays produced here (bf16 values are carried as their
+uint16 bit patterns).
+
+Recipe (the paper's datasets and trained checkpoints are not available, so
+these synthetic layers stand in for them):
+  * one ``numpy.random.default_rng(seed)`` (PCG64) stream per layer, drawn in
+    the fixed order W_r, W_gate, W_up, W_down, then the layer extras (skewed
+    router bias);
+  * expert/gate/up/down weights ~ N(0, 0.02^2);  router weights
+    ~ N(0, (3/sqrt(d))^2) so that logits of a unit-variance token have std ~3
+    (sharp routing distributions, which the paper's entropy loss aims for);
+  * tokens come from a separate stream: x ~ N(0, 1), optionally each row scaled
+    by LogNormal(0, 0.5) (prefill workload), and for the skewed workload a
+    per-token temperature ~ U(0.5, 2) passed as its inverse;
+  * the skewed workload adds a per-expert router bias ~ Gumbel(0, 1.5);
+  * every value is drawn in fp32 and rounded to bf16 with round-to-nearest-even.
+"""
+from dataclasses import dataclass, field
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+EXPERT_WIDTH = 128
+
+
+def bf16_bits(a) -> np.ndarray:
+    """Round fp32 values to bf16 (nearest, ties to even); return uint16 bits."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    u = u.astype(np.uint64)
+    r = ((u >> 16) & 1) + 0x7FFF
+    return ((u + r) >> 16).astype(np.uint16)
+
+
+def bf16_to_f32(bits) -> np.ndarray:
+    """Exact fp32 value of bf16 bit patterns."""
+    b = np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32)
+
+
+@dataclass
+class Layer:
+    d: int
+    d_ff: int
+    E: int
+    W_r: np.ndarray      # [E, d]    bf16 bits
+    W_gate: np.ndarray   # [d_ff, d] bf16 bits
+    W_up: np.ndarray     # [d_ff, d] bf16 bits
+    W_down: np.ndarray   # [d, d_ff] bf16 bits
+    bias: Optional[np.ndarray] = None   # [E] fp32 (skewed router only)
+    perm: Optional[np.ndarray] = None   # [d_ff] int32 neuron permutation
+
+
+def make_layer(d: int, d_ff: int, E: int, seed, *, weight_std: float = 0.02,
+               router_std: Optional[float] = None, skewed: bool = False,
+               perm: bool = False) -> Layer:
+    """One bias-free SwiGLU FFN layer with its linear router."""
+    rng = np.random.default_rng(seed)
+    if router_std is None:
+        router_std = 3.0 / np.sqrt(d)
+    W_r = bf16_bits(rng.standard_normal((E, d), dtype=np.float32) * np.float32(router_std))
+    W_gate = bf16_bits(rng.standard_normal((d_ff, d), dtype=np.float32) * np.float32(weight_std))
+    W_up = bf16_bits(rng.standard_normal((d_ff, d), dtype=np.float32) * np.float32(weight_std))
+    W_down = bf16_bits(rng.standard_normal((d, d_ff), dtype=np.float32) * np.float32(weight_std))
+    bias = None
+    if skewed:
+        bias = rng.gumbel(0.0, 1.5, size=E).astype(np.float32)
+    p = None
+    if perm:
+        p = rng.permutation(d_ff).astype(np.int32)
+    return Layer(d, d_ff, E, W_r, W_gate, W_up, W_down, bias, p)
+
+
+def make_tokens(T: int, d: int, seed, *, row_lognormal_sigma: float = 0.0,
+                temperature: bool = False) -> Tuple[np.ndarray, Optional[np.ndarray]]:
+    """x [T, d] bf16 bits and, for the skewed workload, inv_temp [T] fp32."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((T, d), dtype=np.float32)
+    if row_lognormal_sigma > 0.0:
+        s = rng.lognormal(0.0, row_lognormal_sigma, size=(T, 1)).astype(np.float32)
+        x = x * s
+    inv_temp = None
+    if temperature:
+        inv_temp = (1.0 / rng.uniform(0.5, 2.0, size=T)).astype(np.float32)
+    return bf16_bits(x), inv_temp
+
+
+# --------------------------------------------------------------------------
+# The five workloads.  Token streams use seed + 1000 so that changing T never
+# changes the weights.
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    d: int
+    d_ff: int
+    E: int
+    T: Tuple[int, ...]
+    taus: Tuple[float, ...]
+    layers: int = 1
+    skewed: bool = False
+    row_lognormal_sigma: float = 0.0
+    notes: str = ""
+
+
+WORKLOADS: Dict[str, Workload] = {
+    "tiny": Workload("tiny", 512, 2048, 16, (4,), (0.9,),
+                     notes="single FFN layer, E=16 experts of 128 neurons, T=4 decode"),
+    "llama8b_decode": Workload("llama8b_decode", 4096, 14336, 112, (1, 8, 32, 64),
+                               (0.5, 0.7, 0.9, 1.0),
+                               notes="LLaMA-3-8B-shaped FFN layer, decode batches"),
+    "llama8b_stack32": Workload("llama8b_stack32", 4096, 14336, 112, (16,), (0.8,), layers=32,
+                                notes="32 layers chained by residual add + RMSNorm(eps 1e-5)"),
+    "llama8b_prefill": Workload("llama8b_prefill", 4096, 14336, 112, (2048,), (0.7, 0.9),
+                                row_lognormal_sigma=0.5,
+                                notes="prefill, rows scaled by LogNormal(0, 0.5)"),
+    "qwen7b_skewed": Workload("qwen7b_skewed", 3584, 18944, 148, (64,), (0.5, 0.9),
+                              skewed=True,
+                              notes="Gumbel(0,1.5) router bias, per-token temperature U(0.5,2)"),
+}
+
+
+def workload_layer(w: Workload, seed: int = 0, layer: int = 0) -> Layer:
+    if w.layers > 1:
+        s = np.random.SeedSequence(seed).spawn(w.layers + 1)[layer]
+    else:
+        s = seed
+    return make_layer(w.d, w.d_ff, w.E, s, skewed=w.skewed)
+
+
+def workload_tokens(w: Workload, T: int, seed: int = 0):
+    if w.layers > 1:
+        s = np.random.SeedSequence(seed).spawn(w.layers + 1)[w.layers]
+    else:
+        s = seed + 1000
+    return make_tokens(T, w.d, s, row_lognormal_sigma=w.row_lognormal_sigma,
+                       temperature=w.skewed)

@@ -1,0 +1,321 @@
+"""Pins of the CPU oracle against things other than itself.
+
+Each check ties one part of the oracle (Sec. 3.1 routing, Sec. 2.1/2.2 expert
+evaluation) to a library routine, a closed form, brute force or the paper's
+exact identity (Eq. moefication_decomp: all experts reproduce the dense FFN).
+Chosen so that a dropped term, a wrong sign, a swapped operand or an index
+slip anywhere in the oracle fails at least one of them.
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy.special import softmax as sp_softmax
+
+from paper_2605_28283_amd.workloads import bf16_bits, bf16_to_f32, make_layer, make_tokens
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "select_worked_cases.txt")
+
+
+def f64(bits):
+    return bf16_to_f32(bits).astype(np.float64)
+
+
+def silu(a):
+    return a / (1.0 + np.exp(-a))
+
+
+def dense_ffn(x, Wg, Wu, Wd):
+    """Eq. (ffn) with the API's [out, in] layouts, numpy float64, no experts."""
+    X, G, U, D = f64(x), f64(Wg), f64(Wu), f64(Wd)
+    return (silu(X @ G.T) * (X @ U.T)) @ D.T
+
+
+def small_layer(d=64, E=6, seed=3, perm=False, skewed=False):
+    return make_layer(d, 128 * E, E, seed, perm=perm, skewed=skewed)
+
+
+# ---------------------------------------------------------------- routing steps
+
+def test_logits_match_numpy_matmul(oracle_mod):
+    L = small_layer(d=96, E=12, skewed=True)
+    x, it = make_tokens(7, 96, 11, temperature=True)
+    r = oracle_mod.route(x, L.W_r, 0.9, bias=L.bias, inv_temp=it)
+    ref = (f64(x) @ f64(L.W_r).T + L.bias.astype(np.float64)) * it.astype(np.float64)[:, None]
+    np.testing.assert_allclose(r["g"], ref, rtol=1e-12, atol=1e-12)
+    # and without the extras the bias / temperature must not leak in
+    r0 = oracle_mod.route(x, L.W_r, 0.9)
+    np.testing.assert_allclose(r0["g"], f64(x) @ f64(L.W_r).T, rtol=1e-12, atol=1e-12)
+
+
+def test_softmax_textbook(oracle_mod):
+    rng = np.random.default_rng(5)
+    for E in (1, 2, 16, 112, 256):
+        g = rng.normal(0, 3, E) + 40.0  # offset: must be shift-invariant
+        p = oracle_mod.softmax(g)
+        np.testing.assert_allclose(p, sp_softmax(g), rtol=1e-13, atol=1e-300)
+        assert abs(p.sum() - 1.0) < 1e-14
+
+
+def test_order_matches_stable_argsort(oracle_mod):
+    rng = np.random.default_rng(6)
+    for E in (1, 3, 16, 112, 256):
+        g = np.round(rng.normal(0, 2, E), 1)  # rounding creates exact ties
+        pi = oracle_mod.order(g)
+        np.testing.assert_array_equal(pi, np.argsort(-g, kind="stable"))
+
+
+def nucleus_ref(C, tau):
+    E = len(C)
+    if tau >= 1.0:
+        return E
+    for i in range(E):
+        if C[i] >= tau:
+            return i + 1
+    return E
+
+
+def test_cut_closed_form(oracle_mod):
+    rng = np.random.default_rng(7)
+    for trial in range(50):
+        E = int(rng.integers(1, 40))
+        p = np.sort(rng.dirichlet(np.full(E, 0.3)))[::-1]
+        for tau in np.concatenate([[0.0, 1.0, 1.05], rng.uniform(0, 1, 8)]):
+            k, C = oracle_mod.cut(p, tau, 0)
+            np.testing.assert_allclose(C, np.cumsum(p), rtol=1e-14)
+            assert 1 <= k <= E
+            if tau < 1.0 and k < E:
+                assert C[k - 1] >= tau
+            if k > 1 and tau < 1.0:
+                assert C[k - 2] < tau
+            if tau >= 1.0:
+                assert k == E
+            assert k == nucleus_ref(C, tau)
+    # tau = 1 keeps every expert even when the float cumulative sum saturates
+    # at 1 before the tail (every softmax probability is positive)
+    p = np.array([1.0, 1e-20, 1e-30])
+    assert oracle_mod.cut(p, 1.0, 0)[0] == 3
+    assert oracle_mod.cut(p, 1.0 - 1e-12, 0)[0] == 1
+
+
+def test_strict_relation(oracle_mod):
+    """The printed rule keeps one expert fewer than the nucleus prefix for
+    0 < tau < 1, never fewer than one, and all E only for tau > 1."""
+    rng = np.random.default_rng(8)
+    for trial in range(50):
+        E = int(rng.integers(2, 40))
+        p = np.sort(rng.dirichlet(np.full(E, 0.5)))[::-1]
+        for tau in rng.uniform(0.01, 0.99, 6):
+            kn, C = oracle_mod.cut(p, tau, 0)
+            ks, _ = oracle_mod.cut(p, tau, 1)
+            if np.min(np.abs(C - tau)) < 1e-12:
+                continue
+            assert ks == max(1, kn - 1)
+        kn1, C = oracle_mod.cut(p, 1.0, 1)
+        assert kn1 == int(np.sum(C[:-1] < 1.0))
+        assert oracle_mod.cut(p, 1.05, 1)[0] == E
+        assert oracle_mod.cut(p, 0.0, 1)[0] == 1
+
+
+def test_brute_force_small_E(oracle_mod):
+    """E <= 8: the nucleus set is a minimum-cardinality subset reaching tau
+    and has the largest mass among subsets of that size."""
+    rng = np.random.default_rng(9)
+    for trial in range(40):
+        E = int(rng.integers(2, 9))
+        g = rng.normal(0, 2, E)
+        p = sp_softmax(g)
+        tau = float(rng.uniform(0.05, 0.99))
+        pi = oracle_mod.order(g)
+        k, C = oracle_mod.cut(p[pi], tau, 0)
+        if np.min(np.abs(C - tau)) < 1e-12:
+            continue
+        best_card, best_mass = None, {}
+        for r in range(1, E + 1):
+            for sub in itertools.combinations(range(E), r):
+                m = p[list(sub)].sum()
+                best_mass[r] = max(best_mass.get(r, 0.0), m)
+                if m >= tau and best_card is None:
+                    best_card = r
+        assert k == best_card
+        assert abs(p[pi[:k]].sum() - best_mass[k]) < 1e-12
+
+
+def _golden_cases():
+    out = []
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            kind, vals, tau, rule, exp = [s.strip() for s in line.split("|")]
+            out.append((kind, [float(v) for v in vals.split()], float(tau), rule,
+                        [int(v) for v in exp.split()]))
+    return out
+
+
+def test_golden_worked_cases(oracle_mod):
+    cases = _golden_cases()
+    assert len(cases) >= 20
+    for kind, vals, tau, rule, expected in cases:
+        flags = oracle_mod.SELECT_STRICT if rule == "strict" else 0
+        if kind == "probs":
+            p = np.array(vals)
+            pi = oracle_mod.order(np.log(p))
+            k, _ = oracle_mod.cut(p[pi], tau, flags)
+            got = list(pi[:k])
+        else:
+            E = len(vals)
+            x = bf16_bits(np.array([[1.0]], np.float32))
+            W_r = bf16_bits(np.array(vals, np.float32).reshape(E, 1))
+            r = oracle_mod.route(x, W_r, tau, flags)
+            got = list(r["idx"][0, : r["count"][0]])
+        assert got == expected, (kind, vals, tau, rule)
+
+
+def test_route_selection_vs_numpy(oracle_mod):
+    L = small_layer(d=128, E=16, seed=4)
+    x, _ = make_tokens(40, 128, 12)
+    for tau in (0.0, 0.3, 0.5, 0.8, 0.95, 1.0, 1.05):
+        r = oracle_mod.route(x, L.W_r, tau)
+        g = f64(x) @ f64(L.W_r).T
+        for t in range(x.shape[0]):
+            order = np.argsort(-g[t], kind="stable")
+            C = np.cumsum(sp_softmax(g[t])[order])
+            k = nucleus_ref(C, tau)
+            assert r["count"][t] == k
+            np.testing.assert_array_equal(r["idx"][t, :k], order[:k])
+            assert (r["idx"][t, k:] == -1).all()
+
+
+def test_count_monotone_in_tau(oracle_mod):
+    L = small_layer(d=128, E=32, seed=5)
+    x, _ = make_tokens(30, 128, 13)
+    prev = None
+    for tau in np.linspace(0, 1.05, 43):
+        c = oracle_mod.route(x, L.W_r, tau)["count"]
+        if prev is not None:
+            assert (c >= prev).all()
+        prev = c
+    assert (prev == 32).all()
+
+
+# ---------------------------------------------------------------- expert evaluation
+
+@pytest.mark.parametrize("perm", [False, True])
+def test_all_experts_equal_dense_ffn(oracle_mod, perm):
+    """Eq. (moefication_decomp): activating every expert is an identity
+    transformation of the dense FFN (also after a neuron permutation)."""
+    L = small_layer(d=64, E=6, seed=21, perm=perm)
+    x, _ = make_tokens(9, 64, 22)
+    ref = dense_ffn(x, L.W_gate, L.W_up, L.W_down)
+    for tau in (1.0, 1.05):
+        r, y = oracle_mod.forward(x, L.W_r, L.W_gate, L.W_up, L.W_down, tau, perm=L.perm)
+        assert (r["count"] == 6).all()
+        np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-12)
+
+
+def masked_dense(x, L, idx, count, scale=None):
+    """Eq. (ffn) over all neurons, then zero the neurons of unkept experts
+    (optionally scaling kept ones), then the down projection."""
+    X = f64(x)
+    H = silu(X @ f64(L.W_gate).T) * (X @ f64(L.W_up).T)
+    T, d_ff = H.shape
+    E = idx.shape[1]
+    owner = np.empty(d_ff, np.int64)
+    neurons = L.perm if L.perm is not None else np.arange(d_ff)
+    owner[neurons] = np.arange(d_ff) // (d_ff // E)
+    M = np.zeros((T, E))
+    for t in range(T):
+        M[t, idx[t, : count[t]]] = 1.0 if scale is None else scale[t, idx[t, : count[t]]]
+    return (H * M[:, owner]) @ f64(L.W_down).T
+
+
+@pytest.mark.parametrize("perm", [False, True])
+def test_partial_selection_equals_masked_dense(oracle_mod, perm):
+    L = small_layer(d=64, E=8, seed=31, perm=perm)
+    x, _ = make_tokens(12, 64, 32)
+    for tau in (0.0, 0.4, 0.8):
+        r, y = oracle_mod.forward(x, L.W_r, L.W_gate, L.W_up, L.W_down, tau, perm=L.perm)
+        np.testing.assert_allclose(y, masked_dense(x, L, r["idx"], r["count"]), rtol=1e-10,
+                                   atol=1e-12)
+
+
+def test_sigmoid_aggregation_equals_scaled_masked_dense(oracle_mod):
+    """Eq. (moe_output): each kept expert's output scaled by sigmoid(g_e)."""
+    L = small_layer(d=64, E=8, seed=41, skewed=True)
+    x, it = make_tokens(10, 64, 42, temperature=True)
+    fl = oracle_mod.AGG_SIGMOID
+    r, y = oracle_mod.forward(x, L.W_r, L.W_gate, L.W_up, L.W_down, 0.7, flags=fl, bias=L.bias,
+                              inv_temp=it)
+    g = (f64(x) @ f64(L.W_r).T + L.bias) * it.astype(np.float64)[:, None]
+    sig = 1.0 / (1.0 + np.exp(-g))
+    np.testing.assert_allclose(y, masked_dense(x, L, r["idx"], r["count"], scale=sig),
+                               rtol=1e-10, atol=1e-12)
+
+
+def test_single_expert_is_dense(oracle_mod):
+    L = make_layer(64, 128, 1, 51)
+    x, _ = make_tokens(5, 64, 52)
+    ref = dense_ffn(x, L.W_gate, L.W_up, L.W_down)
+    for tau in (0.0, 0.5, 1.0):
+        _, y = oracle_mod.forward(x, L.W_r, L.W_gate, L.W_up, L.W_down, tau)
+        np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-12)
+
+
+def test_expert_sum_is_additive(oracle_mod):
+    """y over a union of disjoint expert sets is the sum of the parts."""
+    L = small_layer(d=64, E=6, seed=61)
+    x, _ = make_tokens(3, 64, 62)
+    A = np.array([[0, 4, -1, -1, -1, -1]] * 3, np.int32)
+    B = np.array([[5, 1, 2, -1, -1, -1]] * 3, np.int32)
+    AB = np.array([[2, 0, 5, 4, 1, -1]] * 3, np.int32)
+    yA = oracle_mod.ffn(x, L.W_gate, L.W_up, L.W_down, A, np.full(3, 2, np.int32))
+    yB = oracle_mod.ffn(x, L.W_gate, L.W_up, L.W_down, B, np.full(3, 3, np.int32))
+    yAB = oracle_mod.ffn(x, L.W_gate, L.W_up, L.W_down, AB, np.full(3, 5, np.int32))
+    np.testing.assert_allclose(yAB, yA + yB, rtol=1e-12, atol=1e-13)
+
+
+def test_scalar_closed_form(oracle_mod):
+    """One-hot token, hand-placed bf16-exact weights: every output has a
+    closed form in terms of SiLU(a) b = a b / (1 + e^-a)."""
+    d, E = 64, 2
+    d_ff = 128 * E
+    Wg = np.zeros((d_ff, d), np.float32)
+    Wu = np.zeros((d_ff, d), np.float32)
+    Wd = np.zeros((d, d_ff), np.float32)
+    a_vals = {3: 1.5, 130: -2.0, 200: 0.25}   # neuron -> gate pre-activation
+    b_vals = {3: 2.0, 130: 0.5, 200: -4.0}    # neuron -> up pre-activation
+    for n in a_vals:
+        Wg[n, 0] = a_vals[n]
+        Wu[n, 0] = b_vals[n]
+    Wd[7, 3] = 1.0
+    Wd[7, 130] = 0.5
+    Wd[9, 200] = -2.0
+    x = np.zeros((1, d), np.float32)
+    x[0, 0] = 1.0
+    h = {n: a_vals[n] * b_vals[n] / (1.0 + math.exp(-a_vals[n])) for n in a_vals}
+    args = [bf16_bits(v) for v in (x, Wg, Wu, Wd)]
+    for sel, cnt in (([0, 1], 2), ([0, -1], 1), ([1, -1], 1)):
+        y = oracle_mod.ffn(*args, np.array([sel], np.int32), np.array([cnt], np.int32))
+        kept = set(sel[:cnt])
+        e7 = (h[3] if 0 in kept else 0.0) + (0.5 * h[130] if 1 in kept else 0.0)
+        e9 = -2.0 * h[200] if 1 in kept else 0.0
+        exp = np.zeros(d)
+        exp[7], exp[9] = e7, e9
+        np.testing.assert_allclose(y[0], exp, rtol=1e-14, atol=1e-15)
+    # sigmoid aggregation with known logits g = (2, -1)
+    g = np.array([[2.0, -1.0]])
+    y = oracle_mod.ffn(*args, np.array([[0, 1]], np.int32), np.array([2], np.int32),
+                       flags=oracle_mod.AGG_SIGMOID, g=g)
+    s0, s1 = 1 / (1 + math.exp(-2.0)), 1 / (1 + math.exp(1.0))
+    assert abs(y[0, 7] - (s0 * h[3] + s1 * 0.5 * h[130])) < 1e-14
+    assert abs(y[0, 9] - s1 * (-2.0) * h[200]) < 1e-14
+
+
+def test_near_tie_helper(oracle_mod):
+    cum = np.array([[0.5, 0.899995, 1.0], [0.5, 0.95, 1.0]])
+    assert list(oracle_mod.near_tie(cum, 0.9)) == [True, False]
+    assert not oracle_mod.near_tie(cum, 1.0).any()
