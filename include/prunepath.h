@@ -1,0 +1,135 @@
+/*
+ * prunepath.h -- C ABI of the MI355X (gfx950) PrunePath sparse-FFN forward.
+ *
+ * What is computed (PrunePath, Sec. 3.1, on the MoEfied FFN of Sec. 2.2):
+ * a bias-free SwiGLU FFN (Eq. ffn) whose d_ff intermediate neurons are split
+ * into E contiguous experts of de = d_ff/E = 128 neurons (Eq. moefication_decomp,
+ * optionally after a neuron permutation, Eq. permuted_weights).  For every
+ * token x a linear router gives logits g = W_r x (Eq. routing_logits), their
+ * softmax p (Eq. softmax_prob) is ordered descending, and a prefix of that
+ * order is kept according to the cumulative-mass budget tau
+ * (Eq. tau_thresh_activate).  Only the kept experts' gate/up/down slices are
+ * evaluated and their outputs summed (Eq. moefication_decomp restricted to the
+ * kept set; Eq. moe_output with PP_AGG_SIGMOID).
+ *
+ * Conventions shared by every entry point
+ *  - All array arguments are DEVICE pointers on the current HIP device, unless
+ *    stated otherwise.  bf16 values are passed as their uint16_t bit patterns.
+ *  - Row-major layouts with the API's [out, in] orientation: W_r [E, d],
+ *    W_gate/W_up [d_ff, d], W_down [d, d_ff] (the paper's matrices are the
+ *    transposes), x [T, d], y [T, d].
+ *  - `hip_stream` is a hipStream_t (NULL = the default stream).  Every call
+ *    except create/destroy only enqueues work on that stream and returns; the
+ *    results are valid once the stream has reached that point.
+ *  - A handle owns internal scratch, so one handle must not be used by two
+ *    calls that can run concurrently (for example on two streams).
+ *  - Errors: a call that returns anything but PP_OK has enqueued no work and
+ *    left every output untouched, except PP_EHIP, which reports a failure of
+ *    the HIP runtime (outputs then undefined).  No exception or abort crosses
+ *    this interface.
+ */
+#ifndef PRUNEPATH_H
+#define PRUNEPATH_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Opaque layer handle: the repacked expert weights plus scratch. */
+typedef struct pp_layer pp_layer;
+
+typedef enum {
+    PP_OK = 0,
+    PP_EINVAL = 1,        /* bad argument (NULL pointer, size, tau, permutation) */
+    PP_ENOMEM = 2,        /* device allocation failed */
+    PP_EHIP = 3,          /* HIP runtime error */
+    PP_EUNSUPPORTED = 4   /* valid but unsupported shape (see create) */
+} pp_status;
+
+/* Selection rule (Eq. tau_thresh_activate; pi = experts by descending p,
+ * C_i = p_pi1 + ... + p_pii; ties in p are ordered by ascending expert index):
+ *  PP_SELECT_NUCLEUS: keep the smallest prefix pi_1..pi_k with C_k >= tau (the
+ *    top-p reading named next to the equation); tau >= 1 keeps all E experts,
+ *    tau = 0 keeps pi_1.
+ *  PP_SELECT_STRICT: the printed rule {pi_1} U {pi_i : C_i < tau}, C_E = 1. */
+#define PP_SELECT_NUCLEUS 0u
+#define PP_SELECT_STRICT 1u
+/* Aggregation: PP_AGG_SUM = plain sum of the kept experts' outputs (the
+ * all-expert case is the dense FFN, Eq. moefication_decomp);
+ * PP_AGG_SIGMOID = each kept expert scaled by sigmoid(g_e), Eq. moe_output. */
+#define PP_AGG_SUM 0u
+#define PP_AGG_SIGMOID 2u
+
+/* prunepath_create -- build a layer (Sec. 2.2 expert split, Sec. 3.1 router).
+ *   out        : receives the handle (host pointer to a host variable).
+ *   d          : model width; must be a positive multiple of 64.
+ *   d_ff, E    : intermediate width and expert count; d_ff must equal 128*E
+ *                (PP_EUNSUPPORTED otherwise) and 1 <= E <= 256.
+ *   max_tokens : largest T any later call will pass (1 .. 65536); scratch is
+ *                sized for it.
+ *   W_r        : [E, d] bf16 router weights (paper's W_r transposed).
+ *   W_gate,
+ *   W_up       : [d_ff, d] bf16, row n = intermediate neuron n.
+ *   W_down     : [d, d_ff] bf16, column n = intermediate neuron n.
+ *   perm       : [d_ff] int32 neuron permutation Pi (expert e owns neurons
+ *                perm[128e .. 128e+127]), or NULL for the identity; it must be
+ *                a permutation of 0..d_ff-1 (PP_EINVAL otherwise).
+ *   router_bias: [E] fp32 added to the logits (g = W_r x + b), or NULL.
+ *   flags      : PP_SELECT_* | PP_AGG_*.
+ * The weights are copied and repacked into library-owned device memory; the
+ * call synchronises `hip_stream` before returning, after which the caller may
+ * free its arrays.  On failure *out is set to NULL. */
+pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
+                           int32_t max_tokens, const uint16_t *W_r, const uint16_t *W_gate,
+                           const uint16_t *W_up, const uint16_t *W_down, const int32_t *perm,
+                           const float *router_bias, uint32_t flags, void *hip_stream);
+
+/* prunepath_route -- routing only (Eqs. routing_logits, softmax_prob,
+ * tau_thresh_activate).
+ *   x          : [T, d] bf16 tokens, 1 <= T <= max_tokens.
+ *   tau        : budget, >= 0 (NaN or negative: PP_EINVAL).
+ *   inv_temp   : [T] fp32 per-token inverse temperature, or NULL (= 1):
+ *                g = (W_r x + b) * inv_temp[t].
+ *   expert_idx : [T, E] int32 out; row t holds the kept experts pi_1..pi_k in
+ *                descending-logit order, then -1.
+ *   count      : [T] int32 out; k for each token.
+ *   gate_w     : [T, E] fp32 out or NULL; weight applied to the expert in the
+ *                same slot of expert_idx (sigmoid(g_e) with PP_AGG_SIGMOID,
+ *                else 1), 0 in unused slots. */
+pp_status prunepath_route(pp_layer *L, const uint16_t *x, int32_t T, float tau,
+                          const float *inv_temp, int32_t *expert_idx, int32_t *count,
+                          float *gate_w, void *hip_stream);
+
+/* prunepath_ffn_decode -- routing plus the sparse FFN output, tuned for small
+ * token batches (decode).  Batches larger than 64 tokens are processed in
+ * slices of 64.
+ *   x, T, tau, inv_temp : as for prunepath_route.
+ *   y          : [T, d] fp32 out, overwritten: sum over kept experts of
+ *                FFN_e(x) (times sigmoid(g_e) with PP_AGG_SIGMOID).
+ *   expert_idx, count   : as for prunepath_route, or both NULL to skip them. */
+pp_status prunepath_ffn_decode(pp_layer *L, const uint16_t *x, int32_t T, float tau,
+                               const float *inv_temp, float *y, int32_t *expert_idx,
+                               int32_t *count, void *hip_stream);
+
+/* prunepath_ffn_prefill -- same result as prunepath_ffn_decode (up to fp32
+ * summation order), organised for long token batches: tokens are bucketed per
+ * kept expert and each expert's bucket runs as a grouped bf16 MFMA GEMM
+ * (the multi-token dispatch described in Sec. 4.5). */
+pp_status prunepath_ffn_prefill(pp_layer *L, const uint16_t *x, int32_t T, float tau,
+                                const float *inv_temp, float *y, int32_t *expert_idx,
+                                int32_t *count, void *hip_stream);
+
+/* prunepath_destroy -- free a handle and its device memory.  NULL is a no-op.
+ * The caller must ensure no enqueued work still uses the handle. */
+void prunepath_destroy(pp_layer *L);
+
+/* prunepath_status_string -- static text for a status code (never NULL). */
+const char *prunepath_status_string(pp_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRUNEPATH_H */

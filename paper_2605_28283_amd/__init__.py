@@ -1,0 +1,10 @@
+"""PrunePath sparse-FFN forward for MI355X (gfx950).
+
+The computation runs in the HIP library libprunepath.so (C ABI in
+include/prunepath.h); this package is its thin Python binding plus the seeded
+synthetic-input generators (``workloads``).
+"""
+from ._lib import (EXPORTED, PP_AGG_SIGMOID, PP_AGG_SUM, PP_EHIP, PP_EINVAL, PP_ENOMEM,  # noqa: F401
+                   PP_EUNSUPPORTED, PP_OK, PP_SELECT_NUCLEUS, PP_SELECT_STRICT, PrunePathError,
+                   load, prunepath_create, prunepath_destroy, prunepath_ffn_decode,
+                   prunepath_ffn_prefill, prunepath_route, prunepath_status_string)

@@ -1,0 +1,150 @@
+"""ctypes binding of libprunepath.so -- argument marshalling only.
+
+Every function has the name and argument order of the C entry point declared
+in include/prunepath.h.  Array arguments may be torch tensors on the current
+HIP device (their data pointer is passed; bf16 arrays may be typed bfloat16,
+int16 or uint16) or raw integer device addresses.  A non-OK status raises
+PrunePathError.  There is no fallback: if the shared library is missing the
+import fails.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libprunepath.so")
+
+PP_OK = 0
+PP_EINVAL = 1
+PP_ENOMEM = 2
+PP_EHIP = 3
+PP_EUNSUPPORTED = 4
+
+PP_SELECT_NUCLEUS = 0
+PP_SELECT_STRICT = 1
+PP_AGG_SUM = 0
+PP_AGG_SIGMOID = 2
+
+EXPORTED = ("prunepath_create", "prunepath_route", "prunepath_ffn_decode",
+            "prunepath_ffn_prefill", "prunepath_destroy", "prunepath_status_string")
+
+
+class PrunePathError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, _status_text(status), status))
+
+
+_lib = None
+
+
+def load():
+    """Load the HIP library (raises OSError if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise OSError("libprunepath.so not built: run __graft_entry__.build() "
+                          "or python paper_2605_28283_amd/build.py")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, I32, U32, F32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_float
+        lib.prunepath_create.argtypes = [ctypes.POINTER(ctypes.c_void_p), I32, I32, I32, I32,
+                                         P, P, P, P, P, P, U32, P]
+        lib.prunepath_create.restype = ctypes.c_int
+        lib.prunepath_route.argtypes = [P, P, I32, F32, P, P, P, P, P]
+        lib.prunepath_route.restype = ctypes.c_int
+        for f in (lib.prunepath_ffn_decode, lib.prunepath_ffn_prefill):
+            f.argtypes = [P, P, I32, F32, P, P, P, P, P]
+            f.restype = ctypes.c_int
+        lib.prunepath_destroy.argtypes = [P]
+        lib.prunepath_destroy.restype = None
+        lib.prunepath_status_string.argtypes = [ctypes.c_int]
+        lib.prunepath_status_string.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def _status_text(s):
+    try:
+        return load().prunepath_status_string(int(s)).decode()
+    except OSError:
+        return "unknown"
+
+
+_BF16_LIKE = None
+
+
+def _ptr(a, kind=None):
+    """Device address of a tensor (checked) or an int; None -> NULL."""
+    if a is None:
+        return None
+    if isinstance(a, int):
+        return a
+    import torch
+    global _BF16_LIKE
+    if _BF16_LIKE is None:
+        _BF16_LIKE = {torch.bfloat16, torch.int16, torch.uint16}
+    if not a.is_cuda:
+        raise ValueError("array arguments must live on the GPU")
+    if not a.is_contiguous():
+        raise ValueError("array arguments must be contiguous")
+    want = {"bf16": _BF16_LIKE, "f32": {torch.float32}, "i32": {torch.int32}}.get(kind)
+    if want is not None and a.dtype not in want:
+        raise TypeError("expected %s array, got %s" % (kind, a.dtype))
+    return a.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(st, where):
+    if st != PP_OK:
+        raise PrunePathError(st, where)
+
+
+def prunepath_status_string(status):
+    return _status_text(status)
+
+
+def prunepath_create(d, d_ff, E, max_tokens, W_r, W_gate, W_up, W_down, perm=None,
+                     router_bias=None, flags=0, stream=None):
+    """Returns an opaque handle (int)."""
+    out = ctypes.c_void_p()
+    st = load().prunepath_create(ctypes.byref(out), d, d_ff, E, max_tokens,
+                                 _ptr(W_r, "bf16"), _ptr(W_gate, "bf16"), _ptr(W_up, "bf16"),
+                                 _ptr(W_down, "bf16"), _ptr(perm, "i32"),
+                                 _ptr(router_bias, "f32"), flags, _stream(stream))
+    _check(st, "prunepath_create")
+    return out.value
+
+
+def prunepath_route(handle, x, T, tau, inv_temp, expert_idx, count, gate_w=None, stream=None):
+    st = load().prunepath_route(handle, _ptr(x, "bf16"), T, tau, _ptr(inv_temp, "f32"),
+                                _ptr(expert_idx, "i32"), _ptr(count, "i32"),
+                                _ptr(gate_w, "f32"), _stream(stream))
+    _check(st, "prunepath_route")
+
+
+def prunepath_ffn_decode(handle, x, T, tau, inv_temp, y, expert_idx=None, count=None,
+                         stream=None):
+    st = load().prunepath_ffn_decode(handle, _ptr(x, "bf16"), T, tau, _ptr(inv_temp, "f32"),
+                                     _ptr(y, "f32"), _ptr(expert_idx, "i32"), _ptr(count, "i32"),
+                                     _stream(stream))
+    _check(st, "prunepath_ffn_decode")
+
+
+def prunepath_ffn_prefill(handle, x, T, tau, inv_temp, y, expert_idx=None, count=None,
+                          stream=None):
+    st = load().prunepath_ffn_prefill(handle, _ptr(x, "bf16"), T, tau, _ptr(inv_temp, "f32"),
+                                      _ptr(y, "f32"), _ptr(expert_idx, "i32"),
+                                      _ptr(count, "i32"), _stream(stream))
+    _check(st, "prunepath_ffn_prefill")
+
+
+def prunepath_destroy(handle):
+    if handle:
+        load().prunepath_destroy(handle)

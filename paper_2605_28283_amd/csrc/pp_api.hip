@@ -1,0 +1,214 @@
+// C ABI entry points (include/prunepath.h): argument validation, ownership of
+// the repacked weights and scratch, and the launch sequence of each call on
+// the caller's stream.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "pp_internal.h"
+
+namespace {
+
+using namespace pp;
+
+constexpr int kMaxTokensLimit = 65536;
+
+template <typename T>
+hipError_t dev_alloc(T **p, size_t elems) {
+    *p = nullptr;
+    if (elems == 0) elems = 1;
+    return hipMalloc(reinterpret_cast<void **>(p), elems * sizeof(T));
+}
+
+void free_layer(pp_layer *L) {
+    if (!L) return;
+    void *bufs[] = {L->Wr,     L->bias,  L->Wgu,     L->Wd,    L->gpart, L->counters,
+                    L->selmask, L->gsig, L->idx_tmp, L->cnt_tmp, L->abpart, L->h_hi,
+                    L->h_lo,   L->ypart, L->ecount,  L->tokl};
+    for (void *b : bufs)
+        if (b) (void)hipFree(b);
+    delete L;
+}
+
+size_t gpart_capacity(const pp_dims &dm, int max_tokens) {
+    size_t best = 0;
+    for (int T = 1; T <= max_tokens; ++T) {
+        const size_t need = (size_t)route_split(dm, T) * T * dm.E;
+        if (need > best) best = need;
+    }
+    return best;
+}
+
+bool valid_tau(float tau) { return !isnan(tau) && tau >= 0.0f; }
+
+pp_status check_call(const pp_layer *L, const uint16_t *x, int32_t T, float tau) {
+    if (!L || !x) return PP_EINVAL;
+    if (T < 1 || T > L->max_tokens) return PP_EINVAL;
+    if (!valid_tau(tau)) return PP_EINVAL;
+    return PP_OK;
+}
+
+pp_status hip_status(hipError_t e) {
+    if (e == hipSuccess) return PP_OK;
+    if (e == hipErrorOutOfMemory) return PP_ENOMEM;
+    return PP_EHIP;
+}
+
+pp_status run_ffn(pp_layer *L, const uint16_t *x, int32_t T, float tau, const float *inv_temp,
+                  float *y, int32_t *expert_idx, int32_t *count, void *hip_stream, bool prefill) {
+    pp_status st = check_call(L, x, T, tau);
+    if (st != PP_OK) return st;
+    if (!y || ((expert_idx == nullptr) != (count == nullptr))) return PP_EINVAL;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    const int E = L->dm.E, d = L->dm.d;
+    const int slice = prefill ? T : kDecodeTile;
+    for (int t0 = 0; t0 < T; t0 += slice) {
+        const int n = (T - t0 < slice) ? T - t0 : slice;
+        int32_t *idx = expert_idx ? expert_idx + (size_t)t0 * E : L->idx_tmp;
+        int32_t *cnt = count ? count + t0 : L->cnt_tmp;
+        const uint16_t *xs = x + (size_t)t0 * d;
+        float *ys = y + (size_t)t0 * d;
+        const float *it = inv_temp ? inv_temp + t0 : nullptr;
+        hipError_t e = launch_route(L, xs, n, tau, it, idx, cnt, nullptr, s);
+        if (e == hipSuccess)
+            e = prefill ? launch_prefill_ffn(L, xs, n, ys, s) : launch_decode_ffn(L, xs, n, ys, s);
+        if (e != hipSuccess) return hip_status(e);
+    }
+    return PP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
+                           int32_t max_tokens, const uint16_t *W_r, const uint16_t *W_gate,
+                           const uint16_t *W_up, const uint16_t *W_down, const int32_t *perm,
+                           const float *router_bias, uint32_t flags, void *hip_stream) {
+    if (!out) return PP_EINVAL;
+    *out = nullptr;
+    if (!W_r || !W_gate || !W_up || !W_down) return PP_EINVAL;
+    if (d < 1 || d_ff < 1 || E < 1 || max_tokens < 1 || max_tokens > kMaxTokensLimit)
+        return PP_EINVAL;
+    if (flags & ~(PP_SELECT_STRICT | PP_AGG_SIGMOID)) return PP_EINVAL;
+    if (d_ff % E != 0) return PP_EINVAL;
+    if (E > kMaxExperts) return PP_EUNSUPPORTED;
+    if (d_ff / E != kExpertWidth) return PP_EUNSUPPORTED;
+    if (d % 64 != 0) return PP_EUNSUPPORTED;
+
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    if (perm) {
+        std::vector<int32_t> hp((size_t)d_ff);
+        if (hipMemcpy(hp.data(), perm, sizeof(int32_t) * d_ff, hipMemcpyDeviceToHost) !=
+            hipSuccess)
+            return PP_EHIP;
+        std::vector<unsigned char> seen((size_t)d_ff, 0);
+        for (int32_t v : hp) {
+            if (v < 0 || v >= d_ff || seen[v]) return PP_EINVAL;
+            seen[v] = 1;
+        }
+    }
+
+    pp_layer *L = new (std::nothrow) pp_layer;
+    if (!L) return PP_ENOMEM;
+    memset(L, 0, sizeof *L);
+    L->dm.d = d;
+    L->dm.d_ff = d_ff;
+    L->dm.E = E;
+    L->dm.NS = d / kKStep;
+    L->max_tokens = max_tokens;
+    L->flags = flags;
+    hipError_t e = hipGetDevice(&L->device);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&L->num_cu, hipDeviceAttributeMultiprocessorCount, L->device);
+    if (e != hipSuccess) {
+        free_layer(L);
+        return PP_EHIP;
+    }
+
+    const size_t dE = (size_t)d * E;
+    const counter_layout cl = counters_for(L->dm, max_tokens);
+    L->gpart_elems = gpart_capacity(L->dm, max_tokens);
+    L->n_counters = cl.total;
+    L->max_pairs = (size_t)max_tokens * E;
+    const int min_rb = d / 256 > 0 ? d / 256 : 1;
+    L->ypart_elems = (size_t)((kUnitTarget + min_rb - 1) / min_rb + 1) * kDecodeTile * d;
+
+    hipError_t a = hipSuccess;
+    auto chk = [&](hipError_t r) {
+        if (a == hipSuccess) a = r;
+    };
+    chk(dev_alloc(&L->Wr, dE));
+    chk(dev_alloc(&L->bias, (size_t)E));
+    chk(dev_alloc(&L->Wgu, (size_t)2 * d_ff * d));
+    chk(dev_alloc(&L->Wd, (size_t)d_ff * d));
+    chk(dev_alloc(&L->gpart, L->gpart_elems));
+    chk(dev_alloc(&L->counters, L->n_counters));
+    chk(dev_alloc(&L->selmask, (size_t)max_tokens * 8));
+    chk(dev_alloc(&L->gsig, (size_t)max_tokens * E));
+    chk(dev_alloc(&L->idx_tmp, (size_t)max_tokens * E));
+    chk(dev_alloc(&L->cnt_tmp, (size_t)max_tokens));
+    chk(dev_alloc(&L->abpart, kAbPartRows * 256));
+    chk(dev_alloc(&L->h_hi, L->max_pairs * kExpertWidth));
+    chk(dev_alloc(&L->h_lo, L->max_pairs * kExpertWidth));
+    chk(dev_alloc(&L->ypart, L->ypart_elems));
+    chk(dev_alloc(&L->ecount, (size_t)E));
+    chk(dev_alloc(&L->tokl, (size_t)E * max_tokens));
+    if (a != hipSuccess) {
+        free_layer(L);
+        return hip_status(a);
+    }
+    chk(hipMemcpyAsync(L->Wr, W_r, dE * sizeof(uint16_t), hipMemcpyDeviceToDevice, s));
+    if (router_bias)
+        chk(hipMemcpyAsync(L->bias, router_bias, sizeof(float) * E, hipMemcpyDeviceToDevice, s));
+    else
+        chk(hipMemsetAsync(L->bias, 0, sizeof(float) * E, s));
+    chk(hipMemsetAsync(L->counters, 0, sizeof(uint32_t) * L->n_counters, s));
+    if (a == hipSuccess) a = launch_repack(L, W_gate, W_up, W_down, perm, s);
+    chk(hipStreamSynchronize(s));
+    if (a != hipSuccess) {
+        free_layer(L);
+        return hip_status(a);
+    }
+    *out = L;
+    return PP_OK;
+}
+
+pp_status prunepath_route(pp_layer *L, const uint16_t *x, int32_t T, float tau,
+                          const float *inv_temp, int32_t *expert_idx, int32_t *count,
+                          float *gate_w, void *hip_stream) {
+    pp_status st = check_call(L, x, T, tau);
+    if (st != PP_OK) return st;
+    if (!expert_idx || !count) return PP_EINVAL;
+    return hip_status(launch_route(L, x, T, tau, inv_temp, expert_idx, count, gate_w,
+                                   static_cast<hipStream_t>(hip_stream)));
+}
+
+pp_status prunepath_ffn_decode(pp_layer *L, const uint16_t *x, int32_t T, float tau,
+                               const float *inv_temp, float *y, int32_t *expert_idx,
+                               int32_t *count, void *hip_stream) {
+    return run_ffn(L, x, T, tau, inv_temp, y, expert_idx, count, hip_stream, false);
+}
+
+pp_status prunepath_ffn_prefill(pp_layer *L, const uint16_t *x, int32_t T, float tau,
+                                const float *inv_temp, float *y, int32_t *expert_idx,
+                                int32_t *count, void *hip_stream) {
+    return run_ffn(L, x, T, tau, inv_temp, y, expert_idx, count, hip_stream, true);
+}
+
+void prunepath_destroy(pp_layer *L) { free_layer(L); }
+
+const char *prunepath_status_string(pp_status s) {
+    switch (s) {
+    case PP_OK: return "ok";
+    case PP_EINVAL: return "invalid argument";
+    case PP_ENOMEM: return "out of device memory";
+    case PP_EHIP: return "HIP runtime error";
+    case PP_EUNSUPPORTED: return "unsupported shape";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

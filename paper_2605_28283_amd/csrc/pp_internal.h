@@ -1,0 +1,146 @@
+// Internal declarations of the gfx950 PrunePath library: the layer handle,
+// kernel parameter blocks, launchers and small device helpers shared by the
+// kernel files.  Nothing here is part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/prunepath.h"
+
+namespace pp {
+
+constexpr int kExpertWidth = 128;      // neurons per expert (de)
+constexpr int kKStep = 32;             // K per bf16 MFMA 16x16x32
+constexpr int kMaxExperts = 256;
+constexpr int kDecodeTile = 64;        // tokens per decode slice (one u64 token mask)
+constexpr int kRouteTile = 16;         // tokens / experts per router MFMA tile
+constexpr int kGroupTokens = 64;       // tokens per prefill expert group
+constexpr int kUnitTarget = 512;       // work units a persistent grid aims for
+
+// Byte sizes of the scratch areas whose size does not follow from max_tokens.
+constexpr size_t kAbPartRows = 65536;  // K-split partial (a,b) rows of 256 floats
+
+struct pp_dims {
+    int d, d_ff, E, NS;      // NS = d / 32 K-steps
+};
+
+}  // namespace pp
+
+struct pp_layer {
+    pp::pp_dims dm;
+    int max_tokens;
+    uint32_t flags;
+    int device;
+    int num_cu;
+    // library-owned weights
+    uint16_t *Wr;      // [E][d] bf16
+    float *bias;       // [E] fp32 (zeros when the caller gave none)
+    uint16_t *Wgu;     // expert-major gate/up MFMA fragments
+    uint16_t *Wd;      // expert-major down MFMA fragments
+    // scratch
+    float *gpart;       // router K-split partial logits [KSr][T][E]
+    size_t gpart_elems;
+    uint32_t *counters; // arrival counters, zero between calls
+    size_t n_counters;
+    uint32_t *selmask;  // [max_tokens][8] kept-expert bitmask per token
+    float *gsig;        // [max_tokens][E] expert scale (sigmoid(g) or 1)
+    int32_t *idx_tmp;   // [max_tokens][E] used when the caller passes no expert_idx
+    int32_t *cnt_tmp;   // [max_tokens]
+    float *abpart;      // [kAbPartRows][256] K-split partial gate/up outputs
+    uint16_t *h_hi;     // [pairs][128] bf16 high part of h
+    uint16_t *h_lo;     // [pairs][128] bf16 low part of h (h - hi)
+    size_t max_pairs;
+    float *ypart;       // [ypart_elems] expert-split partial outputs (decode)
+    size_t ypart_elems;
+    int32_t *ecount;    // [E] tokens per expert (prefill)
+    int32_t *tokl;      // [E][max_tokens] token ids per expert (prefill)
+};
+
+namespace pp {
+
+// Counter regions inside pp_layer::counters.
+struct counter_layout {
+    size_t route;   // ceil(max_tokens/16)
+    size_t gateup;  // one per expert group
+    size_t down;    // one per row block
+    size_t total;
+};
+counter_layout counters_for(const pp_dims &dm, int max_tokens);
+
+int route_split(const pp_dims &dm, int T);  // router K-split factor for T tokens
+
+hipError_t launch_repack(pp_layer *L, const uint16_t *W_gate, const uint16_t *W_up,
+                         const uint16_t *W_down, const int32_t *perm, hipStream_t s);
+hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const float *inv_temp,
+                        int32_t *idx, int32_t *count, float *gate_w, hipStream_t s);
+hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
+hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
+
+// ---------------------------------------------------------------- device helpers
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+    return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// Round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ f32x4 mfma16(uint4 a, uint4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint4 ldg16(const void *p) {
+    return *reinterpret_cast<const uint4 *>(p);
+}
+
+__device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
+
+// Inclusive scan of one int per lane across a 64-lane wavefront.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        int n = __shfl_up(v, o, 64);
+        if (lane >= o) v += n;
+    }
+    return v;
+}
+
+// Exclusive scan over a block of nthreads (multiple of 64, <= 1024) for two
+// ints at once.  `sm` needs 2 * (nthreads/64) ints of shared memory.  Returns
+// the exclusive prefixes; totals are written to *tot0 / *tot1 for every thread.
+__device__ __forceinline__ void block_excl_scan2(int v0, int v1, int *e0, int *e1, int *tot0,
+                                                 int *tot1, int *sm) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    int i0 = wave_incl_scan(v0), i1 = wave_incl_scan(v1);
+    if (lane == 63) {
+        sm[wv] = i0;
+        sm[nw + wv] = i1;
+    }
+    __syncthreads();
+    int b0 = 0, b1 = 0, t0 = 0, t1 = 0;
+    for (int w = 0; w < nw; ++w) {
+        if (w < wv) {
+            b0 += sm[w];
+            b1 += sm[nw + w];
+        }
+        t0 += sm[w];
+        t1 += sm[nw + w];
+    }
+    *e0 = b0 + i0 - v0;
+    *e1 = b1 + i1 - v1;
+    *tot0 = t0;
+    *tot1 = t1;
+    __syncthreads();
+}
+
+}  // namespace pp

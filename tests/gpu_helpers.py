@@ -1,0 +1,107 @@
+"""Helpers shared by the GPU parity tests: upload seeded layers, run the HIP
+entry points through the binding, and compare against the oracle."""
+import numpy as np
+
+import paper_2605_28283_amd as pp
+
+TOL = 1e-2          # max |y - y_ref| <= TOL * RMS(y_ref)  (global RMS of the call)
+TIE_BAND = 1e-5     # cumulative-mass / logit band treated as a tie
+
+
+def torch():
+    import torch as _t
+    return _t
+
+
+def to_dev(bits):
+    t = torch()
+    return t.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+
+
+class DevLayer:
+    def __init__(self, L, max_tokens, flags=0):
+        t = torch()
+        self.L = L
+        self.flags = flags
+        self.E, self.d = L.E, L.d
+        self.W = [to_dev(a) for a in (L.W_r, L.W_gate, L.W_up, L.W_down)]
+        self.perm = None if L.perm is None else t.from_numpy(L.perm).cuda()
+        self.bias = None if L.bias is None else t.from_numpy(L.bias).cuda()
+        self.h = pp.prunepath_create(L.d, L.d_ff, L.E, max_tokens, *self.W, perm=self.perm,
+                                     router_bias=self.bias, flags=flags)
+
+    def close(self):
+        if self.h:
+            pp.prunepath_destroy(self.h)
+            self.h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def run(self, mode, x_bits, tau, inv_temp=None):
+        """mode: 'decode' | 'prefill' | 'route'.  Returns numpy (idx, count, y or gate_w)."""
+        t = torch()
+        T = x_bits.shape[0]
+        x = to_dev(x_bits)
+        it = None if inv_temp is None else t.from_numpy(inv_temp).cuda()
+        idx = t.full((T, self.E), -7, dtype=t.int32, device="cuda")
+        cnt = t.full((T,), -7, dtype=t.int32, device="cuda")
+        if mode == "route":
+            gw = t.full((T, self.E), -7.0, dtype=t.float32, device="cuda")
+            pp.prunepath_route(self.h, x, T, tau, it, idx, cnt, gw)
+            t.cuda.synchronize()
+            return idx.cpu().numpy(), cnt.cpu().numpy(), gw.cpu().numpy()
+        y = t.full((T, self.d), float("nan"), dtype=t.float32, device="cuda")
+        fn = pp.prunepath_ffn_decode if mode == "decode" else pp.prunepath_ffn_prefill
+        fn(self.h, x, T, tau, it, y, idx, cnt)
+        t.cuda.synchronize()
+        return idx.cpu().numpy(), cnt.cpu().numpy(), y.cpu().numpy()
+
+
+def check_selection(oracle, L, x, tau, flags, idx_g, cnt_g, inv_temp=None):
+    """Bit-exact selections except tokens whose cumulative mass (or logit order
+    at the cut) lies within TIE_BAND; those are counted and their GPU result
+    is checked for validity.  Returns (oracle route dict, exempt mask)."""
+    r = oracle.route(x, L.W_r, tau, flags=flags, bias=L.bias, inv_temp=inv_temp)
+    sel_flags = flags & oracle.SELECT_STRICT
+    exempt = oracle.near_tie(r["cum"], tau, TIE_BAND, flags=sel_flags) | \
+        oracle.order_tie(r["g"], r["idx"], r["count"], TIE_BAND)
+    T, E = idx_g.shape
+    bad = []
+    for t in range(T):
+        k = int(cnt_g[t])
+        assert 1 <= k <= E, (t, k)
+        kept = idx_g[t, :k]
+        assert len(set(kept.tolist())) == k and (kept >= 0).all() and (kept < E).all(), t
+        assert (idx_g[t, k:] == -1).all(), t
+        if exempt[t]:
+            assert abs(k - int(r["count"][t])) <= 1, (t, k, r["count"][t])
+            continue
+        if k != r["count"][t] or not (kept == r["idx"][t, :k]).all():
+            bad.append(t)
+    assert not bad, "selection mismatch at tokens %s (tau=%g)" % (bad[:10], tau)
+    return r, exempt
+
+
+def check_output(oracle, L, x, flags, idx_g, cnt_g, y_g, g_ref, rows=None):
+    """y against the oracle evaluated on the GPU's own selection."""
+    if rows is None:
+        rows = np.arange(x.shape[0])
+    y_ref = oracle.ffn(x[rows], L.W_gate, L.W_up, L.W_down, idx_g[rows], cnt_g[rows],
+                       flags=flags, g=g_ref[rows], perm=L.perm)
+    err = np.abs(y_g[rows].astype(np.float64) - y_ref)
+    rms = float(np.sqrt(np.mean(y_ref ** 2)))
+    assert np.isfinite(y_g[rows]).all()
+    worst = float(err.max()) / rms
+    assert worst <= TOL, "max|dy|/RMS = %.3g" % worst
+    return worst
+
+
+def parity(oracle, dl, mode, x, tau, inv_temp=None, rows=None):
+    idx, cnt, y = dl.run(mode, x, tau, inv_temp)
+    r, exempt = check_selection(oracle, dl.L, x, tau, dl.flags, idx, cnt, inv_temp)
+    worst = check_output(oracle, dl.L, x, dl.flags, idx, cnt, y, r["g"], rows)
+    return dict(idx=idx, cnt=cnt, y=y, exempt=int(exempt.sum()), worst=worst)

@@ -1,0 +1,93 @@
+"""CPU-side checks of the C ABI: the library loads, exports every entry point
+declared in include/prunepath.h, and rejects bad arguments on the host before
+touching the GPU (these calls return before any HIP runtime call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2605_28283_amd as pp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "prunepath.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(prunepath_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_five_calls():
+    syms = declared_symbols()
+    for s in ("prunepath_create", "prunepath_route", "prunepath_ffn_decode",
+              "prunepath_ffn_prefill", "prunepath_destroy"):
+        assert s in syms
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pp.load()
+    for s in declared_symbols():
+        assert hasattr(lib, s), s
+    # and the binding exposes the same names
+    for s in declared_symbols():
+        assert callable(getattr(pp, s)), s
+    assert sorted(pp.EXPORTED) == declared_symbols()
+
+
+def test_status_strings():
+    for code, text in ((pp.PP_OK, "ok"), (pp.PP_EINVAL, "invalid argument"),
+                       (pp.PP_EUNSUPPORTED, "unsupported shape")):
+        assert pp.prunepath_status_string(code) == text
+    assert pp.prunepath_status_string(99) == "unknown status"
+
+
+def _create(**kw):
+    lib = pp.load()
+    a = dict(d=512, d_ff=2048, E=16, max_tokens=8, W_r=8, W_gate=8, W_up=8, W_down=8, perm=None,
+             bias=None, flags=0)
+    a.update(kw)
+    out = ctypes.c_void_p(1234)
+    st = lib.prunepath_create(ctypes.byref(out), a["d"], a["d_ff"], a["E"], a["max_tokens"],
+                              a["W_r"], a["W_gate"], a["W_up"], a["W_down"], a["perm"], a["bias"],
+                              a["flags"], None)
+    return st, out.value
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(W_r=None), pp.PP_EINVAL),
+    (dict(W_down=None), pp.PP_EINVAL),
+    (dict(d=0), pp.PP_EINVAL),
+    (dict(max_tokens=0), pp.PP_EINVAL),
+    (dict(max_tokens=70000), pp.PP_EINVAL),
+    (dict(flags=4), pp.PP_EINVAL),
+    (dict(d_ff=2050), pp.PP_EINVAL),
+    (dict(d_ff=4096), pp.PP_EUNSUPPORTED),        # experts of 256 neurons
+    (dict(E=512, d_ff=512 * 128), pp.PP_EUNSUPPORTED),
+    (dict(d=520), pp.PP_EUNSUPPORTED),            # d not a multiple of 64
+])
+def test_create_rejects_bad_arguments(kw, expect):
+    st, h = _create(**kw)
+    assert st == expect
+    assert h is None or h == 0
+
+
+def test_create_null_out():
+    lib = pp.load()
+    assert lib.prunepath_create(None, 512, 2048, 16, 8, 8, 8, 8, 8, None, None, 0, None) == \
+        pp.PP_EINVAL
+
+
+def test_calls_reject_null_handle():
+    lib = pp.load()
+    assert lib.prunepath_route(None, 8, 1, 0.5, None, 8, 8, None, None) == pp.PP_EINVAL
+    assert lib.prunepath_ffn_decode(None, 8, 1, 0.5, None, 8, None, None, None) == pp.PP_EINVAL
+    assert lib.prunepath_ffn_prefill(None, 8, 1, 0.5, None, 8, None, None, None) == pp.PP_EINVAL
+    lib.prunepath_destroy(None)  # NULL-safe
+
+
+def test_binding_raises_on_error():
+    with pytest.raises(pp.PrunePathError) as ei:
+        pp.prunepath_route(0, 8, 1, 0.5, None, 8, 8, stream=0)
+    assert ei.value.status == pp.PP_EINVAL

@@ -1,0 +1,204 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Selections must match bit for bit except tokens whose cumulative mass (or
+logit order at the cut) lies within 1e-5 (counted, checked for validity);
+y must satisfy max|y - y_ref| <= 1e-2 * RMS(y_ref), y_ref evaluated by the
+oracle on the GPU's own selection.
+"""
+import numpy as np
+import pytest
+
+import paper_2605_28283_amd as pp
+from paper_2605_28283_amd.workloads import (WORKLOADS, make_layer, make_tokens, workload_layer,
+                                            workload_tokens)
+from gpu_helpers import DevLayer, check_output, check_selection, parity, to_dev
+
+pytestmark = pytest.mark.gpu
+
+NUC, STRICT, SUM, SIG = pp.PP_SELECT_NUCLEUS, pp.PP_SELECT_STRICT, pp.PP_AGG_SUM, pp.PP_AGG_SIGMOID
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    pp.load()
+    torch.cuda.init()
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    w = WORKLOADS["tiny"]
+    return workload_layer(w, 0), w
+
+
+@pytest.mark.parametrize("flags", [NUC | SUM, NUC | SIG, STRICT | SUM, STRICT | SIG])
+@pytest.mark.parametrize("mode", ["decode", "prefill"])
+def test_tiny_workload(oracle_mod, tiny, flags, mode):
+    L, w = tiny
+    x, _ = workload_tokens(w, 4, 0)
+    with DevLayer(L, 64, flags) as dl:
+        for tau in (0.9, 0.0, 0.3, 0.5, 0.7, 1.0, 1.05):
+            parity(oracle_mod, dl, mode, x, tau)
+
+
+@pytest.mark.parametrize("T", [1, 5, 17, 37, 63, 64, 65, 130])
+@pytest.mark.parametrize("mode", ["decode", "prefill"])
+def test_ragged_batches(oracle_mod, tiny, T, mode):
+    L, _ = tiny
+    x, _ = make_tokens(T, L.d, 100 + T)
+    with DevLayer(L, 256) as dl:
+        for tau in (0.5, 0.9, 1.0):
+            parity(oracle_mod, dl, mode, x, tau)
+
+
+def test_route_entry_point(oracle_mod):
+    L = make_layer(512, 2048, 16, 7, skewed=True)
+    x, it = make_tokens(23, 512, 8, temperature=True)
+    for flags in (NUC | SUM, STRICT | SIG):
+        with DevLayer(L, 32, flags) as dl:
+            idx, cnt, gw = dl.run("route", x, 0.8, it)
+            r, _ = check_selection(oracle_mod, L, x, 0.8, flags, idx, cnt, it)
+            for t in range(x.shape[0]):
+                k = cnt[t]
+                if flags & SIG:
+                    exp = 1.0 / (1.0 + np.exp(-r["g"][t, idx[t, :k]]))
+                    np.testing.assert_allclose(gw[t, :k], exp, rtol=1e-5, atol=1e-6)
+                else:
+                    assert (gw[t, :k] == 1.0).all()
+                assert (gw[t, k:] == 0.0).all()
+
+
+@pytest.mark.parametrize("mode", ["decode", "prefill"])
+def test_permuted_skewed_medium(oracle_mod, mode):
+    """Neuron permutation (Eq. permuted_weights), router bias and temperature,
+    several expert tiles (E=24) and a width spanning many K-steps."""
+    L = make_layer(1024, 24 * 128, 24, 9, skewed=True, perm=True)
+    x, it = make_tokens(50, 1024, 10, temperature=True)
+    for flags in (NUC | SUM, STRICT | SIG):
+        with DevLayer(L, 64, flags) as dl:
+            for tau in (0.5, 0.9, 1.0):
+                parity(oracle_mod, dl, mode, x, tau, it)
+
+
+def test_single_and_max_experts(oracle_mod):
+    for E, d, T in ((1, 128, 9), (256, 64, 12), (200, 128, 70)):
+        L = make_layer(d, 128 * E, E, 11 + E)
+        x, _ = make_tokens(T, d, 12 + E)
+        with DevLayer(L, 128) as dl:
+            for mode in ("decode", "prefill"):
+                for tau in (0.3, 0.9, 1.0):
+                    res = parity(oracle_mod, dl, mode, x, tau)
+                    if E == 1:
+                        assert (res["cnt"] == 1).all()
+
+
+def test_tau_edges_and_counts(oracle_mod, tiny):
+    L, _ = tiny
+    x, _ = make_tokens(20, L.d, 13)
+    with DevLayer(L, 32) as dl:
+        _, c0, _ = dl.run("decode", x, 0.0)
+        assert (c0 == 1).all()
+        _, c1, _ = dl.run("decode", x, 1.0)
+        assert (c1 == L.E).all()
+        _, c2, _ = dl.run("decode", x, 1.05)
+        assert (c2 == L.E).all()
+        prev = None
+        for tau in np.linspace(0, 1, 21):
+            _, c, _ = dl.run("route", x, float(tau))
+            if prev is not None:
+                assert (c >= prev).all()
+            prev = c
+    with DevLayer(L, 32, STRICT) as dl:
+        _, c, _ = dl.run("decode", x, 1.05)
+        assert (c == L.E).all()
+        _, c, _ = dl.run("decode", x, 0.0)
+        assert (c == 1).all()
+
+
+def test_invalid_calls_leave_outputs_untouched(tiny):
+    import torch
+    L, _ = tiny
+    x, _ = make_tokens(4, L.d, 14)
+    with DevLayer(L, 8) as dl:
+        xd = to_dev(x)
+        y = torch.full((4, L.d), 3.0, device="cuda")
+        idx = torch.full((4, L.E), 5, dtype=torch.int32, device="cuda")
+        cnt = torch.full((4,), 5, dtype=torch.int32, device="cuda")
+        for T, tau in ((0, 0.5), (9, 0.5), (4, float("nan")), (4, -0.1)):
+            for fn in (pp.prunepath_ffn_decode, pp.prunepath_ffn_prefill):
+                with pytest.raises(pp.PrunePathError) as ei:
+                    fn(dl.h, xd, T, tau, None, y, idx, cnt)
+                assert ei.value.status == pp.PP_EINVAL
+        with pytest.raises(pp.PrunePathError):
+            pp.prunepath_ffn_decode(dl.h, xd, 4, 0.5, None, y, idx, None)
+        torch.cuda.synchronize()
+        assert (y == 3.0).all() and (idx == 5).all() and (cnt == 5).all()
+    bad_perm = torch.zeros(L.d_ff, dtype=torch.int32, device="cuda")
+    W = [to_dev(a) for a in (L.W_r, L.W_gate, L.W_up, L.W_down)]
+    with pytest.raises(pp.PrunePathError) as ei:
+        pp.prunepath_create(L.d, L.d_ff, L.E, 8, *W, perm=bad_perm)
+    assert ei.value.status == pp.PP_EINVAL
+
+
+def test_decode_deterministic_and_matches_prefill(tiny):
+    L, _ = tiny
+    x, _ = make_tokens(48, L.d, 15)
+    with DevLayer(L, 64, STRICT | SIG) as dl:
+        a = dl.run("decode", x, 0.8)
+        b = dl.run("decode", x, 0.8)
+        c = dl.run("prefill", x, 0.8)
+    for u, v in zip(a, b):
+        np.testing.assert_array_equal(u, v)
+    np.testing.assert_array_equal(a[0], c[0])
+    np.testing.assert_array_equal(a[1], c[1])
+    rms = np.sqrt(np.mean(a[2].astype(np.float64) ** 2))
+    assert np.abs(a[2] - c[2]).max() <= 1e-4 * rms
+
+
+# ------------------------------------------------------------------ full-size workloads
+
+@pytest.fixture(scope="module")
+def llama8b():
+    w = WORKLOADS["llama8b_decode"]
+    L = workload_layer(w, 0)
+    dl = DevLayer(L, 2048)
+    yield L, w, dl
+    dl.close()
+
+
+@pytest.mark.parametrize("T", [1, 8, 32, 64])
+def test_llama8b_decode_sweep(oracle_mod, llama8b, T):
+    """Full LLaMA-3-8B FFN shape, the decode launch configuration the benchmark
+    times: every token's selection, y on sampled tokens."""
+    L, w, dl = llama8b
+    x, _ = workload_tokens(w, 64, 0)
+    x = x[:T]
+    rows = np.unique(np.linspace(0, T - 1, min(T, 4)).astype(int))
+    for tau in w.taus:
+        parity(oracle_mod, dl, "decode", x, tau, rows=rows)
+
+
+def test_llama8b_prefill(oracle_mod, llama8b):
+    L, _, dl = llama8b
+    w = WORKLOADS["llama8b_prefill"]
+    x, _ = workload_tokens(w, 2048, 0)
+    rows = np.arange(0, 2048, 97)
+    for tau in w.taus:
+        res = parity(oracle_mod, dl, "prefill", x, tau, rows=rows)
+        # decode path on the same tokens agrees with prefill everywhere
+        idx, cnt, y = dl.run("decode", x, tau)
+        np.testing.assert_array_equal(idx, res["idx"])
+        rms = np.sqrt(np.mean(res["y"].astype(np.float64) ** 2))
+        assert np.abs(y - res["y"]).max() <= 1e-3 * rms
+
+
+def test_qwen_skewed(oracle_mod):
+    w = WORKLOADS["qwen7b_skewed"]
+    L = workload_layer(w, 0)
+    x, it = workload_tokens(w, 64, 0)
+    with DevLayer(L, 64) as dl:
+        for tau in w.taus:
+            res = parity(oracle_mod, dl, "decode", x, tau, it, rows=np.array([0, 21, 42, 63]))
+            assert res["cnt"].min() >= 1
