@@ -15,6 +15,7 @@ constexpr int kKStep = 32;             // K per bf16 MFMA 16x16x32
 constexpr int kMaxExperts = 256;
 constexpr int kDecodeTile = 64;        // tokens per decode slice (one u64 token mask)
 constexpr int kRouteTile = 16;         // tokens / experts per router MFMA tile
+constexpr int kRouteSliceSteps = 16;   // K-steps per router K-slice (fixed: batch invariance)
 constexpr int kGroupTokens = 64;       // tokens per prefill expert group
 constexpr int kUnitTarget = 512;       // work units a persistent grid aims for
 

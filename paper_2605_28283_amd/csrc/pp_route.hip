@@ -2,7 +2,7 @@
 // order pi, the cumulative mass C and the tau cut of Eq. (tau_thresh_activate).
 //
 // Grid: one workgroup (4 wavefronts) per (16-token tile, 16-expert tile,
-// K-slice).  Each wavefront accumulates a 16x16 logit tile with bf16 MFMA over
+// K-slice of 16 K-steps = 512 columns of d).  Each wavefront accumulates a 16x16 logit tile with bf16 MFMA over
 // every fourth 32-wide K-step of the slice; the four tiles are summed in a
 // fixed order and the slice's partial logits are stored.  The workgroup that
 // completes a token tile last (arrival counter; release/acquire fences make
@@ -233,14 +233,12 @@ __global__ __launch_bounds__(256) void route_k(RouteParams P) {
 
 }  // namespace
 
+// The K-slices depend on d only, never on T, so a token's logits are summed
+// in the same order whatever batch it arrives in (routing is batch-invariant:
+// decode slices and one large prefill batch select identically).
 int route_split(const pp_dims &dm, int T) {
-    const int nTt = (T + kRouteTile - 1) / kRouteTile;
-    const int nEt = (dm.E + kRouteTile - 1) / kRouteTile;
-    const int base = nTt * nEt;
-    int ks = (256 + base - 1) / base;
-    int maxks = dm.NS / 4;
-    if (maxks < 1) maxks = 1;
-    if (ks > maxks) ks = maxks;
+    (void)T;
+    const int ks = (dm.NS + kRouteSliceSteps - 1) / kRouteSliceSteps;
     return ks < 1 ? 1 : ks;
 }
 

@@ -142,6 +142,20 @@ def test_invalid_calls_leave_outputs_untouched(tiny):
     assert ei.value.status == pp.PP_EINVAL
 
 
+def test_routing_is_batch_invariant(oracle_mod):
+    """A token's selection does not depend on the batch it is routed in."""
+    L = make_layer(1024, 24 * 128, 24, 17)
+    x, _ = make_tokens(70, 1024, 18)
+    with DevLayer(L, 128) as dl:
+        full = dl.run("route", x, 0.8)
+        for t in (0, 13, 69):
+            one = dl.run("route", x[t:t + 1], 0.8)
+            np.testing.assert_array_equal(one[0][0], full[0][t])
+            assert one[1][0] == full[1][t]
+        part = dl.run("route", x[5:40], 0.8)
+        np.testing.assert_array_equal(part[0], full[0][5:40])
+
+
 def test_decode_deterministic_and_matches_prefill(tiny):
     L, _ = tiny
     x, _ = make_tokens(48, L.d, 15)
