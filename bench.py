@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Benchmark of the PrunePath sparse-FFN forward on one MI355X.
+
+Workload: one LLaMA-3-8B-shaped SwiGLU FFN layer (d=4096, d_ff=14336, E=112
+experts of 128 neurons), decode batches T in {1, 8, 32, 64}, budget tau in
+{0.5, 0.7, 0.9, 1.0}; synthetic seeded bf16 weights (N(0, 0.02^2), router
+N(0, (3/sqrt(d))^2)) and tokens (N(0,1)).  A step is one call of
+prunepath_ffn_decode: routing + gate/up + down for one batch, inputs resident
+in HBM.  Steps rotate over several independent layer copies (> 2 GiB in
+total) so that the 256 MB Infinity Cache cannot hold the weights.
+
+Headline value: tokens/s/layer at the point selected by --T/--tau.  Each sweep
+point also reports effective HBM GB/s on algorithmic bytes (router weights +
+batch-union expert blocks + x + fp32 y) and its fraction of the 8 TB/s peak.
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gateup_llama8b_decode_traffic.json")
+
+
+def parse_args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--T", type=int, default=32, help="headline decode batch")
+    ap.add_argument("--tau", type=float, default=0.7, help="headline budget")
+    ap.add_argument("--sweep", default="full", choices=["full", "headline"],
+                    help="time every (T, tau) point or only the headline one")
+    ap.add_argument("--copies", type=int, default=0, help="layer copies (0 = enough for 2.2 GB)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target duration of the CPU-oracle baseline (0 = skip)")
+    return ap.parse_args()
+
+
+def source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2605_28283_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def device_layer(torch, d, d_ff, E, seed):
+    """Another layer of the same distributions, drawn on the GPU."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+
+    def draw(shape, std):
+        return (torch.randn(shape, generator=g, device="cuda", dtype=torch.float32) * std).to(
+            torch.bfloat16)
+
+    return [draw((E, d), 3.0 / math.sqrt(d)), draw((d_ff, d), 0.02), draw((d_ff, d), 0.02),
+            draw((d, d_ff), 0.02)]
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)." % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2605_28283_amd as pp
+    from paper_2605_28283_amd.workloads import WORKLOADS, workload_layer, workload_tokens
+
+    pp.load()
+    torch.cuda.init()
+    dev_name = torch.cuda.get_device_name(0)
+    w = WORKLOADS["llama8b_decode"]
+    d, d_ff, E = w.d, w.d_ff, w.E
+    layer_bytes = 3 * d_ff * d * 2 + E * d * 2
+    n_copies = args.copies or max(2, math.ceil(2.2e9 / layer_bytes))
+    T_max = max(w.T)
+    stream = torch.cuda.current_stream()
+
+    # ---- layers: copy 0 from the seeded numpy generator (shared with the CPU
+    # baseline), the rest drawn on the GPU
+    L0 = workload_layer(w, 0)
+    handles = []
+    for c in range(n_copies):
+        if c == 0:
+            Wt = [torch.from_numpy(a.view(np.int16)).cuda()
+                  for a in (L0.W_r, L0.W_gate, L0.W_up, L0.W_down)]
+        else:
+            Wt = device_layer(torch, d, d_ff, E, 1000 + c)
+        handles.append(pp.prunepath_create(d, d_ff, E, T_max, *Wt))
+        del Wt
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    x_np, _ = workload_tokens(w, T_max, 0)
+    x = torch.from_numpy(x_np.view(np.int16)).cuda()
+    y = torch.empty((T_max, d), dtype=torch.float32, device="cuda")
+    idx = torch.empty((T_max, E), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((T_max,), dtype=torch.int32, device="cuda")
+
+    def step(i, T, tau):
+        pp.prunepath_ffn_decode(handles[i % n_copies], x, T, tau, None, y, idx, cnt,
+                                stream=stream)
+
+    def union_stats(T, tau):
+        """Per copy: |U| (batch-union experts) and pairs sum_t k_t."""
+        out = []
+        for h in handles:
+            pp.prunepath_route(h, x, T, tau, None, idx, cnt, stream=stream)
+            torch.cuda.synchronize()
+            ii = idx[:T].cpu().numpy()
+            out.append((len(np.unique(ii[ii >= 0])), int(cnt[:T].sum().item())))
+        return out
+
+    def run_point(T, tau):
+        for i in range(args.warmup):
+            step(i, T, tau)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(args.steps):
+            step(i, T, tau)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        # per-kernel device time of the same sequence, HIP events on the call stream
+        for h in handles:
+            pp.prunepath_profile_begin(h, 4 * args.steps)
+        for i in range(args.steps):
+            step(i, T, tau)
+        torch.cuda.synchronize()
+        kms = [0.0] * pp.PP_KERNEL_COUNT
+        kn = [0] * pp.PP_KERNEL_COUNT
+        for h in handles:
+            a, n = pp.prunepath_profile_end(h)
+            kms = [u + v for u, v in zip(kms, a)]
+            kn = [u + v for u, v in zip(kn, n)]
+        us = union_stats(T, tau)
+        seq = [us[i % n_copies] for i in range(args.steps)]
+        U = float(np.mean([s[0] for s in seq]))
+        pairs = float(np.mean([s[1] for s in seq]))
+        step_bytes = E * d * 2 + U * 6 * 128 * d + 2 * T * d + 4 * T * d
+        gateup_bytes = U * 2 * 128 * d * 2 + 2 * T * d + pairs * 128 * 4
+        down_bytes = U * 128 * d * 2 + pairs * 128 * 4 + 4 * T * d
+        kavg = {name: (kms[k] / kn[k] * 1e3 if kn[k] else None)
+                for name, k in (("route", pp.PP_KERNEL_ROUTE), ("gateup", pp.PP_KERNEL_GATEUP),
+                                ("down", pp.PP_KERNEL_DOWN))}
+        gbps = step_bytes / (ms * 1e-3) / 1e9
+        return {
+            "T": T, "tau": tau, "ms_per_step": ms, "tokens_per_s_layer": T / (ms * 1e-3),
+            "union_experts": U, "pairs": pairs, "k_mean": pairs / T,
+            "algorithmic_bytes": step_bytes, "effective_GBps": gbps,
+            "frac_hbm_peak": gbps / HBM_PEAK_GBPS,
+            "kernel_us": kavg,
+            "gateup_bytes": gateup_bytes, "down_bytes": down_bytes,
+            "gateup_GBps": (gateup_bytes / (kavg["gateup"] * 1e-6) / 1e9
+                            if kavg["gateup"] else None),
+            "down_GBps": (down_bytes / (kavg["down"] * 1e-6) / 1e9 if kavg["down"] else None),
+        }
+
+    points = [(args.T, args.tau)]
+    if args.sweep == "full":
+        points = [(T, tau) for T in w.T for tau in w.taus]
+        if (args.T, args.tau) not in points:
+            points.append((args.T, args.tau))
+    results = {}
+    for T, tau in points:
+        r = run_point(T, tau)
+        results[(T, tau)] = r
+        print("# T=%-3d tau=%.2f  %8.1f us/step  %9.0f tok/s/layer  |U|=%5.1f  %7.1f GB/s "
+              "(%4.1f%% of peak)  gateup %s us  down %s us  route %s us" % (
+                  T, tau, r["ms_per_step"] * 1e3, r["tokens_per_s_layer"], r["union_experts"],
+                  r["effective_GBps"], 100 * r["frac_hbm_peak"],
+                  "%.1f" % r["kernel_us"]["gateup"], "%.1f" % r["kernel_us"]["down"],
+                  "%.1f" % r["kernel_us"]["route"]), file=sys.stderr, flush=True)
+    head = results[(args.T, args.tau)]
+
+    # ---- traffic from the committed rocprofv3 counter summary, if it is current
+    traffic = None
+    try:
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        if tr.get("source_hash") == source_hash() and tr.get("T") == args.T and \
+                abs(tr.get("tau", -1) - args.tau) < 1e-9:
+            traffic = tr.get("hbm_bytes_per_launch")
+    except (OSError, ValueError):
+        pass
+
+    roof = {"bound": "hbm", "achieved": head["gateup_GBps"], "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": head["gateup_GBps"] / HBM_PEAK_GBPS if head["gateup_GBps"] else None,
+            "traffic": traffic, "kernel": "gateup_k (gate/up projections + SiLU product)",
+            "algorithmic_bytes_per_launch": head["gateup_bytes"],
+            "avg_launch_us": head["kernel_us"]["gateup"]}
+
+    # ---- CPU oracle baseline (rank 0, N=1): same layer copy 0 and batch
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+        T = args.T
+        xs = x_np[:T]
+        oracle.forward(xs[:1], L0.W_r, L0.W_gate, L0.W_up, L0.W_down, args.tau)  # load / warm
+        n, t0 = 0, time.perf_counter()
+        while True:
+            oracle.forward(xs, L0.W_r, L0.W_gate, L0.W_up, L0.W_down, args.tau)
+            n += 1
+            el = time.perf_counter() - t0
+            if el >= args.cpu_seconds:
+                break
+        cpu = {"value": n * T / el, "unit": "tokens/s/layer", "cores": oracle.num_threads(),
+               "kind": "oracle",
+               "sample": "fp64 C oracle (route + kept-expert FFN), layer copy 0, the T=%d "
+                         "headline batch at tau=%g, repeated %d times in %.1f s" % (
+                             T, args.tau, n, el)}
+
+    sweep = [{k: v for k, v in r.items() if k not in ("gateup_bytes", "down_bytes")}
+             for r in results.values()]
+    out = {
+        "metric": "sparse-FFN decode tokens/s/layer",
+        "value": head["tokens_per_s_layer"],
+        "unit": "tokens/s/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llama8b_ffn_decode", "d_model": d, "d_ff": d_ff, "experts": E,
+                   "T": args.T, "tau": args.tau, "selection": "nucleus", "aggregation": "sum",
+                   "layer_copies": n_copies, "device": dev_name},
+        "effective_GBps": head["effective_GBps"],
+        "frac_hbm_peak": head["frac_hbm_peak"],
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "sweep": sweep,
+        "source_hash": source_hash(),
+    }
+    for h in handles:
+        pp.prunepath_destroy(h)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -64,7 +64,8 @@ typedef enum {
 
 /* prunepath_create -- build a layer (Sec. 2.2 expert split, Sec. 3.1 router).
  *   out        : receives the handle (host pointer to a host variable).
- *   d          : model width; must be a positive multiple of 64.
+ *   d          : model width; a positive multiple of 64, at most 8192
+ *                (PP_EUNSUPPORTED otherwise).
  *   d_ff, E    : intermediate width and expert count; d_ff must equal 128*E
  *                (PP_EUNSUPPORTED otherwise) and 1 <= E <= 256.
  *   max_tokens : largest T any later call will pass (1 .. 65536); scratch is
@@ -120,6 +121,27 @@ pp_status prunepath_ffn_decode(pp_layer *L, const uint16_t *x, int32_t T, float 
 pp_status prunepath_ffn_prefill(pp_layer *L, const uint16_t *x, int32_t T, float tau,
                                 const float *inv_temp, float *y, int32_t *expert_idx,
                                 int32_t *count, void *hip_stream);
+
+/* Kernel kinds reported by prunepath_profile_end. */
+#define PP_KERNEL_ROUTE 0     /* router: logits, softmax, sort, cut */
+#define PP_KERNEL_DISPATCH 1  /* prefill token bucketing */
+#define PP_KERNEL_GATEUP 2    /* gate/up projections + SiLU product */
+#define PP_KERNEL_DOWN 3      /* down projection + per-token sum */
+#define PP_KERNEL_COUNT 4
+
+/* prunepath_profile_begin -- benchmarking aid (not part of the method):
+ * from now on every kernel this handle launches is bracketed by two HIP
+ * events recorded on the call's stream, for at most `capacity` launches
+ * (1 .. 1<<20).  Creates the events, so call it outside any timed or
+ * captured region.  PP_EINVAL if already recording. */
+pp_status prunepath_profile_begin(pp_layer *L, int32_t capacity);
+
+/* prunepath_profile_end -- stop recording, wait for the recorded events and
+ * return, per kernel kind k < PP_KERNEL_COUNT, the summed device time in
+ * milliseconds (ms[k], host array) and the number of launches recorded
+ * (launches[k], host array).  Either array may be NULL.  PP_EINVAL if not
+ * recording. */
+pp_status prunepath_profile_end(pp_layer *L, double *ms, int32_t *launches);
 
 /* prunepath_destroy -- free a handle and its device memory.  NULL is a no-op.
  * The caller must ensure no enqueued work still uses the handle. */

@@ -24,8 +24,15 @@ PP_SELECT_STRICT = 1
 PP_AGG_SUM = 0
 PP_AGG_SIGMOID = 2
 
+PP_KERNEL_ROUTE = 0
+PP_KERNEL_DISPATCH = 1
+PP_KERNEL_GATEUP = 2
+PP_KERNEL_DOWN = 3
+PP_KERNEL_COUNT = 4
+
 EXPORTED = ("prunepath_create", "prunepath_route", "prunepath_ffn_decode",
-            "prunepath_ffn_prefill", "prunepath_destroy", "prunepath_status_string")
+            "prunepath_ffn_prefill", "prunepath_destroy", "prunepath_status_string",
+            "prunepath_profile_begin", "prunepath_profile_end")
 
 
 class PrunePathError(RuntimeError):
@@ -56,6 +63,11 @@ def load():
             f.restype = ctypes.c_int
         lib.prunepath_destroy.argtypes = [P]
         lib.prunepath_destroy.restype = None
+        lib.prunepath_profile_begin.argtypes = [P, I32]
+        lib.prunepath_profile_begin.restype = ctypes.c_int
+        lib.prunepath_profile_end.argtypes = [P, ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(ctypes.c_int32)]
+        lib.prunepath_profile_end.restype = ctypes.c_int
         lib.prunepath_status_string.argtypes = [ctypes.c_int]
         lib.prunepath_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -143,6 +155,18 @@ def prunepath_ffn_prefill(handle, x, T, tau, inv_temp, y, expert_idx=None, count
                                       _ptr(y, "f32"), _ptr(expert_idx, "i32"),
                                       _ptr(count, "i32"), _stream(stream))
     _check(st, "prunepath_ffn_prefill")
+
+
+def prunepath_profile_begin(handle, capacity):
+    _check(load().prunepath_profile_begin(handle, capacity), "prunepath_profile_begin")
+
+
+def prunepath_profile_end(handle):
+    """Returns (ms[PP_KERNEL_COUNT], launches[PP_KERNEL_COUNT]) as lists."""
+    ms = (ctypes.c_double * PP_KERNEL_COUNT)()
+    n = (ctypes.c_int32 * PP_KERNEL_COUNT)()
+    _check(load().prunepath_profile_end(handle, ms, n), "prunepath_profile_end")
+    return list(ms), list(n)
 
 
 def prunepath_destroy(handle):

@@ -9,9 +9,38 @@
 
 #include "pp_internal.h"
 
+namespace pp {
+
+struct profiler {
+    std::vector<hipEvent_t> ev;  // start/stop pairs
+    std::vector<int> kind;
+    int cap = 0, used = 0;
+};
+
+void prof_mark(pp_layer *L, int kind, hipStream_t s, bool start) {
+    profiler *P = L->prof;
+    if (!P || P->used >= P->cap) return;
+    if (start) {
+        (void)hipEventRecord(P->ev[2 * P->used], s);
+        P->kind[P->used] = kind;
+    } else {
+        (void)hipEventRecord(P->ev[2 * P->used + 1], s);
+        ++P->used;
+    }
+}
+
+}  // namespace pp
+
 namespace {
 
 using namespace pp;
+
+void free_profiler(profiler *P) {
+    if (!P) return;
+    for (hipEvent_t e : P->ev)
+        if (e) (void)hipEventDestroy(e);
+    delete P;
+}
 
 constexpr int kMaxTokensLimit = 65536;
 
@@ -29,6 +58,7 @@ void free_layer(pp_layer *L) {
                     L->h_lo,   L->ypart, L->ecount,  L->tokl};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
+    free_profiler(L->prof);
     delete L;
 }
 
@@ -96,7 +126,7 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     if (d_ff % E != 0) return PP_EINVAL;
     if (E > kMaxExperts) return PP_EUNSUPPORTED;
     if (d_ff / E != kExpertWidth) return PP_EUNSUPPORTED;
-    if (d % 64 != 0) return PP_EUNSUPPORTED;
+    if (d % 64 != 0 || d > kRouteMaxSlices * kRouteSliceSteps * kKStep) return PP_EUNSUPPORTED;
 
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     if (perm) {
@@ -196,6 +226,49 @@ pp_status prunepath_ffn_prefill(pp_layer *L, const uint16_t *x, int32_t T, float
                                 const float *inv_temp, float *y, int32_t *expert_idx,
                                 int32_t *count, void *hip_stream) {
     return run_ffn(L, x, T, tau, inv_temp, y, expert_idx, count, hip_stream, true);
+}
+
+pp_status prunepath_profile_begin(pp_layer *L, int32_t capacity) {
+    if (!L || L->prof || capacity < 1 || capacity > (1 << 20)) return PP_EINVAL;
+    profiler *P = new (std::nothrow) profiler;
+    if (!P) return PP_ENOMEM;
+    P->cap = capacity;
+    P->ev.assign((size_t)2 * capacity, nullptr);
+    P->kind.assign((size_t)capacity, 0);
+    for (auto &e : P->ev) {
+        if (hipEventCreate(&e) != hipSuccess) {
+            e = nullptr;
+            free_profiler(P);
+            return PP_EHIP;
+        }
+    }
+    L->prof = P;
+    return PP_OK;
+}
+
+pp_status prunepath_profile_end(pp_layer *L, double *ms, int32_t *launches) {
+    if (!L || !L->prof) return PP_EINVAL;
+    profiler *P = L->prof;
+    L->prof = nullptr;
+    double acc[PP_KERNEL_COUNT] = {0, 0, 0, 0};
+    int32_t n[PP_KERNEL_COUNT] = {0, 0, 0, 0};
+    pp_status st = PP_OK;
+    for (int i = 0; i < P->used && st == PP_OK; ++i) {
+        float t = 0.f;
+        if (hipEventSynchronize(P->ev[2 * i + 1]) != hipSuccess ||
+            hipEventElapsedTime(&t, P->ev[2 * i], P->ev[2 * i + 1]) != hipSuccess) {
+            st = PP_EHIP;
+            break;
+        }
+        acc[P->kind[i]] += t;
+        n[P->kind[i]] += 1;
+    }
+    free_profiler(P);
+    for (int k = 0; k < PP_KERNEL_COUNT; ++k) {
+        if (ms) ms[k] = acc[k];
+        if (launches) launches[k] = n[k];
+    }
+    return st;
 }
 
 void prunepath_destroy(pp_layer *L) { free_layer(L); }

@@ -185,8 +185,11 @@ __global__ __launch_bounds__(512) void gateup_k(GUParams P) {
     else
         prefill_groups(P.ecount, P.E, G);
     const int nG = G.nG, npairs = G.npairs;
-    int KS = (kUnitTarget + nG - 1) / nG;
-    if (KS > P.NS) KS = P.NS;
+    // K-slices per group: as many as keep every unit in the one round of
+    // resident workgroups (gridDim.x), each slice at least kMinStepsPerSlice
+    int KS = (int)gridDim.x / nG;
+    const int max_ks = P.NS / kMinStepsPerSlice > 0 ? P.NS / kMinStepsPerSlice : 1;
+    if (KS > max_ks) KS = max_ks;
     if (KS > 1 && (size_t)KS * npairs > P.abpart_rows) KS = (int)(P.abpart_rows / npairs);
     if (KS < 1) KS = 1;
     const int units = nG * KS;
@@ -255,37 +258,44 @@ __global__ __launch_bounds__(512) void gateup_k(GUParams P) {
                 const int q = 16 * j + (lane & 15);
                 if (j < NT && q < n) {
                     float *row = P.abpart + ((size_t)ks * npairs + poff + q) * 256 + r0;
-                    *reinterpret_cast<float4 *>(row) =
-                        make_float4(ag[j][0], ag[j][1], ag[j][2], ag[j][3]);
-                    *reinterpret_cast<float4 *>(row + 128) =
-                        make_float4(au[j][0], au[j][1], au[j][2], au[j][3]);
+                    st_dev2(row, ag[j][0], ag[j][1]);
+                    st_dev2(row + 2, ag[j][2], ag[j][3]);
+                    st_dev2(row + 128, au[j][0], au[j][1]);
+                    st_dev2(row + 130, au[j][2], au[j][3]);
                 }
             }
-            __threadfence();
-            __syncthreads();
-            if (tid == 0) {
-                const unsigned old = atomicAdd(&P.cnt[g], 1u);
-                const int last = (old == (unsigned)KS - 1u);
-                if (last) atomicExch(&P.cnt[g], 0u);
-                G.flag = last;
-            }
-            __syncthreads();
-            if (G.flag) {
-                __threadfence();
-                for (int i = tid; i < n * kExpertWidth; i += blockDim.x) {
-                    const int q = i >> 7, r = i & 127;
-                    float a = 0.f, b = 0.f;
-                    for (int k = 0; k < KS; ++k) {
-                        const float *row = P.abpart + ((size_t)k * npairs + poff + q) * 256;
-                        a += row[r];
-                        b += row[128 + r];
+            if (arrive_last(&P.cnt[g], (unsigned)KS, &G.flag)) {
+                for (int i = tid; i < n * (kExpertWidth / 2); i += blockDim.x) {
+                    const int q = i >> 6, r = 2 * (i & 63);
+                    float2 a = make_float2(0.f, 0.f), b = make_float2(0.f, 0.f);
+                    for (int k0 = 0; k0 < KS; k0 += 8) {
+                        float2 u[8], v[8];
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            u[k] = v[k] = make_float2(0.f, 0.f);
+                            if (k0 + k < KS) {
+                                const float *row =
+                                    P.abpart + ((size_t)(k0 + k) * npairs + poff + q) * 256;
+                                u[k] = ld_dev2(row + r);
+                                v[k] = ld_dev2(row + 128 + r);
+                            }
+                        }
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            a.x += u[k].x;
+                            a.y += u[k].y;
+                            b.x += v[k].x;
+                            b.y += v[k].y;
+                        }
                     }
                     const float scl = sig ? P.gsig[(size_t)stok[q] * P.E + e] : 1.0f;
-                    const float h = silu(a) * b * scl;
-                    const uint16_t hi = f32_to_bf16(h);
+                    const float h0 = silu(a.x) * b.x * scl, h1 = silu(a.y) * b.y * scl;
+                    const uint16_t hi0 = f32_to_bf16(h0), hi1 = f32_to_bf16(h1);
+                    const uint16_t lo0 = f32_to_bf16(h0 - bf16_to_f32(hi0)),
+                                   lo1 = f32_to_bf16(h1 - bf16_to_f32(hi1));
                     const size_t o = (size_t)(poff + q) * kExpertWidth + r;
-                    P.h_hi[o] = hi;
-                    P.h_lo[o] = f32_to_bf16(h - bf16_to_f32(hi));
+                    *reinterpret_cast<uint32_t *>(P.h_hi + o) = hi0 | ((uint32_t)hi1 << 16);
+                    *reinterpret_cast<uint32_t *>(P.h_lo + o) = lo0 | ((uint32_t)lo1 << 16);
                 }
             }
         }
@@ -303,7 +313,7 @@ __global__ __launch_bounds__(256) void down_dec_k(DNParams P) {
     decode_groups(P.selmask, P.T, P.E, G, sel);
     const int nU = G.nG;
     const int RB = 64 * MT, n_rb = P.d / RB;
-    int ES = (kUnitTarget + n_rb - 1) / n_rb;
+    int ES = (int)gridDim.x / n_rb;  // expert chunks: one round of resident workgroups
     if (ES > nU) ES = nU;
     if (ES > 1 && (size_t)ES * P.T * P.d > P.ypart_elems) ES = (int)(P.ypart_elems / ((size_t)P.T * P.d));
     if (ES < 1) ES = 1;
@@ -384,35 +394,32 @@ __global__ __launch_bounds__(256) void down_dec_k(DNParams P) {
 #pragma unroll
                 for (int j = 0; j < NTB; ++j) {
                     const int t = 16 * j + (lane & 15);
-                    if (t < P.T)
-                        *reinterpret_cast<float4 *>(P.ypart + ((size_t)c * P.T + t) * P.d + r0) =
-                            make_float4(acc[mt][j][0], acc[mt][j][1], acc[mt][j][2], acc[mt][j][3]);
+                    if (t < P.T) {
+                        float *row = P.ypart + ((size_t)c * P.T + t) * P.d + r0;
+                        st_dev2(row, acc[mt][j][0], acc[mt][j][1]);
+                        st_dev2(row + 2, acc[mt][j][2], acc[mt][j][3]);
+                    }
                 }
             }
-            __threadfence();
-            __syncthreads();
-            if (tid == 0) {
-                const unsigned old = atomicAdd(&P.cnt[rb], 1u);
-                const int last = (old == (unsigned)ES - 1u);
-                if (last) atomicExch(&P.cnt[rb], 0u);
-                G.flag = last;
-            }
-            __syncthreads();
-            if (G.flag) {
-                __threadfence();
-                for (int i = tid; i < P.T * (RB / 4); i += blockDim.x) {
-                    const int t = i / (RB / 4);
-                    const int r = rb * RB + 4 * (i - t * (RB / 4));
-                    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-                    for (int k = 0; k < ES; ++k) {
-                        const float4 v = *reinterpret_cast<const float4 *>(
-                            P.ypart + ((size_t)k * P.T + t) * P.d + r);
-                        s.x += v.x;
-                        s.y += v.y;
-                        s.z += v.z;
-                        s.w += v.w;
+            if (arrive_last(&P.cnt[rb], (unsigned)ES, &G.flag)) {
+                for (int i = tid; i < P.T * (RB / 2); i += blockDim.x) {
+                    const int t = i / (RB / 2);
+                    const int r = rb * RB + 2 * (i - t * (RB / 2));
+                    float2 s = make_float2(0.f, 0.f);
+                    for (int k0 = 0; k0 < ES; k0 += 8) {
+                        float2 v[8];
+#pragma unroll
+                        for (int k = 0; k < 8; ++k)
+                            v[k] = (k0 + k < ES)
+                                       ? ld_dev2(P.ypart + ((size_t)(k0 + k) * P.T + t) * P.d + r)
+                                       : make_float2(0.f, 0.f);
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            s.x += v[k].x;
+                            s.y += v[k].y;
+                        }
                     }
-                    *reinterpret_cast<float4 *>(P.y + (size_t)t * P.d + r) = s;
+                    *reinterpret_cast<float2 *>(P.y + (size_t)t * P.d + r) = s;
                 }
             }
         }
@@ -522,15 +529,30 @@ __global__ __launch_bounds__(256) void down_pf_k(DNParams P) {
     }
 }
 
-template <int MT>
-hipError_t launch_down_dec(const DNParams &P, int NTB, dim3 grid, hipStream_t s) {
-    switch (NTB) {
-    case 1: hipLaunchKernelGGL((down_dec_k<MT, 1>), grid, dim3(256), 0, s, P); break;
-    case 2: hipLaunchKernelGGL((down_dec_k<MT, 2>), grid, dim3(256), 0, s, P); break;
-    case 3: hipLaunchKernelGGL((down_dec_k<MT, 3>), grid, dim3(256), 0, s, P); break;
-    default: hipLaunchKernelGGL((down_dec_k<MT, 4>), grid, dim3(256), 0, s, P); break;
-    }
+// Resident workgroups per CU of a kernel (0 if the query fails).
+template <typename K>
+int resident(K kernel, int threads) {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess) n = 0;
+    return n;
+}
+
+template <int MT, int NTB>
+hipError_t launch_down_dec_v(const DNParams &P, int num_cu, hipStream_t s) {
+    static const int occ = resident(down_dec_k<MT, NTB>, 256);
+    const dim3 grid((occ > 0 ? occ : 1) * num_cu);
+    hipLaunchKernelGGL((down_dec_k<MT, NTB>), grid, dim3(256), 0, s, P);
     return hipGetLastError();
+}
+
+template <int MT>
+hipError_t launch_down_dec(const DNParams &P, int NTB, int num_cu, hipStream_t s) {
+    switch (NTB) {
+    case 1: return launch_down_dec_v<MT, 1>(P, num_cu, s);
+    case 2: return launch_down_dec_v<MT, 2>(P, num_cu, s);
+    case 3: return launch_down_dec_v<MT, 3>(P, num_cu, s);
+    default: return launch_down_dec_v<MT, 4>(P, num_cu, s);
+    }
 }
 
 GUParams gu_params(pp_layer *L, const uint16_t *x, int T) {
@@ -597,37 +619,57 @@ counter_layout counters_for(const pp_dims &dm, int max_tokens) {
 
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s) {
     const GUParams gp = gu_params(L, x, T);
-    hipLaunchKernelGGL(gateup_k<0>, dim3(2 * L->num_cu), dim3(512), 0, s, gp);
+    static const int occ_gu = resident(gateup_k<0>, 512);
+    prof_mark(L, PP_KERNEL_GATEUP, s, true);
+    hipLaunchKernelGGL(gateup_k<0>, dim3((occ_gu > 0 ? occ_gu : 1) * L->num_cu), dim3(512), 0, s,
+                       gp);
+    prof_mark(L, PP_KERNEL_GATEUP, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     const DNParams dp = dn_params(L, T, y);
     const int NTB = (T + 15) / 16;
     const int mt = pick_mt(L->dm.d, T);
-    const dim3 grid(4 * L->num_cu);
-    if (mt == 1) return launch_down_dec<1>(dp, NTB, grid, s);
-    if (mt == 2) return launch_down_dec<2>(dp, NTB, grid, s);
-    return launch_down_dec<4>(dp, NTB, grid, s);
+    prof_mark(L, PP_KERNEL_DOWN, s, true);
+    if (mt == 1)
+        err = launch_down_dec<1>(dp, NTB, L->num_cu, s);
+    else if (mt == 2)
+        err = launch_down_dec<2>(dp, NTB, L->num_cu, s);
+    else
+        err = launch_down_dec<4>(dp, NTB, L->num_cu, s);
+    prof_mark(L, PP_KERNEL_DOWN, s, false);
+    return err;
 }
 
 hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s) {
     const pp_dims &dm = L->dm;
+    prof_mark(L, PP_KERNEL_DISPATCH, s, true);
     hipLaunchKernelGGL(dispatch_k, dim3(dm.E), dim3(256), 0, s, L->selmask, T, dm.E, L->ecount,
                        L->tokl, L->max_tokens, y, (size_t)T * dm.d / 4);
+    prof_mark(L, PP_KERNEL_DISPATCH, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     const GUParams gp = gu_params(L, x, T);
-    hipLaunchKernelGGL(gateup_k<1>, dim3(2 * L->num_cu), dim3(512), 0, s, gp);
+    static const int occ_gu = resident(gateup_k<1>, 512);
+    prof_mark(L, PP_KERNEL_GATEUP, s, true);
+    hipLaunchKernelGGL(gateup_k<1>, dim3((occ_gu > 0 ? occ_gu : 1) * L->num_cu), dim3(512), 0, s,
+                       gp);
+    prof_mark(L, PP_KERNEL_GATEUP, s, false);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     const DNParams dp = dn_params(L, T, y);
     const int mt = pick_mt(dm.d, 64);
-    const dim3 grid(4 * L->num_cu);
+    static const int occ4 = resident(down_pf_k<4>, 256), occ2 = resident(down_pf_k<2>, 256),
+                     occ1 = resident(down_pf_k<1>, 256);
+    const int occ = mt == 4 ? occ4 : (mt == 2 ? occ2 : occ1);
+    const dim3 grid((occ > 0 ? occ : 1) * L->num_cu);
+    prof_mark(L, PP_KERNEL_DOWN, s, true);
     if (mt == 4)
         hipLaunchKernelGGL((down_pf_k<4>), grid, dim3(256), 0, s, dp);
     else if (mt == 2)
         hipLaunchKernelGGL((down_pf_k<2>), grid, dim3(256), 0, s, dp);
     else
         hipLaunchKernelGGL((down_pf_k<1>), grid, dim3(256), 0, s, dp);
+    prof_mark(L, PP_KERNEL_DOWN, s, false);
     return hipGetLastError();
 }
 

@@ -16,8 +16,10 @@ constexpr int kMaxExperts = 256;
 constexpr int kDecodeTile = 64;        // tokens per decode slice (one u64 token mask)
 constexpr int kRouteTile = 16;         // tokens / experts per router MFMA tile
 constexpr int kRouteSliceSteps = 16;   // K-steps per router K-slice (fixed: batch invariance)
+constexpr int kRouteMaxSlices = 16;    // router K-slices supported (d <= 8192)
 constexpr int kGroupTokens = 64;       // tokens per prefill expert group
 constexpr int kUnitTarget = 512;       // work units a persistent grid aims for
+constexpr int kMinStepsPerSlice = 8;   // K-steps each gate/up K-slice covers at least
 
 // Byte sizes of the scratch areas whose size does not follow from max_tokens.
 constexpr size_t kAbPartRows = 65536;  // K-split partial (a,b) rows of 256 floats
@@ -25,6 +27,11 @@ constexpr size_t kAbPartRows = 65536;  // K-split partial (a,b) rows of 256 floa
 struct pp_dims {
     int d, d_ff, E, NS;      // NS = d / 32 K-steps
 };
+
+struct profiler;  // per-kernel event timing (benchmarking aid)
+
+// Brackets one kernel launch with profiling events when the handle records.
+void prof_mark(pp_layer *L, int kind, hipStream_t s, bool start);
 
 }  // namespace pp
 
@@ -56,6 +63,7 @@ struct pp_layer {
     size_t ypart_elems;
     int32_t *ecount;    // [E] tokens per expert (prefill)
     int32_t *tokl;      // [E][max_tokens] token ids per expert (prefill)
+    pp::profiler *prof; // non-NULL while per-kernel timing is recorded
 };
 
 namespace pp {
@@ -104,6 +112,54 @@ __device__ __forceinline__ uint4 ldg16(const void *p) {
 }
 
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
+
+// ------------------------------------------------ hand-off between workgroups
+// Partial results that one workgroup passes to another inside the same kernel
+// are written and read with agent-scope relaxed atomic accesses, which gfx950
+// performs at the device coherence point (the per-XCD L2s are not coherent
+// with each other).  The writer waits for its stores to complete before it
+// bumps the arrival counter; the last arriver then reads with the same scope.
+// No cache-wide writeback or invalidate is needed, so other workgroups keep
+// their L2 contents.
+__device__ __forceinline__ void st_dev(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev2(float *p, float a, float b) {
+    const unsigned long long u =
+        (unsigned long long)__float_as_uint(a) | ((unsigned long long)__float_as_uint(b) << 32);
+    __hip_atomic_store(reinterpret_cast<unsigned long long *>(p), u, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 ld_dev2(const float *p) {
+    const unsigned long long u = __hip_atomic_load(
+        reinterpret_cast<const unsigned long long *>(p), __ATOMIC_RELAXED,
+        __HIP_MEMORY_SCOPE_AGENT);
+    return make_float2(__uint_as_float((uint32_t)u), __uint_as_float((uint32_t)(u >> 32)));
+}
+// Wait until this thread's outstanding vector-memory operations completed
+// (s_waitcnt vmcnt(0); the expcnt and lgkmcnt fields are left at their maxima).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Arrival on a counter shared by `n` workgroups after each has stored its
+// partial results with st_dev*; returns true in exactly one workgroup, the
+// last to arrive, which also resets the counter for the next call.  Must be
+// reached by every thread of the workgroup.  `flag` is a shared int.
+__device__ __forceinline__ bool arrive_last(uint32_t *counter, unsigned n, int *flag) {
+    wait_vmem();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned old =
+            __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int last = (old == n - 1u);
+        if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *flag = last;
+    }
+    __syncthreads();
+    return *flag != 0;
+}
 
 // Inclusive scan of one int per lane across a 64-lane wavefront.
 __device__ __forceinline__ int wave_incl_scan(int v) {

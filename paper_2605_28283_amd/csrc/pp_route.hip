@@ -5,8 +5,8 @@
 // K-slice of 16 K-steps = 512 columns of d).  Each wavefront accumulates a 16x16 logit tile with bf16 MFMA over
 // every fourth 32-wide K-step of the slice; the four tiles are summed in a
 // fixed order and the slice's partial logits are stored.  The workgroup that
-// completes a token tile last (arrival counter; release/acquire fences make
-// the other slices' partials visible) then routes its 16 tokens, four per
+// completes a token tile last (arrival counter;
+// device-scope stores/loads carry the other slices' partials) then routes its 16 tokens, four per
 // wavefront, interleaved so the four dependency chains overlap:
 //   g = (sum of partials in slice order + b) * inv_temp
 //   bitonic sort of (g, expert) over 64*J lanes/registers: larger g first,
@@ -38,15 +38,14 @@ struct RouteParams {
     float *gsig;
 };
 
-constexpr int kTokPerWave = 4;
-
 // a comes before b in pi
 __device__ __forceinline__ bool before(float ga, int ia, float gb, int ib) {
     return ga > gb || (ga == gb && ia < ib);
 }
 
-template <int J>
-__device__ void route_tokens(const RouteParams &P, int tt, int wv, int lane, uint32_t *smask) {
+template <int J, int kTokPerWave>
+__device__ void route_tokens(const RouteParams &P, int tt, int wv, int lane, uint32_t *smask,
+                             const float (*lg)[kMaxExperts]) {
     constexpr int N = 64 * J;
     float g[kTokPerWave][J];
     int id[kTokPerWave][J];
@@ -54,23 +53,20 @@ __device__ void route_tokens(const RouteParams &P, int tt, int wv, int lane, uin
     bool tv[kTokPerWave];
 #pragma unroll
     for (int m = 0; m < kTokPerWave; ++m) {
-        tok[m] = tt * kRouteTile + wv + 4 * m;
+        const int tl = wv + 4 * m;
+        tok[m] = tt * kRouteTile + tl;
         tv[m] = tok[m] < P.T;
-        const float it = (tv[m] && P.inv_temp) ? P.inv_temp[tok[m]] : 1.0f;
 #pragma unroll
         for (int j = 0; j < J; ++j) {
             const int e = lane + 64 * j;
             id[m][j] = e;
-            float v = -INFINITY;
-            if (tv[m] && e < P.E) {
-                float s = 0.0f;
-                for (int k = 0; k < P.KSr; ++k)
-                    s += P.gpart[((size_t)k * P.T + tok[m]) * P.E + e];
-                v = (s + P.bias[e]) * it;
-            }
-            g[m][j] = v;
+            g[m][j] = (tv[m] && e < P.E) ? lg[tl][e] : -INFINITY;
         }
     }
+    bool any = false;
+#pragma unroll
+    for (int m = 0; m < kTokPerWave; ++m) any |= tv[m];
+    if (!any) return;
     // bitonic sort, "smaller" = comes first in pi
 #pragma unroll
     for (int k = 2; k <= N; k <<= 1) {
@@ -178,8 +174,9 @@ __device__ void route_tokens(const RouteParams &P, int tt, int wv, int lane, uin
 template <int J>
 __global__ __launch_bounds__(256) void route_k(RouteParams P) {
     __shared__ f32x4 red[4][64];
-    __shared__ uint32_t smask[4][kTokPerWave * 8];
+    __shared__ uint32_t smask[4][4 * 8];
     __shared__ int s_last;
+    __shared__ float lg[kRouteTile][kMaxExperts];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int per_tile = P.nEt * P.KSr;
     const int tt = blockIdx.x / per_tile;
@@ -193,12 +190,18 @@ __global__ __launch_bounds__(256) void route_k(RouteParams P) {
     const uint16_t *xa = P.x + (size_t)(va ? tr : 0) * P.d + koff;
     const uint16_t *wb = P.Wr + (size_t)(vb ? ec : 0) * P.d + koff;
     const uint4 z = make_uint4(0, 0, 0, 0);
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s = s0 + wv; s < s1; s += 4) {
-        const uint4 a = va ? ldg16(xa + s * kKStep) : z;
-        const uint4 b = vb ? ldg16(wb + s * kKStep) : z;
-        acc = mfma16(a, b, acc);
+    // a slice has at most kRouteSliceSteps = 16 K-steps: four per wavefront
+    uint4 a[4], b[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int s = s0 + wv + 4 * i;
+        const bool ok = s < s1;
+        a[i] = (ok && va) ? ldg16(xa + s * kKStep) : z;
+        b[i] = (ok && vb) ? ldg16(wb + s * kKStep) : z;
     }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc = mfma16(a[i], b[i], acc);
     red[wv][lane] = acc;
     __syncthreads();
     if (wv == 0) {
@@ -211,24 +214,50 @@ __global__ __launch_bounds__(256) void route_k(RouteParams P) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int t = tt * kRouteTile + 4 * (lane >> 4) + i;
-            if (t < P.T && e < P.E) P.gpart[((size_t)ks * P.T + t) * P.E + e] = r[i];
+            if (t < P.T && e < P.E) st_dev(P.gpart + ((size_t)ks * P.T + t) * P.E + e, r[i]);
         }
     }
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int last = 1;
-        if (per_tile > 1) {
-            const unsigned old = atomicAdd(&P.cnt[tt], 1u);
-            last = (old == (unsigned)per_tile - 1u);
-            if (last) atomicExch(&P.cnt[tt], 0u);
+    if (!arrive_last(&P.cnt[tt], (unsigned)per_tile, &s_last)) return;
+    // logits of the tile's tokens: slices summed in slice order (fixed), then
+    // bias and temperature; all loads of a batch are issued before any add
+    const int nt = min(kRouteTile, P.T - tt * kRouteTile);
+    const int n_el = nt * P.E;
+    for (int base = 0; base < n_el; base += 4 * 256) {
+        float v[4][kRouteMaxSlices];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = base + q * 256 + threadIdx.x;
+            const bool ok = i < n_el;
+            const int t = tt * kRouteTile + (ok ? i / P.E : 0), e = ok ? i % P.E : 0;
+#pragma unroll
+            for (int k = 0; k < kRouteMaxSlices; ++k)
+                v[q][k] = (ok && k < P.KSr) ? ld_dev(P.gpart + ((size_t)k * P.T + t) * P.E + e)
+                                            : 0.0f;
         }
-        s_last = last;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = base + q * 256 + threadIdx.x;
+            if (i < n_el) {
+                float sum = 0.0f;
+#pragma unroll
+                for (int k = 0; k < kRouteMaxSlices; ++k)
+                    if (k < P.KSr) sum += v[q][k];
+                const int tl = i / P.E, e = i % P.E;
+                const int t = tt * kRouteTile + tl;
+                const float it = P.inv_temp ? P.inv_temp[t] : 1.0f;
+                lg[tl][e] = (sum + P.bias[e]) * it;
+            }
+        }
     }
     __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    route_tokens<J>(P, tt, wv, lane, smask[wv]);
+    // four wavefronts share the tile's tokens
+    const int tpw = (nt + 3) / 4;
+    if (tpw == 1)
+        route_tokens<J, 1>(P, tt, wv, lane, smask[wv], lg);
+    else if (tpw == 2)
+        route_tokens<J, 2>(P, tt, wv, lane, smask[wv], lg);
+    else
+        route_tokens<J, 4>(P, tt, wv, lane, smask[wv], lg);
 }
 
 }  // namespace
@@ -267,12 +296,14 @@ hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const 
     P.gsig = L->gsig;
     const int nTt = (T + kRouteTile - 1) / kRouteTile;
     const dim3 grid(nTt * P.nEt * P.KSr);
+    prof_mark(L, PP_KERNEL_ROUTE, s, true);
     if (dm.E <= 64)
         hipLaunchKernelGGL(route_k<1>, grid, dim3(256), 0, s, P);
     else if (dm.E <= 128)
         hipLaunchKernelGGL(route_k<2>, grid, dim3(256), 0, s, P);
     else
         hipLaunchKernelGGL(route_k<4>, grid, dim3(256), 0, s, P);
+    prof_mark(L, PP_KERNEL_ROUTE, s, false);
     return hipGetLastError();
 }
 
