@@ -38,6 +38,9 @@ def parse_args():
     ap.add_argument("--copies", type=int, default=0, help="layer copies (0 = enough for 2.2 GB)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the CPU-oracle baseline (0 = skip)")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (5 times), the "
+                         "reference dispatch for scaling HBM byte counters")
     return ap.parse_args()
 
 
@@ -249,6 +252,14 @@ def main():
     }
     for h in handles:
         pp.prunepath_destroy(h)
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calibration_copy_bytes"] = 4 * n
     print(json.dumps(out), flush=True)
 
 

@@ -55,20 +55,12 @@ void free_layer(pp_layer *L) {
     if (!L) return;
     void *bufs[] = {L->Wr,     L->bias,  L->Wgu,     L->Wd,    L->gpart, L->counters,
                     L->selmask, L->gsig, L->idx_tmp, L->cnt_tmp, L->abpart, L->h_hi,
-                    L->h_lo,   L->ypart, L->ecount,  L->tokl};
+                    L->h_lo,   L->ypart, L->ecount,  L->tokl,  L->plan,  L->dec_tok,
+                    L->emask};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
     free_profiler(L->prof);
     delete L;
-}
-
-size_t gpart_capacity(const pp_dims &dm, int max_tokens) {
-    size_t best = 0;
-    for (int T = 1; T <= max_tokens; ++T) {
-        const size_t need = (size_t)route_split(dm, T) * T * dm.E;
-        if (need > best) best = need;
-    }
-    return best;
 }
 
 bool valid_tau(float tau) { return !isnan(tau) && tau >= 0.0f; }
@@ -101,7 +93,7 @@ pp_status run_ffn(pp_layer *L, const uint16_t *x, int32_t T, float tau, const fl
         const uint16_t *xs = x + (size_t)t0 * d;
         float *ys = y + (size_t)t0 * d;
         const float *it = inv_temp ? inv_temp + t0 : nullptr;
-        hipError_t e = launch_route(L, xs, n, tau, it, idx, cnt, nullptr, s);
+        hipError_t e = launch_route(L, xs, n, tau, it, idx, cnt, nullptr, !prefill, s);
         if (e == hipSuccess)
             e = prefill ? launch_prefill_ffn(L, xs, n, ys, s) : launch_decode_ffn(L, xs, n, ys, s);
         if (e != hipSuccess) return hip_status(e);
@@ -126,7 +118,7 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     if (d_ff % E != 0) return PP_EINVAL;
     if (E > kMaxExperts) return PP_EUNSUPPORTED;
     if (d_ff / E != kExpertWidth) return PP_EUNSUPPORTED;
-    if (d % 64 != 0 || d > kRouteMaxSlices * kRouteSliceSteps * kKStep) return PP_EUNSUPPORTED;
+    if (d % 64 != 0 || d > kMaxWidth) return PP_EUNSUPPORTED;
 
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     if (perm) {
@@ -160,11 +152,10 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
 
     const size_t dE = (size_t)d * E;
     const counter_layout cl = counters_for(L->dm, max_tokens);
-    L->gpart_elems = gpart_capacity(L->dm, max_tokens);
+    L->gpart_elems = (size_t)max_tokens * E;
     L->n_counters = cl.total;
     L->max_pairs = (size_t)max_tokens * E;
-    const int min_rb = d / 256 > 0 ? d / 256 : 1;
-    L->ypart_elems = (size_t)((kUnitTarget + min_rb - 1) / min_rb + 1) * kDecodeTile * d;
+    L->ypart_elems = (size_t)32 * kDecodeTile * d;  // at most 32 expert chunks of a 64-token slice
 
     hipError_t a = hipSuccess;
     auto chk = [&](hipError_t r) {
@@ -186,6 +177,9 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     chk(dev_alloc(&L->ypart, L->ypart_elems));
     chk(dev_alloc(&L->ecount, (size_t)E));
     chk(dev_alloc(&L->tokl, (size_t)E * max_tokens));
+    chk(dev_alloc(&L->plan, (size_t)4 + 4 * (size_t)plan_max_groups(L->dm, max_tokens)));
+    chk(dev_alloc(&L->dec_tok, (size_t)kDecodeTile * E));
+    chk(dev_alloc(&L->emask, (size_t)E));
     if (a != hipSuccess) {
         free_layer(L);
         return hip_status(a);
@@ -196,6 +190,7 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     else
         chk(hipMemsetAsync(L->bias, 0, sizeof(float) * E, s));
     chk(hipMemsetAsync(L->counters, 0, sizeof(uint32_t) * L->n_counters, s));
+    chk(hipMemsetAsync(L->emask, 0, sizeof(unsigned long long) * E, s));
     if (a == hipSuccess) a = launch_repack(L, W_gate, W_up, W_down, perm, s);
     chk(hipStreamSynchronize(s));
     if (a != hipSuccess) {
@@ -212,7 +207,7 @@ pp_status prunepath_route(pp_layer *L, const uint16_t *x, int32_t T, float tau,
     pp_status st = check_call(L, x, T, tau);
     if (st != PP_OK) return st;
     if (!expert_idx || !count) return PP_EINVAL;
-    return hip_status(launch_route(L, x, T, tau, inv_temp, expert_idx, count, gate_w,
+    return hip_status(launch_route(L, x, T, tau, inv_temp, expert_idx, count, gate_w, false,
                                    static_cast<hipStream_t>(hip_stream)));
 }
 

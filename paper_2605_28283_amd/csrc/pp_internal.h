@@ -15,10 +15,8 @@ constexpr int kKStep = 32;             // K per bf16 MFMA 16x16x32
 constexpr int kMaxExperts = 256;
 constexpr int kDecodeTile = 64;        // tokens per decode slice (one u64 token mask)
 constexpr int kRouteTile = 16;         // tokens / experts per router MFMA tile
-constexpr int kRouteSliceSteps = 16;   // K-steps per router K-slice (fixed: batch invariance)
-constexpr int kRouteMaxSlices = 16;    // router K-slices supported (d <= 8192)
+constexpr int kMaxWidth = 8192;        // largest supported d
 constexpr int kGroupTokens = 64;       // tokens per prefill expert group
-constexpr int kUnitTarget = 512;       // work units a persistent grid aims for
 constexpr int kMinStepsPerSlice = 8;   // K-steps each gate/up K-slice covers at least
 
 // Byte sizes of the scratch areas whose size does not follow from max_tokens.
@@ -29,6 +27,24 @@ struct pp_dims {
 };
 
 struct profiler;  // per-kernel event timing (benchmarking aid)
+
+// Work plan of one FFN call (device memory): head[0] = number of groups,
+// head[1] = number of (token, expert) pair rows; group g is expert grp_e[g]
+// with grp_n[g] <= 64 tokens toklist[grp_tok[g] .. + grp_n[g]) whose h rows
+// start at grp_pair[g].
+struct PlanView {
+    int32_t *head;
+    int32_t *grp_e;
+    int32_t *grp_pair;
+    int32_t *grp_n;
+    int32_t *grp_tok;
+    int32_t *toklist;
+};
+
+// Largest number of groups a call can produce.
+inline int plan_max_groups(const pp_dims &dm, int max_tokens) {
+    return dm.E + (int)(((long)max_tokens * dm.E + 63) / 64);
+}
 
 // Brackets one kernel launch with profiling events when the handle records.
 void prof_mark(pp_layer *L, int kind, hipStream_t s, bool start);
@@ -47,7 +63,7 @@ struct pp_layer {
     uint16_t *Wgu;     // expert-major gate/up MFMA fragments
     uint16_t *Wd;      // expert-major down MFMA fragments
     // scratch
-    float *gpart;       // router K-split partial logits [KSr][T][E]
+    float *gpart;       // router logits [max_tokens][E]
     size_t gpart_elems;
     uint32_t *counters; // arrival counters, zero between calls
     size_t n_counters;
@@ -63,6 +79,9 @@ struct pp_layer {
     size_t ypart_elems;
     int32_t *ecount;    // [E] tokens per expert (prefill)
     int32_t *tokl;      // [E][max_tokens] token ids per expert (prefill)
+    int32_t *plan;      // PlanView storage: 4 + 4 * plan_max_groups ints
+    int32_t *dec_tok;   // [64 * E] token ids of the decode plan, pair order
+    unsigned long long *emask;  // [E] decode: tokens that kept each expert (zero between calls)
     pp::profiler *prof; // non-NULL while per-kernel timing is recorded
 };
 
@@ -70,21 +89,36 @@ namespace pp {
 
 // Counter regions inside pp_layer::counters.
 struct counter_layout {
-    size_t route;   // ceil(max_tokens/16)
-    size_t gateup;  // one per expert group
-    size_t down;    // one per row block
+    size_t route;     // one: the decode plan builder
+    size_t gateup;    // one per group
+    size_t down;      // one per 64-row block
+    size_t dispatch;  // one
     size_t total;
 };
 counter_layout counters_for(const pp_dims &dm, int max_tokens);
 
-int route_split(const pp_dims &dm, int T);  // router K-split factor for T tokens
+inline PlanView plan_view(pp_layer *L, bool prefill);
+
 
 hipError_t launch_repack(pp_layer *L, const uint16_t *W_gate, const uint16_t *W_up,
                          const uint16_t *W_down, const int32_t *perm, hipStream_t s);
 hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const float *inv_temp,
-                        int32_t *idx, int32_t *count, float *gate_w, hipStream_t s);
+                        int32_t *idx, int32_t *count, float *gate_w, bool build_plan,
+                        hipStream_t s);
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
 hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
+
+inline PlanView plan_view(pp_layer *L, bool prefill) {
+    const int G = plan_max_groups(L->dm, L->max_tokens);
+    PlanView v;
+    v.head = L->plan;
+    v.grp_e = L->plan + 4;
+    v.grp_pair = v.grp_e + G;
+    v.grp_n = v.grp_pair + G;
+    v.grp_tok = v.grp_n + G;
+    v.toklist = prefill ? L->tokl : L->dec_tok;
+    return v;
+}
 
 // ---------------------------------------------------------------- device helpers
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -130,6 +164,12 @@ __device__ __forceinline__ void st_dev2(float *p, float a, float b) {
     __hip_atomic_store(reinterpret_cast<unsigned long long *>(p), u, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ void st_dev_u32(uint32_t *p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t ld_dev_u32(const uint32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ float ld_dev(const float *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -159,6 +199,58 @@ __device__ __forceinline__ bool arrive_last(uint32_t *counter, unsigned n, int *
     }
     __syncthreads();
     return *flag != 0;
+}
+
+// ------------------------------------------------ cross-lane exchange (no LDS)
+// Value of lane (lane ^ ST) for ST = 1..32, built from DPP row operations
+// (quad permutes, row shifts, row rotate) and the gfx950 permlane swaps.
+template <int ST>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v, int lane) {
+    if constexpr (ST == 1) {
+        return __builtin_amdgcn_update_dpp(0u, v, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+    } else if constexpr (ST == 2) {
+        return __builtin_amdgcn_update_dpp(0u, v, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+    } else if constexpr (ST == 4) {
+        const uint32_t up = __builtin_amdgcn_update_dpp(0u, v, 0x104, 0xF, 0xF, false);  // i <- i+4
+        const uint32_t dn = __builtin_amdgcn_update_dpp(0u, v, 0x114, 0xF, 0xF, false);  // i <- i-4
+        return (lane & 4) ? dn : up;
+    } else if constexpr (ST == 8) {
+        return __builtin_amdgcn_update_dpp(0u, v, 0x128, 0xF, 0xF, false);  // row_ror:8
+    } else if constexpr (ST == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return (lane & 16) ? r[0] : r[1];
+    } else {
+        static_assert(ST == 32, "xor_lane: stride must be a power of two below 64");
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return (lane & 32) ? r[0] : r[1];
+    }
+}
+
+__device__ __forceinline__ uint32_t xor_lane_rt(uint32_t v, int st, int lane) {
+    switch (st) {
+    case 1: return xor_lane<1>(v, lane);
+    case 2: return xor_lane<2>(v, lane);
+    case 4: return xor_lane<4>(v, lane);
+    case 8: return xor_lane<8>(v, lane);
+    case 16: return xor_lane<16>(v, lane);
+    default: return xor_lane<32>(v, lane);
+    }
+}
+
+// Inclusive prefix sum of one float per lane over the 64-lane wavefront, in
+// DPP row shifts (within rows of 16) and row broadcasts (across rows).
+__device__ __forceinline__ float wave_scan_f32(float x) {
+    x += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), 0x111, 0xF, 0xF, false));
+    x += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), 0x112, 0xF, 0xF, false));
+    x += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), 0x114, 0xF, 0xF, false));
+    x += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), 0x118, 0xF, 0xF, false));
+    x += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), 0x142, 0xA, 0xF, false));
+    x += __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), 0x143, 0xC, 0xF, false));
+    return x;
+}
+
+__device__ __forceinline__ float lane_value(float x, int lane) {
+    return __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), lane));
 }
 
 // Inclusive scan of one int per lane across a 64-lane wavefront.

@@ -1,24 +1,35 @@
-// Fused router: Eq. (routing_logits) GEMV, Eq. (softmax_prob), the descending
-// order pi, the cumulative mass C and the tau cut of Eq. (tau_thresh_activate).
+// Router: Eq. (routing_logits) GEMV, Eq. (softmax_prob), the descending order
+// pi, the cumulative mass C and the tau cut of Eq. (tau_thresh_activate).
 //
-// Grid: one workgroup (4 wavefronts) per (16-token tile, 16-expert tile,
-// K-slice of 16 K-steps = 512 columns of d).  Each wavefront accumulates a 16x16 logit tile with bf16 MFMA over
-// every fourth 32-wide K-step of the slice; the four tiles are summed in a
-// fixed order and the slice's partial logits are stored.  The workgroup that
-// completes a token tile last (arrival counter;
-// device-scope stores/loads carry the other slices' partials) then routes its 16 tokens, four per
-// wavefront, interleaved so the four dependency chains overlap:
-//   g = (sum of partials in slice order + b) * inv_temp
-//   bitonic sort of (g, expert) over 64*J lanes/registers: larger g first,
-//   equal g by ascending expert index (ordering g orders p: softmax is monotone)
-//   p = exp(g - g_max) / sum, inclusive prefix sums C in sorted order
-//   m = #{i < E : C_i < tau} over the first E-1 positions, then
-//   nucleus: k = E if tau >= 1 else min(E, m + 1);  strict: k = max(1, m + [tau > 1]).
-// The result is deterministic: no floating-point atomics anywhere.
+// logits_k : one workgroup of 16 wavefronts per (16-token tile, 16-expert
+//            tile).  Wavefront w accumulates its contiguous share of the K-steps
+//            of d with bf16 MFMA; the 16 partial tiles are summed in wavefront
+//            order, then g = (W_r x + b) * inv_temp is stored.  The summation
+//            order depends on d only, never on T, so a token's logits are the
+//            same bits in any batch: routing is batch-invariant.
+// select_k : one wavefront per token.  pi orders experts by descending g,
+//            equal g by ascending expert index (ordering g orders p: softmax is
+//            monotone).  With e_i = exp(g_i - g_max), S = sum e and
+//            C_i = (e_pi1 + ... + e_pii) / S:
+//              nucleus: k = min{i : C_i >= tau}, all E if tau >= 1;
+//              strict:  k = max(1, #{i < E : C_i < tau} + [tau > 1]).
+//            The kept prefix is found by repeated wavefront arg-max (DPP /
+//            permlane exchanges, no LDS traffic), one expert at a time, which
+//            costs O(k); past kMaxIterative kept experts the token falls back
+//            to a bitonic sort of all experts.  When every expert is kept
+//            (tau >= 1 nucleus, tau > 1 strict) the order comes from the sort.
+//            For a decode batch (T <= 64) each token also sets its bit in the
+//            per-expert token masks (device-scope atomic OR) and the last token
+//            to finish writes the batch plan: the union of kept experts, each
+//            with its tokens and its first pair row.
+// Deterministic: no floating-point atomics.
 #include "pp_internal.h"
 
 namespace pp {
 namespace {
+
+constexpr int kRouteWaves = 16;
+constexpr int kMaxIterative = 16;  // kept experts found by arg-max before falling back to a sort
 
 struct RouteParams {
     const uint16_t *x;
@@ -28,46 +39,88 @@ struct RouteParams {
     const float *inv_temp;
     float tau;
     uint32_t flags;
-    int KSr, nEt;
-    float *gpart;
-    uint32_t *cnt;
+    int nEt;
+    float *glog;         // [T][E] logits
     int32_t *idx;
     int32_t *count;
     float *gate_w;
     uint32_t *selmask;
     float *gsig;
+    PlanView plan;       // written when build_plan != 0
+    int build_plan;
+    unsigned long long *emask;  // [E] tokens of the batch that kept each expert (zero between calls)
+    uint32_t *plan_cnt;         // arrival counter of the plan builder
 };
+
+__global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
+    __shared__ f32x4 red[kRouteWaves][64];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int tt = blockIdx.x / P.nEt, et = blockIdx.x - tt * P.nEt;
+    const int tr = tt * kRouteTile + (lane & 15);
+    const int ec = et * kRouteTile + (lane & 15);
+    const int koff = 8 * (lane >> 4);
+    const bool va = tr < P.T, vb = ec < P.E;
+    const uint16_t *xa = P.x + (size_t)(va ? tr : 0) * P.d + koff;
+    const uint16_t *wb = P.Wr + (size_t)(vb ? ec : 0) * P.d + koff;
+    const int spw = (P.NS + kRouteWaves - 1) / kRouteWaves;  // K-steps per wavefront (<= 16)
+    const int s_lo = wv * spw, s_hi = min(P.NS, s_lo + spw);
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int b0 = s_lo; b0 < s_hi; b0 += 8) {
+        uint4 a[8], b[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int s = b0 + i;
+            a[i] = (va && s < s_hi) ? ldg16(xa + s * kKStep) : z;
+            b[i] = (vb && s < s_hi) ? ldg16(wb + s * kKStep) : z;
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc = mfma16(a[i], b[i], acc);
+    }
+    red[wv][lane] = acc;
+    __syncthreads();
+    if (wv != 0) return;
+    f32x4 r = red[0][lane];
+#pragma unroll
+    for (int w = 1; w < kRouteWaves; ++w) r += red[w][lane];
+    // MFMA 16x16 result: lane holds rows 4*(lane/16)+i (tokens), column lane%16 (expert)
+    if (!vb) return;
+    const float bias = P.bias[ec];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int t = tt * kRouteTile + 4 * (lane >> 4) + i;
+        if (t < P.T) {
+            const float it = P.inv_temp ? P.inv_temp[t] : 1.0f;
+            P.glog[(size_t)t * P.E + ec] = (r[i] + bias) * it;
+        }
+    }
+}
 
 // a comes before b in pi
 __device__ __forceinline__ bool before(float ga, int ia, float gb, int ib) {
     return ga > gb || (ga == gb && ia < ib);
 }
 
-template <int J, int kTokPerWave>
-__device__ void route_tokens(const RouteParams &P, int tt, int wv, int lane, uint32_t *smask,
-                             const float (*lg)[kMaxExperts]) {
-    constexpr int N = 64 * J;
-    float g[kTokPerWave][J];
-    int id[kTokPerWave][J];
-    int tok[kTokPerWave];
-    bool tv[kTokPerWave];
+// Wavefront arg-max under `before`: every lane ends with the same (g, id).
+__device__ __forceinline__ void wave_first(float &g, int &id, int lane) {
 #pragma unroll
-    for (int m = 0; m < kTokPerWave; ++m) {
-        const int tl = wv + 4 * m;
-        tok[m] = tt * kRouteTile + tl;
-        tv[m] = tok[m] < P.T;
-#pragma unroll
-        for (int j = 0; j < J; ++j) {
-            const int e = lane + 64 * j;
-            id[m][j] = e;
-            g[m][j] = (tv[m] && e < P.E) ? lg[tl][e] : -INFINITY;
-        }
+    for (int st = 1; st < 64; st <<= 1) {
+        const float og = __uint_as_float(xor_lane_rt(__float_as_uint(g), st, lane));
+        const int oi = (int)xor_lane_rt((uint32_t)id, st, lane);
+        const bool take = before(og, oi, g, id);
+        g = take ? og : g;
+        id = take ? oi : id;
     }
-    bool any = false;
-#pragma unroll
-    for (int m = 0; m < kTokPerWave; ++m) any |= tv[m];
-    if (!any) return;
-    // bitonic sort, "smaller" = comes first in pi
+}
+
+// Sum over the wavefront of one value per lane, in one fixed order, returned
+// identically to every lane.
+__device__ __forceinline__ float wave_sum(float v) { return lane_value(wave_scan_f32(v), 63); }
+
+// Full bitonic sort of (g, id) into pi order over 64*J lanes/registers.
+template <int J>
+__device__ __forceinline__ void sort_pi(float (&g)[J], int (&id)[J], int lane) {
+    constexpr int N = 64 * J;
 #pragma unroll
     for (int k = 2; k <= N; k <<= 1) {
 #pragma unroll
@@ -79,200 +132,236 @@ __device__ void route_tokens(const RouteParams &P, int tt, int wv, int lane, uin
                     if (j & js) continue;
                     const int jp = j | js;
                     const bool asc = ((j * 64 + lane) & k) == 0;
-#pragma unroll
-                    for (int m = 0; m < kTokPerWave; ++m) {
-                        const bool f = before(g[m][j], id[m][j], g[m][jp], id[m][jp]);
-                        if (f != asc) {
-                            float tg = g[m][j];
-                            g[m][j] = g[m][jp];
-                            g[m][jp] = tg;
-                            int ti = id[m][j];
-                            id[m][j] = id[m][jp];
-                            id[m][jp] = ti;
-                        }
-                    }
+                    const bool sw = before(g[j], id[j], g[jp], id[jp]) != asc;
+                    const float ga = g[j], gb = g[jp];
+                    const int ia = id[j], ib = id[jp];
+                    g[j] = sw ? gb : ga;
+                    g[jp] = sw ? ga : gb;
+                    id[j] = sw ? ib : ia;
+                    id[jp] = sw ? ia : ib;
                 }
             } else {
                 const bool lower = (lane & st) == 0;
 #pragma unroll
                 for (int j = 0; j < J; ++j) {
-                    const bool asc = ((j * 64 + lane) & k) == 0;
-#pragma unroll
-                    for (int m = 0; m < kTokPerWave; ++m) {
-                        const float og = __shfl_xor(g[m][j], st, 64);
-                        const int oi = __shfl_xor(id[m][j], st, 64);
-                        const bool f = before(g[m][j], id[m][j], og, oi);
-                        if (f != (lower == asc)) {
-                            g[m][j] = og;
-                            id[m][j] = oi;
-                        }
-                    }
+                    const bool keep_first = lower == (((j * 64 + lane) & k) == 0);
+                    const float og = __uint_as_float(xor_lane_rt(__float_as_uint(g[j]), st, lane));
+                    const int oi = (int)xor_lane_rt((uint32_t)id[j], st, lane);
+                    const bool sw = before(g[j], id[j], og, oi) != keep_first;
+                    g[j] = sw ? og : g[j];
+                    id[j] = sw ? oi : id[j];
                 }
             }
         }
     }
+}
+
+// Output slot `pos` of token t holds expert e (kept) or nothing.
+__device__ __forceinline__ void emit_slot(const RouteParams &P, int t, int pos, int e, float g,
+                                          bool kept, uint32_t *sm) {
     const bool sig = (P.flags & PP_AGG_SIGMOID) != 0;
+    const float w = sig ? 1.0f / (1.0f + expf(-g)) : 1.0f;
+    P.idx[(size_t)t * P.E + pos] = kept ? e : -1;
+    if (P.gate_w) P.gate_w[(size_t)t * P.E + pos] = kept ? w : 0.0f;
+    if (kept) {
+        P.gsig[(size_t)t * P.E + e] = w;
+        atomicOr(&sm[e >> 5], 1u << (e & 31));
+    }
+}
+
+// Records token t (< 64) in the per-expert masks of the decode plan.
+__device__ __forceinline__ void mark_expert(const RouteParams &P, int t, int e) {
+    __hip_atomic_fetch_or(P.emask + e, 1ull << t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Routes token t in one wavefront (the whole workgroup).
+template <int J>
+__device__ void route_token(const RouteParams &P, int t, int lane, uint32_t *sm, int *kept_e) {
+    const float *lgt = P.glog + (size_t)t * P.E;
     const bool strict = (P.flags & PP_SELECT_STRICT) != 0;
+    const bool all = strict ? (P.tau > 1.0f) : (P.tau >= 1.0f);
+    float g[J];
+    int id[J];
+    float gmx = -INFINITY;
 #pragma unroll
-    for (int m = 0; m < kTokPerWave; ++m) {
-        const float gmax = __shfl(g[m][0], 0, 64);
-        float ex[J];
-        float part = 0.0f;
+    for (int j = 0; j < J; ++j) {
+        const int e = lane + 64 * j;
+        id[j] = e;
+        g[j] = (e < P.E) ? lgt[e] : -INFINITY;
+        gmx = fmaxf(gmx, g[j]);
+    }
+    // g_max and S = sum_i exp(g_i - g_max), identical on all lanes
+#pragma unroll
+    for (int st = 1; st < 64; st <<= 1)
+        gmx = fmaxf(gmx, __uint_as_float(xor_lane_rt(__float_as_uint(gmx), st, lane)));
+    float part = 0.0f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) part += (id[j] < P.E) ? expf(g[j] - gmx) : 0.0f;
+    const float S = wave_sum(part);
+    if (lane < 8) sm[lane] = 0u;
+    __builtin_amdgcn_wave_barrier();
+
+    int k = 0;
+    bool done = false;
+    if (!all) {
+        // repeated arg-max: the next expert of pi and its cumulative mass
+        bool rm[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j) rm[j] = id[j] >= P.E;
+        float c = 0.0f;
+        int m = 0;  // strict: #{i < E : C_i < tau} so far
+        for (int pos = 0; pos < kMaxIterative && pos < P.E; ++pos) {
+            float bg = -INFINITY;
+            int bid = 0x7fffffff;
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const bool tk = !rm[j] && before(g[j], id[j], bg, bid);
+                bg = tk ? g[j] : bg;
+                bid = tk ? id[j] : bid;
+            }
+            wave_first(bg, bid, lane);
+#pragma unroll
+            for (int j = 0; j < J; ++j) rm[j] = rm[j] || id[j] == bid;
+            c += expf(bg - gmx);
+            const float C = c / S;
+            const bool below = pos < P.E - 1 && C < P.tau;
+            bool keep, stop;
+            if (strict) {
+                keep = (pos == 0) || below;
+                if (below) m = pos + 1;
+                stop = !below;
+            } else {
+                keep = true;
+                stop = (C >= P.tau) || (pos == P.E - 1);
+            }
+            if (keep && lane == 0) {
+                emit_slot(P, t, pos, bid, bg, true, sm);
+                kept_e[pos] = bid;
+            }
+            if (stop) {
+                k = strict ? (m < 1 ? 1 : m) : pos + 1;
+                done = true;
+                break;
+            }
+        }
+        if (done) {
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const int pos = j * 64 + lane;
+                if (pos >= k && pos < P.E) {
+                    P.idx[(size_t)t * P.E + pos] = -1;
+                    if (P.gate_w) P.gate_w[(size_t)t * P.E + pos] = 0.0f;
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+            if (P.build_plan && lane < k) mark_expert(P, t, kept_e[lane]);
+        } else {
+            // more than kMaxIterative kept experts: start over with a full sort
+            __builtin_amdgcn_wave_barrier();
+            if (lane < 8) sm[lane] = 0u;
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+    if (!done) {
+        sort_pi<J>(g, id, lane);
+        float cs[J];
+        float carry = 0.0f;
 #pragma unroll
         for (int j = 0; j < J; ++j) {
-            ex[j] = (id[m][j] < P.E) ? expf(g[m][j] - gmax) : 0.0f;
-            part += ex[j];
+            const float ex = (id[j] < P.E) ? expf(g[j] - gmx) : 0.0f;
+            cs[j] = wave_scan_f32(ex) + carry;
+            carry = lane_value(cs[j], 63);
         }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
-        const float S = __shfl(part, 0, 64);
-        float carry = 0.0f;
         int mcount = 0;
 #pragma unroll
         for (int j = 0; j < J; ++j) {
-            float c = ex[j] / S;
-#pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const float n = __shfl_up(c, o, 64);
-                if (lane >= o) c += n;
-            }
-            c += carry;
-            carry = __shfl(c, 63, 64);
             const int pos = j * 64 + lane;
-            mcount += __popcll(__ballot(pos < P.E - 1 && c < P.tau));
+            mcount += __popcll(__ballot(pos < P.E - 1 && cs[j] / S < P.tau));
         }
-        int k;
         if (strict) {
             k = mcount + (P.tau > 1.0f ? 1 : 0);
             k = k < 1 ? 1 : k;
         } else {
-            k = (P.tau >= 1.0f) ? P.E : min(P.E, mcount + 1);
+            k = all ? P.E : min(P.E, mcount + 1);
         }
-        if (!tv[m]) continue;
-        const int t = tok[m];
-        if (lane < 8) smask[m * 8 + lane] = 0u;
-        __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int j = 0; j < J; ++j) {
             const int pos = j * 64 + lane;
-            const int e = id[m][j];
             if (pos < P.E) {
-                const float w = sig ? 1.0f / (1.0f + expf(-g[m][j])) : 1.0f;
-                P.idx[(size_t)t * P.E + pos] = pos < k ? e : -1;
-                if (P.gate_w) P.gate_w[(size_t)t * P.E + pos] = pos < k ? w : 0.0f;
-                if (e < P.E) P.gsig[(size_t)t * P.E + e] = w;
-                if (pos < k && e < P.E) atomicOr(&smask[m * 8 + (e >> 5)], 1u << (e & 31));
+                emit_slot(P, t, pos, id[j], g[j], pos < k, sm);
+                if (P.build_plan && pos < k) mark_expert(P, t, id[j]);
             }
         }
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
-        if (lane < 8) P.selmask[(size_t)t * 8 + lane] = smask[m * 8 + lane];
-        if (lane == 0) P.count[t] = k;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    if (lane < 8) P.selmask[(size_t)t * 8 + lane] = sm[lane];
+    if (lane == 0) P.count[t] = k;
+}
+
+// Decode plan for a batch of T <= 64 tokens, built by one wavefront from the
+// per-expert token masks: groups = experts kept by at least one token
+// (ascending expert index); group u owns pair rows [pair_u, pair_u + n_u),
+// one per token, tokens ascending.  The masks are cleared for the next call.
+__device__ void build_decode_plan(const RouteParams &P, int lane) {
+    constexpr int kPer = kMaxExperts / 64;
+    uint64_t m[kPer];
+    int pc[kPer];
+    int tot = 0;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int e = lane * kPer + q;  // consecutive experts per lane keep the order ascending
+        m[q] = e < P.E ? __hip_atomic_load(P.emask + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                       : 0ull;
+        if (e < P.E && m[q]) P.emask[e] = 0ull;
+        pc[q] = __popcll(m[q]);
+        tot += m[q] != 0;
+    }
+    // exclusive prefixes over lanes of (groups, pairs)
+    int pairs = 0;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) pairs += pc[q];
+    const int incl_g = wave_incl_scan(tot), incl_p = wave_incl_scan(pairs);
+    int slot = incl_g - tot, poff = incl_p - pairs;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        if (!m[q]) continue;
+        const int e = lane * kPer + q;
+        P.plan.grp_e[slot] = e;
+        P.plan.grp_pair[slot] = poff;
+        P.plan.grp_n[slot] = pc[q];
+        P.plan.grp_tok[slot] = poff;
+        int r = 0;
+        for (uint64_t mm = m[q]; mm; mm &= mm - 1) P.plan.toklist[poff + r++] = __builtin_ctzll(mm);
+        ++slot;
+        poff += pc[q];
+    }
+    if (lane == 63) {
+        P.plan.head[0] = incl_g;
+        P.plan.head[1] = incl_p;
     }
 }
 
+// One wavefront per token; with a decode plan the last token to finish
+// builds it.
 template <int J>
-__global__ __launch_bounds__(256) void route_k(RouteParams P) {
-    __shared__ f32x4 red[4][64];
-    __shared__ uint32_t smask[4][4 * 8];
+__global__ __launch_bounds__(64) void select_k(RouteParams P) {
+    __shared__ uint32_t sm[8];
+    __shared__ int kept_e[kMaxIterative];
     __shared__ int s_last;
-    __shared__ float lg[kRouteTile][kMaxExperts];
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int per_tile = P.nEt * P.KSr;
-    const int tt = blockIdx.x / per_tile;
-    const int rem = blockIdx.x % per_tile;
-    const int et = rem / P.KSr, ks = rem % P.KSr;
-    const int s0 = (int)((long)ks * P.NS / P.KSr), s1 = (int)((long)(ks + 1) * P.NS / P.KSr);
-    const int tr = tt * kRouteTile + (lane & 15);
-    const int ec = et * kRouteTile + (lane & 15);
-    const int koff = 8 * (lane >> 4);
-    const bool va = tr < P.T, vb = ec < P.E;
-    const uint16_t *xa = P.x + (size_t)(va ? tr : 0) * P.d + koff;
-    const uint16_t *wb = P.Wr + (size_t)(vb ? ec : 0) * P.d + koff;
-    const uint4 z = make_uint4(0, 0, 0, 0);
-    // a slice has at most kRouteSliceSteps = 16 K-steps: four per wavefront
-    uint4 a[4], b[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int s = s0 + wv + 4 * i;
-        const bool ok = s < s1;
-        a[i] = (ok && va) ? ldg16(xa + s * kKStep) : z;
-        b[i] = (ok && vb) ? ldg16(wb + s * kKStep) : z;
-    }
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) acc = mfma16(a[i], b[i], acc);
-    red[wv][lane] = acc;
-    __syncthreads();
-    if (wv == 0) {
-        f32x4 r = red[0][lane];
-        r += red[1][lane];
-        r += red[2][lane];
-        r += red[3][lane];
-        // MFMA 16x16 result: lane holds rows 4*(lane/16)+i (tokens), column lane%16 (expert)
-        const int e = et * kRouteTile + (lane & 15);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int t = tt * kRouteTile + 4 * (lane >> 4) + i;
-            if (t < P.T && e < P.E) st_dev(P.gpart + ((size_t)ks * P.T + t) * P.E + e, r[i]);
-        }
-    }
-    if (!arrive_last(&P.cnt[tt], (unsigned)per_tile, &s_last)) return;
-    // logits of the tile's tokens: slices summed in slice order (fixed), then
-    // bias and temperature; all loads of a batch are issued before any add
-    const int nt = min(kRouteTile, P.T - tt * kRouteTile);
-    const int n_el = nt * P.E;
-    for (int base = 0; base < n_el; base += 4 * 256) {
-        float v[4][kRouteMaxSlices];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = base + q * 256 + threadIdx.x;
-            const bool ok = i < n_el;
-            const int t = tt * kRouteTile + (ok ? i / P.E : 0), e = ok ? i % P.E : 0;
-#pragma unroll
-            for (int k = 0; k < kRouteMaxSlices; ++k)
-                v[q][k] = (ok && k < P.KSr) ? ld_dev(P.gpart + ((size_t)k * P.T + t) * P.E + e)
-                                            : 0.0f;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = base + q * 256 + threadIdx.x;
-            if (i < n_el) {
-                float sum = 0.0f;
-#pragma unroll
-                for (int k = 0; k < kRouteMaxSlices; ++k)
-                    if (k < P.KSr) sum += v[q][k];
-                const int tl = i / P.E, e = i % P.E;
-                const int t = tt * kRouteTile + tl;
-                const float it = P.inv_temp ? P.inv_temp[t] : 1.0f;
-                lg[tl][e] = (sum + P.bias[e]) * it;
-            }
-        }
-    }
-    __syncthreads();
-    // four wavefronts share the tile's tokens
-    const int tpw = (nt + 3) / 4;
-    if (tpw == 1)
-        route_tokens<J, 1>(P, tt, wv, lane, smask[wv], lg);
-    else if (tpw == 2)
-        route_tokens<J, 2>(P, tt, wv, lane, smask[wv], lg);
-    else
-        route_tokens<J, 4>(P, tt, wv, lane, smask[wv], lg);
+    const int lane = threadIdx.x;
+    route_token<J>(P, blockIdx.x, lane, sm, kept_e);
+    if (!P.build_plan) return;
+    if (!arrive_last(P.plan_cnt, (unsigned)P.T, &s_last)) return;
+    build_decode_plan(P, lane);
 }
 
 }  // namespace
 
-// The K-slices depend on d only, never on T, so a token's logits are summed
-// in the same order whatever batch it arrives in (routing is batch-invariant:
-// decode slices and one large prefill batch select identically).
-int route_split(const pp_dims &dm, int T) {
-    (void)T;
-    const int ks = (dm.NS + kRouteSliceSteps - 1) / kRouteSliceSteps;
-    return ks < 1 ? 1 : ks;
-}
-
 hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const float *inv_temp,
-                        int32_t *idx, int32_t *count, float *gate_w, hipStream_t s) {
+                        int32_t *idx, int32_t *count, float *gate_w, bool build_plan,
+                        hipStream_t s) {
     const pp_dims &dm = L->dm;
     RouteParams P;
     P.x = x;
@@ -285,24 +374,26 @@ hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const 
     P.inv_temp = inv_temp;
     P.tau = tau;
     P.flags = L->flags;
-    P.KSr = route_split(dm, T);
     P.nEt = (dm.E + kRouteTile - 1) / kRouteTile;
-    P.gpart = L->gpart;
-    P.cnt = L->counters;  // route region comes first
+    P.glog = L->gpart;
     P.idx = idx;
     P.count = count;
     P.gate_w = gate_w;
     P.selmask = L->selmask;
     P.gsig = L->gsig;
+    P.plan = plan_view(L, false);
+    P.build_plan = (build_plan && T <= kDecodeTile) ? 1 : 0;
+    P.emask = L->emask;
+    P.plan_cnt = L->counters;  // the router's counter comes first
     const int nTt = (T + kRouteTile - 1) / kRouteTile;
-    const dim3 grid(nTt * P.nEt * P.KSr);
     prof_mark(L, PP_KERNEL_ROUTE, s, true);
+    hipLaunchKernelGGL(logits_k, dim3(nTt * P.nEt), dim3(1024), 0, s, P);
     if (dm.E <= 64)
-        hipLaunchKernelGGL(route_k<1>, grid, dim3(256), 0, s, P);
+        hipLaunchKernelGGL(select_k<1>, dim3(T), dim3(64), 0, s, P);
     else if (dm.E <= 128)
-        hipLaunchKernelGGL(route_k<2>, grid, dim3(256), 0, s, P);
+        hipLaunchKernelGGL(select_k<2>, dim3(T), dim3(64), 0, s, P);
     else
-        hipLaunchKernelGGL(route_k<4>, grid, dim3(256), 0, s, P);
+        hipLaunchKernelGGL(select_k<4>, dim3(T), dim3(64), 0, s, P);
     prof_mark(L, PP_KERNEL_ROUTE, s, false);
     return hipGetLastError();
 }
