@@ -152,7 +152,7 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
 
     const size_t dE = (size_t)d * E;
     const counter_layout cl = counters_for(L->dm, max_tokens);
-    L->gpart_elems = (size_t)max_tokens * E;
+    L->gpart_elems = (size_t)((L->dm.NS + 15) / 16) * max_tokens * E;
     L->n_counters = cl.total;
     L->max_pairs = (size_t)max_tokens * E;
     L->ypart_elems = (size_t)32 * kDecodeTile * d;  // at most 32 expert chunks of a 64-token slice

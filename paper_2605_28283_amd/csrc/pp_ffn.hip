@@ -3,7 +3,8 @@
 //
 // Work is organised in "groups" listed by a plan: one expert with up to 64 of
 // the tokens that kept it.  A decode batch (T <= 64) has one group per expert
-// in the batch union (the router writes that plan); prefill splits each
+// in the batch union (gateup_k derives that plan from the router's per-expert
+// token masks and stores it for the down projection); prefill splits each
 // expert's token bucket into groups of 64 (dispatch_k writes that plan).  Each
 // (token, expert) pair owns one row of the h scratch; rows are numbered group
 // by group, tokens ascending inside a group.
@@ -24,7 +25,8 @@
 //               multiplies its 64x128 down block with the group's compact token
 //               tiles (two MFMAs per fragment: hi and lo) and adds the result
 //               into its own LDS accumulator [tokens][64 rows] -- no
-//               synchronisation inside the chunk.  The four accumulators are
+//               synchronisation inside the chunk; the next group's fragments
+//               are loaded while the current one is multiplied.  The four accumulators are
 //               summed in wavefront order; chunks are summed in chunk order by
 //               the last to arrive.  No float atomics: decode is deterministic.
 //   dispatch_k: prefill bucketing (per expert, the ascending list of tokens
@@ -43,6 +45,7 @@ constexpr int kGuThreads = 512;
 constexpr int kPF = 2;          // K-steps per register buffer in gateup_k (two buffers)
 constexpr int kDnRows = 64;     // rows of d per decode down unit
 constexpr int kMaxChunks = 32;  // expert chunks of the decode down projection
+constexpr int kDnMinPerChunk = 8;  // experts per chunk at least (two per wavefront)
 
 struct GUParams {
     const uint16_t *x;
@@ -51,6 +54,7 @@ struct GUParams {
     const float *gsig;
     uint32_t flags;
     PlanView plan;
+    const unsigned long long *emask;  // decode: tokens that kept each expert
     float *abpart;
     size_t abpart_rows;
     uint32_t *cnt;
@@ -200,44 +204,115 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
         }
     }
     if (!arrive_last(&P.cnt[g], (unsigned)KS, flag)) return;
-    for (int i = tid; i < n * (kExpertWidth / 2); i += blockDim.x) {
-        const int q = i >> 6, r = 2 * (i & 63);
-        float2 a = make_float2(0.f, 0.f), b = make_float2(0.f, 0.f);
-        for (int k0 = 0; k0 < KS; k0 += 4) {
-            float2 u[4], v[4];
+    // (a, b) of the group's n x 128 block = sum of the slice partials in slice
+    // order; a thread owns up to kRedPer float2 of it and issues the loads of
+    // kRedSlices slices at once
+    constexpr int kRedPer = 2;
+    constexpr int kRedSlices = 4;
+    const int nel = n * (kExpertWidth / 2);
+    const size_t slice = (size_t)npairs * 256;
+    for (int i0 = 0; i0 < nel; i0 += kRedPer * kGuThreads) {
+        float2 a[kRedPer], b[kRedPer];
+        int off[kRedPer];
+        const int nq = (nel - i0 - tid + kGuThreads - 1) / kGuThreads;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                u[k] = v[k] = make_float2(0.f, 0.f);
-                if (k0 + k < KS) {
-                    const float *row = P.abpart + ((size_t)(k0 + k) * npairs + p0 + q) * 256;
-                    u[k] = ld_dev2(row + r);
-                    v[k] = ld_dev2(row + 128 + r);
+        for (int q = 0; q < kRedPer; ++q) {
+            const int i = min(i0 + tid + kGuThreads * q, nel - 1);
+            off[q] = (p0 + (i >> 6)) * 256 + 2 * (i & 63);
+            a[q] = b[q] = make_float2(0.f, 0.f);
+        }
+        for (int k0 = 0; k0 < KS; k0 += kRedSlices) {
+            float2 u[kRedSlices][kRedPer], v[kRedSlices][kRedPer];
+#pragma unroll
+            for (int k = 0; k < kRedSlices; ++k) {
+                const float *base = P.abpart + (size_t)min(k0 + k, KS - 1) * slice;
+#pragma unroll
+                for (int q = 0; q < kRedPer; ++q) {
+                    u[k][q] = q < nq ? ld_dev2(base + off[q]) : make_float2(0.f, 0.f);
+                    v[k][q] = q < nq ? ld_dev2(base + off[q] + 128) : make_float2(0.f, 0.f);
                 }
             }
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                a.x += u[k].x;
-                a.y += u[k].y;
-                b.x += v[k].x;
-                b.y += v[k].y;
+            for (int k = 0; k < kRedSlices; ++k)
+                if (k0 + k < KS)
+#pragma unroll
+                    for (int q = 0; q < kRedPer; ++q) {
+                        a[q].x += u[k][q].x;
+                        a[q].y += u[k][q].y;
+                        b[q].x += v[k][q].x;
+                        b[q].y += v[k][q].y;
+                    }
+        }
+#pragma unroll
+        for (int q = 0; q < kRedPer; ++q) {
+            if (q < nq) {
+                const int i = i0 + tid + kGuThreads * q;
+                const int qq = i >> 6, r = 2 * (i & 63);
+                const float scl = sig ? P.gsig[(size_t)stok[qq] * P.E + e] : 1.0f;
+                uint16_t h0, l0, h1, l1;
+                split_bf16(silu(a[q].x) * b[q].x * scl, h0, l0);
+                split_bf16(silu(a[q].y) * b[q].y * scl, h1, l1);
+                const size_t o = (size_t)(p0 + qq) * kExpertWidth + r;
+                *reinterpret_cast<uint32_t *>(P.h_hi + o) = h0 | ((uint32_t)h1 << 16);
+                *reinterpret_cast<uint32_t *>(P.h_lo + o) = l0 | ((uint32_t)l1 << 16);
             }
         }
-        const float scl = sig ? P.gsig[(size_t)stok[q] * P.E + e] : 1.0f;
-        uint16_t h0, l0, h1, l1;
-        split_bf16(silu(a.x) * b.x * scl, h0, l0);
-        split_bf16(silu(a.y) * b.y * scl, h1, l1);
-        const size_t o = (size_t)(p0 + q) * kExpertWidth + r;
-        *reinterpret_cast<uint32_t *>(P.h_hi + o) = h0 | ((uint32_t)h1 << 16);
-        *reinterpret_cast<uint32_t *>(P.h_lo + o) = l0 | ((uint32_t)l1 << 16);
     }
 }
 
+// Decode plan, derived by every workgroup from the per-expert token masks:
+// groups = experts kept by at least one token, ascending; group u owns pair
+// rows [pair_u, pair_u + popcount(mask_u)), tokens ascending.  Workgroup 0
+// also stores it for the down projection.
+struct DecodePlan {
+    unsigned long long mask[kMaxExperts];
+    int e[kMaxExperts];
+    int pair[kMaxExperts];
+    int scan[2 * (kGuThreads / 64)];
+    int nG, npairs;
+};
+
+__device__ void decode_plan(const GUParams &P, DecodePlan &D) {
+    const int tid = threadIdx.x, e = tid;
+    const unsigned long long m = (e < P.E) ? P.emask[e] : 0ull;
+    const int act = m != 0ull ? 1 : 0, pc = __popcll(m);
+    int slot, poff, nG, npairs;
+    block_excl_scan2(act, pc, &slot, &poff, &nG, &npairs, D.scan);
+    if (act) {
+        D.mask[slot] = m;
+        D.e[slot] = e;
+        D.pair[slot] = poff;
+        if (blockIdx.x == 0) {
+            P.plan.grp_e[slot] = e;
+            P.plan.grp_pair[slot] = poff;
+            P.plan.grp_n[slot] = pc;
+            P.plan.grp_tok[slot] = poff;
+            int r = 0;
+            for (unsigned long long mm = m; mm; mm &= mm - 1)
+                P.plan.toklist[poff + r++] = __builtin_ctzll(mm);
+        }
+    }
+    if (tid == 0) {
+        D.nG = nG;
+        D.npairs = npairs;
+        if (blockIdx.x == 0) {
+            P.plan.head[0] = nG;
+            P.plan.head[1] = npairs;
+        }
+    }
+    __syncthreads();
+}
+
+template <int MODE>
 __global__ __launch_bounds__(kGuThreads, 4) void gateup_k(GUParams P) {
     __shared__ uint4 xf[kXBufBytes / 16];
     __shared__ int stok[kGroupTokens];
     __shared__ int s_flag;
+    __shared__ DecodePlan D;
     const int tid = threadIdx.x;
-    const int nG = P.plan.head[0], npairs = P.plan.head[1];
+    if (MODE == 0) decode_plan(P, D);
+    const int nG = MODE == 0 ? D.nG : P.plan.head[0];
+    const int npairs = MODE == 0 ? D.npairs : P.plan.head[1];
     // K-slices per group: as many as keep every unit in the one round of
     // resident workgroups (gridDim.x), each slice at least kMinStepsPerSlice
     int KS = (int)gridDim.x / nG;
@@ -248,9 +323,19 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_k(GUParams P) {
     const int units = nG * KS;
     for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
         const int g = unit / KS, ks = unit - g * KS;
-        const int e = P.plan.grp_e[g], n = P.plan.grp_n[g], p0 = P.plan.grp_pair[g];
-        const int tk = P.plan.grp_tok[g];
-        if (tid < n) stok[tid] = P.plan.toklist[tk + tid];
+        int e, n, p0;
+        if (MODE == 0) {
+            const unsigned long long m = D.mask[g];
+            e = D.e[g];
+            n = __popcll(m);
+            p0 = D.pair[g];
+            if (tid < 64 && ((m >> tid) & 1ull)) stok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
+        } else {
+            e = P.plan.grp_e[g];
+            n = P.plan.grp_n[g];
+            p0 = P.plan.grp_pair[g];
+            if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
+        }
         __syncthreads();
         switch ((n + 15) >> 4) {
         case 1: gateup_unit<1>(P, e, n, p0, g, ks, KS, npairs, stok, xf, &s_flag); break;
@@ -264,69 +349,125 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_k(GUParams P) {
 
 // ------------------------------------------------------------------ down (decode)
 
+// Half of one expert's decode down work, as held in registers by a
+// wavefront: 32 rows of its 64-row down block (2 row tiles x 4 K-steps of A
+// fragments) and the B fragments (h hi and lo) of its first 16 tokens.
+struct DownItem {
+    uint4 w[2][4];
+    uint4 bh[4], bl[4];
+    int tok, n, p0, tk, half;
+};
+
+__device__ __forceinline__ void load_down_item(const DNParams &P, int u, int half, int rb, int RT,
+                                               int lane, DownItem &it) {
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    const int e = P.plan.grp_e[u];
+    it.n = P.plan.grp_n[u];
+    it.p0 = P.plan.grp_pair[u];
+    it.tk = P.plan.grp_tok[u];
+    it.half = half;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+        const uint16_t *wp =
+            P.Wd + (((size_t)e * RT + rb * 4 + 2 * half + mt) * 4 * 64 + lane) * 8;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) it.w[mt][s] = ldg16(wp + s * 512);
+    }
+    const int slot = lane & 15;
+    const bool ok = slot < it.n;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const size_t o = (size_t)(it.p0 + slot) * kExpertWidth + s * kKStep + 8 * (lane >> 4);
+        it.bh[s] = ok ? ldg16(P.h_hi + o) : z;
+        it.bl[s] = ok ? ldg16(P.h_lo + o) : z;
+    }
+    it.tok = ok ? P.plan.toklist[it.tk + slot] : 0;
+}
+
+// acc[t][32 rows of the item's half] += the item's 32 x n block (the first
+// tile of 16 tokens comes with the item; further tiles are loaded here).
+template <int YS>
+__device__ __forceinline__ void apply_down_item(const DNParams &P, const DownItem &it, int lane,
+                                                float (*acc)[YS]) {
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    for (int j = 0; j * 16 < it.n; ++j) {
+        uint4 bh[4], bl[4];
+        int t;
+        const int slot = 16 * j + (lane & 15);
+        const bool ok = slot < it.n;
+        if (j == 0) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                bh[s] = it.bh[s];
+                bl[s] = it.bl[s];
+            }
+            t = it.tok;
+        } else {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const size_t o =
+                    (size_t)(it.p0 + slot) * kExpertWidth + s * kKStep + 8 * (lane >> 4);
+                bh[s] = ok ? ldg16(P.h_hi + o) : z;
+                bl[s] = ok ? ldg16(P.h_lo + o) : z;
+            }
+            t = ok ? P.plan.toklist[it.tk + slot] : 0;
+        }
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+            f32x4 a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                a = mfma16(it.w[mt][s], bh[s], a);
+                a = mfma16(it.w[mt][s], bl[s], a);
+            }
+            if (ok) {
+                float4 *dst = reinterpret_cast<float4 *>(
+                    &acc[t][(2 * it.half + mt) * 16 + 4 * (lane >> 4)]);
+                float4 v = *dst;
+                v.x += a[0];
+                v.y += a[1];
+                v.z += a[2];
+                v.w += a[3];
+                *dst = v;
+            }
+        }
+    }
+}
+
 template <int TB>
-__global__ __launch_bounds__(256) void down_dec_k(DNParams P) {
+__global__ __launch_bounds__(256, 2) void down_dec_k(DNParams P) {
     constexpr int YS = kDnRows + 4;  // padded row stride of an accumulator
     __shared__ float yacc[4][TB][YS];
     __shared__ int s_flag;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int nU = P.plan.head[0];
     const int n_rb = P.d / kDnRows, RT = P.d / 16;
-    int ES = (int)gridDim.x / n_rb;  // expert chunks: one round of resident workgroups
-    if (ES > nU) ES = nU;
+    // expert chunks: enough units for the resident workgroups, but at least
+    // kDnMinPerChunk experts per chunk so each wavefront streams a pipeline
+    int ES = (int)gridDim.x / n_rb;
+    if (ES > nU / kDnMinPerChunk) ES = nU / kDnMinPerChunk;
     if (ES > kMaxChunks) ES = kMaxChunks;
     if (ES > 1 && (size_t)ES * P.T * P.d > P.ypart_elems) ES = (int)(P.ypart_elems / ((size_t)P.T * P.d));
     if (ES < 1) ES = 1;
     const int Uc = (nU + ES - 1) / ES;
     ES = (nU + Uc - 1) / Uc;
     const int units = n_rb * ES;
-    const uint4 z = make_uint4(0, 0, 0, 0);
     float(*acc_w)[YS] = yacc[wv];
 
     for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
         const int c = unit / n_rb, rb = unit - c * n_rb;
         for (int i = lane; i < P.T * YS; i += 64) acc_w[i / YS][i % YS] = 0.0f;
-        const int u1 = min(nU, (c + 1) * Uc);
-        for (int u = c * Uc + wv; u < u1; u += 4) {
-            const int e = P.plan.grp_e[u], n = P.plan.grp_n[u], p0 = P.plan.grp_pair[u];
-            const int tk = P.plan.grp_tok[u];
-            uint4 w[4][4];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                const uint16_t *wp = P.Wd + (((size_t)e * RT + rb * 4 + mt) * 4 * 64 + lane) * 8;
-#pragma unroll
-                for (int s = 0; s < 4; ++s) w[mt][s] = ldg16(wp + s * 512);
-            }
-            for (int j = 0; j * 16 < n; ++j) {
-                const int slot = 16 * j + (lane & 15);
-                const bool ok = slot < n;
-                uint4 bh[4], bl[4];
-#pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    const size_t o = (size_t)(p0 + slot) * kExpertWidth + s * kKStep + 8 * (lane >> 4);
-                    bh[s] = ok ? ldg16(P.h_hi + o) : z;
-                    bl[s] = ok ? ldg16(P.h_lo + o) : z;
-                }
-                const int t = ok ? P.plan.toklist[tk + slot] : 0;
-#pragma unroll
-                for (int mt = 0; mt < 4; ++mt) {
-                    f32x4 a = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int s = 0; s < 4; ++s) {
-                        a = mfma16(w[mt][s], bh[s], a);
-                        a = mfma16(w[mt][s], bl[s], a);
-                    }
-                    if (ok) {
-                        float4 *dst = reinterpret_cast<float4 *>(&acc_w[t][mt * 16 + 4 * (lane >> 4)]);
-                        float4 v = *dst;
-                        v.x += a[0];
-                        v.y += a[1];
-                        v.z += a[2];
-                        v.w += a[3];
-                        *dst = v;
-                    }
-                }
-            }
+        // this wavefront's items: q -> (group c*Uc + wv + 4*(q/2), half q%2);
+        // two items in flight, so the next item's loads overlap this one's math
+        const int u0 = c * Uc + wv, u1 = min(nU, (c + 1) * Uc);
+        const int nq = u0 < u1 ? 2 * ((u1 - u0 + 3) / 4) : 0;
+        DownItem A, B;
+        if (nq > 0) load_down_item(P, u0, 0, rb, RT, lane, A);
+        for (int q = 0; q < nq; q += 2) {
+            load_down_item(P, u0 + 4 * (q >> 1), 1, rb, RT, lane, B);
+            apply_down_item<YS>(P, A, lane, acc_w);
+            if (q + 2 < nq) load_down_item(P, u0 + 4 * ((q + 2) >> 1), 0, rb, RT, lane, A);
+            apply_down_item<YS>(P, B, lane, acc_w);
         }
         __syncthreads();
         // sum the four accumulators in wavefront order
@@ -351,22 +492,42 @@ __global__ __launch_bounds__(256) void down_dec_k(DNParams P) {
             }
         }
         if (ES > 1 && arrive_last(&P.cnt[rb], (unsigned)ES, &s_flag)) {
-            for (int i = tid; i < P.T * (kDnRows / 2); i += blockDim.x) {
-                const int t = i / (kDnRows / 2);
-                const size_t col = (size_t)rb * kDnRows + 2 * (i - t * (kDnRows / 2));
-                float2 v[kMaxChunks];
+            // y[t][64 rows] = sum of the chunk partials in chunk order; every
+            // thread owns up to kRedPer float2 of the block and issues the
+            // loads of kRedChunks chunks at once
+            constexpr int kRedPer = kDecodeTile * (kDnRows / 2) / 256;
+            constexpr int kRedChunks = 4;
+            const int nel = P.T * (kDnRows / 2);
+            float2 acc[kRedPer];
+            int off[kRedPer];
 #pragma unroll
-                for (int k = 0; k < kMaxChunks; ++k)
-                    v[k] = (k < ES) ? ld_dev2(P.ypart + ((size_t)k * P.T + t) * P.d + col)
-                                    : make_float2(0.f, 0.f);
-                float2 s = make_float2(0.f, 0.f);
-#pragma unroll
-                for (int k = 0; k < kMaxChunks; ++k) {
-                    s.x += v[k].x;
-                    s.y += v[k].y;
-                }
-                *reinterpret_cast<float2 *>(P.y + (size_t)t * P.d + col) = s;
+            for (int q = 0; q < kRedPer; ++q) {
+                const int i = min(tid + 256 * q, nel - 1), t = i / (kDnRows / 2);
+                off[q] = t * P.d + rb * kDnRows + 2 * (i - t * (kDnRows / 2));
+                acc[q] = make_float2(0.f, 0.f);
             }
+            const int nq = (nel - tid + 255) / 256;  // float2 owned by this thread
+            for (int k0 = 0; k0 < ES; k0 += kRedChunks) {
+                float2 v[kRedChunks][kRedPer];
+#pragma unroll
+                for (int k = 0; k < kRedChunks; ++k) {
+                    const float *base = P.ypart + (size_t)min(k0 + k, ES - 1) * P.T * P.d;
+#pragma unroll
+                    for (int q = 0; q < kRedPer; ++q)
+                        v[k][q] = q < nq ? ld_dev2(base + off[q]) : make_float2(0.f, 0.f);
+                }
+#pragma unroll
+                for (int k = 0; k < kRedChunks; ++k)
+                    if (k0 + k < ES)
+#pragma unroll
+                        for (int q = 0; q < kRedPer; ++q) {
+                            acc[q].x += v[k][q].x;
+                            acc[q].y += v[k][q].y;
+                        }
+            }
+#pragma unroll
+            for (int q = 0; q < kRedPer; ++q)
+                if (q < nq) *reinterpret_cast<float2 *>(P.y + off[q]) = acc[q];
         }
         __syncthreads();
     }
@@ -526,6 +687,7 @@ GUParams gu_params(pp_layer *L, const uint16_t *x, int T, bool prefill) {
     P.gsig = L->gsig;
     P.flags = L->flags;
     P.plan = plan_view(L, prefill);
+    P.emask = L->emask;
     P.abpart = L->abpart;
     P.abpart_rows = kAbPartRows;
     P.cnt = L->counters + cl.route;
@@ -553,10 +715,13 @@ DNParams dn_params(pp_layer *L, int T, float *y, bool prefill) {
 }
 
 hipError_t launch_gateup(pp_layer *L, const uint16_t *x, int T, bool prefill, hipStream_t s) {
-    static const int occ = resident(gateup_k, kGuThreads);
+    static const int occ0 = resident(gateup_k<0>, kGuThreads), occ1 = resident(gateup_k<1>, kGuThreads);
     const GUParams gp = gu_params(L, x, T, prefill);
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
-    hipLaunchKernelGGL(gateup_k, dim3(occ * L->num_cu), dim3(kGuThreads), 0, s, gp);
+    if (prefill)
+        hipLaunchKernelGGL(gateup_k<1>, dim3(occ1 * L->num_cu), dim3(kGuThreads), 0, s, gp);
+    else
+        hipLaunchKernelGGL(gateup_k<0>, dim3(occ0 * L->num_cu), dim3(kGuThreads), 0, s, gp);
     prof_mark(L, PP_KERNEL_GATEUP, s, false);
     return hipGetLastError();
 }
@@ -571,7 +736,7 @@ void launch_down_dec_tb(const DNParams &P, int num_cu, hipStream_t s) {
 
 counter_layout counters_for(const pp_dims &dm, int max_tokens) {
     counter_layout c;
-    c.route = 1;
+    c.route = 0;
     c.gateup = (size_t)plan_max_groups(dm, max_tokens);
     c.down = (size_t)(dm.d / kDnRows);
     c.dispatch = 1;

@@ -63,7 +63,7 @@ struct pp_layer {
     uint16_t *Wgu;     // expert-major gate/up MFMA fragments
     uint16_t *Wd;      // expert-major down MFMA fragments
     // scratch
-    float *gpart;       // router logits [max_tokens][E]
+    float *gpart;       // router K-slice partial logits [d/512][max_tokens][E]
     size_t gpart_elems;
     uint32_t *counters; // arrival counters, zero between calls
     size_t n_counters;
@@ -89,7 +89,7 @@ namespace pp {
 
 // Counter regions inside pp_layer::counters.
 struct counter_layout {
-    size_t route;     // one: the decode plan builder
+    size_t route;     // none
     size_t gateup;    // one per group
     size_t down;      // one per 64-row block
     size_t dispatch;  // one
