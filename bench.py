@@ -38,6 +38,8 @@ def parse_args():
     ap.add_argument("--copies", type=int, default=0, help="layer copies (0 = enough for 2.2 GB)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the CPU-oracle baseline (0 = skip)")
+    ap.add_argument("--no-stack", action="store_true",
+                    help="skip the 32-layer stacked decode measurement")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (5 times), the "
                          "reference dispatch for scaling HBM byte counters")
@@ -252,6 +254,10 @@ def main():
     }
     for h in handles:
         pp.prunepath_destroy(h)
+    handles = []
+    torch.cuda.empty_cache()
+    if not args.no_stack:
+        out["stack"] = bench_stack(args, torch, np, pp)
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -261,6 +267,67 @@ def main():
         torch.cuda.synchronize()
         out["calibration_copy_bytes"] = 4 * n
     print(json.dumps(out), flush=True)
+
+
+def bench_stack(args, torch, np, pp):
+    """32 LLaMA-3-8B-shaped layers chained by residual + RMSNorm, decode T=16,
+    tau=0.8, one step = all 32 layers, captured once in a HIP graph and
+    replayed; 11.3 GB of distinct weights per step, so no cache holds them."""
+    from paper_2605_28283_amd.stack import DecodeStack
+    from paper_2605_28283_amd.workloads import (WORKLOADS, bf16_to_f32, make_layer_device,
+                                                stack_layer_seed, workload_tokens)
+    w = WORKLOADS["llama8b_stack32"]
+    d, E, T, tau = w.d, w.E, w.T[0], w.taus[0]
+    handles = []
+    for l in range(w.layers):
+        W = make_layer_device(w.d, w.d_ff, w.E, stack_layer_seed(l))
+        handles.append(pp.prunepath_create(w.d, w.d_ff, w.E, T, W["W_r"], W["W_gate"],
+                                           W["W_up"], W["W_down"]))
+        del W
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    S = DecodeStack(handles, d, E, T, tau)
+    x0_bits, _ = workload_tokens(w, T)
+    S.set_input(torch.from_numpy(bf16_to_f32(x0_bits).copy()).cuda())
+    for _ in range(3):
+        S.enqueue()
+    torch.cuda.synchronize()
+    S.capture()
+    steps = max(5, args.steps // 10)
+    for _ in range(3):
+        S.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        S.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    cnt = S.cnt.cpu().numpy()
+    idx = S.idx.cpu().numpy()
+    union = [int(len(np.unique(idx[l][idx[l] >= 0]))) for l in range(w.layers)]
+    layer_bytes = [E * d * 2 + u * 6 * 128 * d + 2 * T * d + 4 * T * d + 14 * T * d
+                   for u in union]
+    hist = np.bincount(cnt.ravel(), minlength=E + 1)
+    for h in handles:
+        pp.prunepath_destroy(h)
+    gbps = sum(layer_bytes) / (ms * 1e-3) / 1e9
+    print("# stack32 T=%d tau=%.2f: %.3f ms/step (%.1f us/layer), %.0f tokens/s, "
+          "mean k %.2f, mean |U| %.1f, %.0f GB/s" % (T, tau, ms, ms * 1e3 / w.layers,
+                                                    T / (ms * 1e-3), cnt.mean(),
+                                                    np.mean(union), gbps),
+          file=sys.stderr, flush=True)
+    return {"workload": "llama8b_stack32_decode", "layers": w.layers, "T": T, "tau": tau,
+            "graph": True, "steps": steps, "ms_per_step": ms,
+            "us_per_layer": ms * 1e3 / w.layers, "tokens_per_s": T / (ms * 1e-3),
+            "tokens_per_s_layer": T / (ms * 1e-3 / w.layers),
+            "algorithmic_bytes_per_step": float(sum(layer_bytes)),
+            "effective_GBps": gbps, "frac_hbm_peak": gbps / HBM_PEAK_GBPS,
+            "k_mean_per_layer": [float(v) for v in cnt.mean(axis=1)],
+            "union_per_layer": union,
+            "k_histogram": {str(k): int(v) for k, v in enumerate(hist) if v}}
 
 
 if __name__ == "__main__":

@@ -122,6 +122,21 @@ pp_status prunepath_ffn_prefill(pp_layer *L, const uint16_t *x, int32_t T, float
                                 const float *inv_temp, float *y, int32_t *expert_idx,
                                 int32_t *count, void *hip_stream);
 
+/* prunepath_residual_rmsnorm -- the wiring between stacked FFN layers (not
+ * part of the paper's method; its stacked-layer decode workload chains layers
+ * with pre-norm residuals, x_{l+1} = x_l + FFN_l(u_l), u_l = RMSNorm(x_l)):
+ *   x_out[t, :] = x[t, :] + y[t, :]            (y NULL: x_out = x)
+ *   u[t, :]     = bf16(x_out[t, :] / sqrt(mean_j x_out[t, j]^2 + eps))
+ * with norm weight 1 and round-to-nearest-even to bf16 (u NULL: residual add
+ * only).  x, y, x_out: [T, d] fp32; u: [T, d] bf16 bits; all device pointers,
+ * owned by the caller; x, y and x_out may be the same array.  The sum of
+ * squares is fp32 in a fixed order that does not depend on T.
+ * PP_EINVAL: NULL x or x_out, T outside [1, 65536], d not a multiple of 4 or
+ * outside [4, 2^20], eps NaN or negative (when u is given), x/y/x_out not
+ * 16-byte aligned or u not 8-byte aligned. */
+pp_status prunepath_residual_rmsnorm(const float *x, const float *y, float *x_out, int32_t T,
+                                     int32_t d, float eps, uint16_t *u, void *hip_stream);
+
 /* Kernel kinds reported by prunepath_profile_end. */
 #define PP_KERNEL_ROUTE 0     /* router: logits, softmax, sort, cut */
 #define PP_KERNEL_DISPATCH 1  /* prefill token bucketing */

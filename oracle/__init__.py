@@ -47,6 +47,10 @@ def _load():
         lib.ppo_order.restype = None
         lib.ppo_cut.argtypes = [I64, P, ctypes.c_double, ctypes.c_uint, P]
         lib.ppo_cut.restype = I64
+        lib.ppo_bf16_round_n.argtypes = [I64, P, P]
+        lib.ppo_bf16_round_n.restype = None
+        lib.ppo_rmsnorm.argtypes = [I64, I64, P, ctypes.c_double, P, P]
+        lib.ppo_rmsnorm.restype = ctypes.c_int
         lib.ppo_num_threads.argtypes = []
         lib.ppo_num_threads.restype = ctypes.c_int
         _lib = lib
@@ -160,3 +164,22 @@ def order_tie(g, idx, count, band=1e-5):
         if m >= 2 and (np.diff(srt[:m]) >= -band).any():
             out[t] = True
     return out
+
+
+def bf16_round(v):
+    """bf16 bit patterns nearest to fp64 values (ties to even, one rounding)."""
+    v = _c(v, np.float64)
+    out = np.empty(v.shape, np.uint16)
+    _load().ppo_bf16_round_n(v.size, _ptr(v), _ptr(out))
+    return out
+
+
+def rmsnorm(x, eps=1e-5):
+    """Pre-norm of the stacked workload: returns (u fp64 [T,d], u bf16 bits)."""
+    x = _c(x, np.float64)
+    T, d = x.shape
+    u = np.empty_like(x)
+    bits = np.empty(x.shape, np.uint16)
+    if _load().ppo_rmsnorm(T, d, _ptr(x), float(eps), _ptr(u), _ptr(bits)) != 0:
+        raise ValueError("oracle rmsnorm: bad arguments")
+    return u, bits

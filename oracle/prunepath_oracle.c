@@ -225,3 +225,53 @@ int ppo_ffn(int64_t T, int64_t d, int64_t d_ff, int64_t E, const uint16_t *x,
     }
     return bad ? -1 : 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Wiring of the stacked-layer decode workload (not part of the paper's
+ * method): pre-norm residual layers, x_{l+1} = x_l + FFN_l(u_l) with
+ * u_l = RMSNorm(x_l), norm weight 1, carried to the next layer in bf16.
+ * ------------------------------------------------------------------------ */
+
+/* bf16 bit pattern nearest to v (ties to the even significand), rounded once
+ * from the double value (no intermediate binary32 rounding).  bf16 has an
+ * 8-bit significand, binary32's exponent range and its subnormals (quantum
+ * 2^-133); values beyond the largest finite bf16 round to infinity. */
+uint16_t ppo_bf16_round(double v) {
+    uint16_t sign = (uint16_t)(signbit(v) ? 0x8000u : 0u);
+    double a = fabs(v);
+    if (isnan(v)) return (uint16_t)(0x7FC0u | sign);
+    if (a == 0.0) return sign;
+    int ex;
+    (void)frexp(a, &ex); /* a = m * 2^ex, 0.5 <= m < 1 */
+    int q_exp = ex - 8;  /* quantum of an 8-bit significand at this binade */
+    if (q_exp < -133) q_exp = -133;
+    double q = ldexp(a, -q_exp); /* exact scaling by a power of two */
+    double r = nearbyint(q);     /* default rounding mode: nearest, ties to even */
+    double rv = ldexp(r, q_exp);
+    if (rv > 3.3895313892515355e38) return (uint16_t)(0x7F80u | sign); /* above max finite */
+    float f = (float)rv; /* exact: rv has at most 8 significant bits */
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    return (uint16_t)((u >> 16) | sign);
+}
+
+void ppo_bf16_round_n(int64_t n, const double *v, uint16_t *out) {
+    for (int64_t i = 0; i < n; ++i) out[i] = ppo_bf16_round(v[i]);
+}
+
+/* u[t, :] = x[t, :] / sqrt(mean_j x[t, j]^2 + eps) in fp64 (unrounded), and
+ * its bf16 rounding u_bits. */
+int ppo_rmsnorm(int64_t T, int64_t d, const double *x, double eps, double *u, uint16_t *u_bits) {
+    if (T < 0 || d < 1 || !x || !u || !u_bits || !(eps >= 0.0)) return -1;
+    for (int64_t t = 0; t < T; ++t) {
+        const double *xt = x + t * d;
+        double ss = 0.0;
+        for (int64_t j = 0; j < d; ++j) ss += xt[j] * xt[j];
+        double den = sqrt(ss / (double)d + eps);
+        for (int64_t j = 0; j < d; ++j) {
+            u[t * d + j] = xt[j] / den;
+            u_bits[t * d + j] = ppo_bf16_round(u[t * d + j]);
+        }
+    }
+    return 0;
+}

@@ -9,4 +9,4 @@ from ._lib import (EXPORTED, PP_AGG_SIGMOID, PP_AGG_SUM, PP_EHIP, PP_EINVAL, PP_
                    PP_KERNEL_GATEUP, PP_KERNEL_ROUTE, PP_OK, PP_SELECT_NUCLEUS, PP_SELECT_STRICT,
                    PrunePathError, load, prunepath_create, prunepath_destroy, prunepath_ffn_decode,
                    prunepath_ffn_prefill, prunepath_profile_begin, prunepath_profile_end,
-                   prunepath_route, prunepath_status_string)
+                   prunepath_residual_rmsnorm, prunepath_route, prunepath_status_string)

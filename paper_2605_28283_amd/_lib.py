@@ -32,7 +32,7 @@ PP_KERNEL_COUNT = 4
 
 EXPORTED = ("prunepath_create", "prunepath_route", "prunepath_ffn_decode",
             "prunepath_ffn_prefill", "prunepath_destroy", "prunepath_status_string",
-            "prunepath_profile_begin", "prunepath_profile_end")
+            "prunepath_profile_begin", "prunepath_profile_end", "prunepath_residual_rmsnorm")
 
 
 class PrunePathError(RuntimeError):
@@ -68,6 +68,8 @@ def load():
         lib.prunepath_profile_end.argtypes = [P, ctypes.POINTER(ctypes.c_double),
                                               ctypes.POINTER(ctypes.c_int32)]
         lib.prunepath_profile_end.restype = ctypes.c_int
+        lib.prunepath_residual_rmsnorm.argtypes = [P, P, P, I32, I32, F32, P, P]
+        lib.prunepath_residual_rmsnorm.restype = ctypes.c_int
         lib.prunepath_status_string.argtypes = [ctypes.c_int]
         lib.prunepath_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -155,6 +157,12 @@ def prunepath_ffn_prefill(handle, x, T, tau, inv_temp, y, expert_idx=None, count
                                       _ptr(y, "f32"), _ptr(expert_idx, "i32"),
                                       _ptr(count, "i32"), _stream(stream))
     _check(st, "prunepath_ffn_prefill")
+
+
+def prunepath_residual_rmsnorm(x, y, x_out, T, d, eps, u=None, stream=None):
+    st = load().prunepath_residual_rmsnorm(_ptr(x, "f32"), _ptr(y, "f32"), _ptr(x_out, "f32"),
+                                           T, d, eps, _ptr(u, "bf16"), _stream(stream))
+    _check(st, "prunepath_residual_rmsnorm")
 
 
 def prunepath_profile_begin(handle, capacity):

@@ -17,7 +17,11 @@ these synthetic layers stand in for them):
     by LogNormal(0, 0.5) (prefill workload), and for the skewed workload a
     per-token temperature ~ U(0.5, 2) passed as its inverse;
   * the skewed workload adds a per-expert router bias ~ Gumbel(0, 1.5);
-  * every value is drawn in fp32 and rounded to bf16 with round-to-nearest-even.
+  * every value is drawn in fp32 and rounded to bf16 with round-to-nearest-even;
+  * the 32-layer stack (11.3 GB of weights) draws its layers on the GPU with
+    torch's Philox generator, seeded 0x5EED0000 + 64 * seed + layer, in the
+    same order and distributions (host PCG64 would take minutes per layer);
+    its first residual x_0 comes from the host stream as above.
 """
 from dataclasses import dataclass, field
 from typing import Dict, Optional, Tuple
@@ -28,11 +32,11 @@ EXPERT_WIDTH = 128
 
 
 def bf16_bits(a) -> np.ndarray:
-    """Round fp32 values to bf16 (nearest, ties to even); return uint16 bits."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
-    u = u.astype(np.uint64)
-    r = ((u >> 16) & 1) + 0x7FFF
-    return ((u + r) >> 16).astype(np.uint16)
+    """Round fp32 values to bf16 (nearest, ties to even); return uint16 bits.
+    (torch's CPU conversion is the same rounding, multithreaded.)"""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
 
 
 def bf16_to_f32(bits) -> np.ndarray:
@@ -121,6 +125,29 @@ WORKLOADS: Dict[str, Workload] = {
                               skewed=True,
                               notes="Gumbel(0,1.5) router bias, per-token temperature U(0.5,2)"),
 }
+
+
+def make_layer_device(d: int, d_ff: int, E: int, seed: int, device="cuda", *,
+                      weight_std: float = 0.02, router_std: Optional[float] = None):
+    """One layer drawn on the GPU: dict of torch int16 tensors (bf16 bits)
+    W_r [E,d], W_gate/W_up [d_ff,d], W_down [d,d_ff]."""
+    import torch
+    if router_std is None:
+        router_std = 3.0 / np.sqrt(d)
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    out = {}
+    for name, shape, std in (("W_r", (E, d), router_std), ("W_gate", (d_ff, d), weight_std),
+                             ("W_up", (d_ff, d), weight_std), ("W_down", (d, d_ff), weight_std)):
+        a = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+        a.mul_(float(np.float32(std)))
+        out[name] = a.to(torch.bfloat16).view(torch.int16)
+        del a
+    return out
+
+
+def stack_layer_seed(layer: int, seed: int = 0) -> int:
+    return 0x5EED0000 + 64 * seed + layer
 
 
 def workload_layer(w: Workload, seed: int = 0, layer: int = 0) -> Layer:

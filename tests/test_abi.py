@@ -91,3 +91,20 @@ def test_binding_raises_on_error():
     with pytest.raises(pp.PrunePathError) as ei:
         pp.prunepath_route(0, 8, 1, 0.5, None, 8, 8, stream=0)
     assert ei.value.status == pp.PP_EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (None, None, 16, 4, 64, 1e-5, 8),          # x NULL
+    (16, None, None, 4, 64, 1e-5, 8),          # x_out NULL
+    (16, None, 16, 0, 64, 1e-5, 8),            # T < 1
+    (16, None, 16, 4, 66, 1e-5, 8),            # d % 4 != 0
+    (16, None, 16, 4, 0, 1e-5, 8),             # d < 4
+    (16, None, 16, 4, 64, float("nan"), 8),    # eps NaN
+    (16, None, 16, 4, 64, -1.0, 8),            # eps < 0
+    (8, None, 24, 4, 64, 1e-5, 8),             # x_out not 16-byte aligned
+    (16, None, 16, 4, 64, 1e-5, 4),            # u not 8-byte aligned
+])
+def test_residual_rmsnorm_rejects_bad_arguments(args):
+    lib = pp.load()
+    x, y, xo, T, d, eps, u = args
+    assert lib.prunepath_residual_rmsnorm(x, y, xo, T, d, eps, u, None) == pp.PP_EINVAL

@@ -319,3 +319,67 @@ def test_near_tie_helper(oracle_mod):
     cum = np.array([[0.5, 0.899995, 1.0], [0.5, 0.95, 1.0]])
     assert list(oracle_mod.near_tie(cum, 0.9)) == [True, False]
     assert not oracle_mod.near_tie(cum, 1.0).any()
+
+
+# ------------------------------------------- stacked-workload wiring (RMSNorm)
+
+def test_bf16_round_matches_library_for_binary32_values(oracle_mod):
+    """Every binary32 value is exact in fp64, so one rounding to bf16 must equal
+    torch's binary32 -> bfloat16 conversion (round to nearest, ties to even),
+    across binades, subnormals and signs."""
+    import torch
+    rng = np.random.default_rng(11)
+    mant = rng.uniform(1.0, 2.0, 20000)
+    ex = rng.integers(-140, 127, 20000)
+    v = (mant * np.exp2(ex.astype(np.float64)) * rng.choice([-1.0, 1.0], 20000)).astype(np.float32)
+    # exact midpoints between neighbouring bf16 values exercise the tie rule
+    lo = rng.integers(0x0080, 0x7F00, 5000).astype(np.uint32)
+    mids = ((lo << 16) | 0x8000).view(np.float32)
+    v = np.concatenate([v, mids, -mids, np.float32([0.0, -0.0, 1.0, -2.5])])
+    ref = torch.from_numpy(v).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert (oracle_mod.bf16_round(v.astype(np.float64)) == ref).all()
+
+
+def test_bf16_round_is_a_single_rounding(oracle_mod):
+    """Hand cases: ties go to the even significand; a value just above a tie
+    (by less than binary32 resolution) rounds up, which a rounding through
+    binary32 would get wrong."""
+    cases = [(1.0 + 2.0 ** -8, 0x3F80), (1.0 + 3 * 2.0 ** -8, 0x3F82),
+             (1.0 + 2.0 ** -8 + 2.0 ** -30, 0x3F81), (-(1.0 + 2.0 ** -8 + 2.0 ** -30), 0xBF81),
+             (2.0 ** -133, 0x0001), (2.0 ** -134, 0x0000), (1.5 * 2.0 ** -134, 0x0001),
+             (3.3895313892515355e38, 0x7F7F), (3.5e38, 0x7F80)]
+    got = oracle_mod.bf16_round([c[0] for c in cases])
+    assert [int(g) for g in got] == [c[1] for c in cases]
+
+
+def test_rmsnorm_closed_forms(oracle_mod):
+    # a constant row c: u = c / sqrt(c^2 + eps)
+    x = np.full((2, 8), 3.0)
+    x[1] = -0.25
+    u, _ = oracle_mod.rmsnorm(x, 1e-5)
+    assert np.allclose(u[0], 3.0 / math.sqrt(9.0 + 1e-5), rtol=1e-15, atol=0)
+    assert np.allclose(u[1], -0.25 / math.sqrt(0.0625 + 1e-5), rtol=1e-15, atol=0)
+    # (3, 4): mean square 12.5, so u = (0.6 sqrt 2, 0.8 sqrt 2) without eps
+    u, bits = oracle_mod.rmsnorm(np.array([[3.0, 4.0]]), 0.0)
+    assert np.allclose(u, [[0.6 * math.sqrt(2.0), 0.8 * math.sqrt(2.0)]], rtol=1e-15, atol=0)
+    # 0.8485... lies between bf16 0.84765625 (0x3F59) and 0.8515625 (0x3F5A)
+    assert bits.tolist() == [[0x3F59, 0x3F91]]
+
+
+def test_rmsnorm_invariants(oracle_mod):
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((6, 96)) * rng.lognormal(0, 1, (6, 1))
+    eps = 1e-3
+    u, bits = oracle_mod.rmsnorm(x, eps)
+    ms = np.mean(x * x, axis=1)
+    # mean(u^2) = ms / (ms + eps); u is a positive multiple of x per row
+    assert np.allclose(np.mean(u * u, axis=1), ms / (ms + eps), rtol=1e-13)
+    ratio = u / x
+    assert (ratio > 0).all() and np.allclose(ratio, ratio[:, :1], rtol=1e-13)
+    # without eps the result is scale invariant
+    u1, _ = oracle_mod.rmsnorm(x, 0.0)
+    u2, _ = oracle_mod.rmsnorm(x * 37.5, 0.0)
+    assert np.allclose(u1, u2, rtol=1e-13)
+    # the bits are the nearest bf16 values of u
+    back = bf16_to_f32(bits).astype(np.float64)
+    assert (np.abs(back - u) <= np.abs(u) * 2.0 ** -8 + 1e-300).all()
