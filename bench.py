@@ -23,7 +23,7 @@ import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gateup_llama8b_decode_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gateup_dec_llama8b_T32_tau0.7_traffic.json")
 
 
 def parse_args():
@@ -182,11 +182,12 @@ def main():
         r = run_point(T, tau)
         results[(T, tau)] = r
         print("# T=%-3d tau=%.2f  %8.1f us/step  %9.0f tok/s/layer  |U|=%5.1f  %7.1f GB/s "
-              "(%4.1f%% of peak)  gateup %s us  down %s us  route %s us" % (
+              "(%4.1f%% of peak)  gateup %.1f us (%.0f GB/s)  down %.1f us (%.0f GB/s)  "
+              "route %.1f us" % (
                   T, tau, r["ms_per_step"] * 1e3, r["tokens_per_s_layer"], r["union_experts"],
-                  r["effective_GBps"], 100 * r["frac_hbm_peak"],
-                  "%.1f" % r["kernel_us"]["gateup"], "%.1f" % r["kernel_us"]["down"],
-                  "%.1f" % r["kernel_us"]["route"]), file=sys.stderr, flush=True)
+                  r["effective_GBps"], 100 * r["frac_hbm_peak"], r["kernel_us"]["gateup"],
+                  r["gateup_GBps"], r["kernel_us"]["down"], r["down_GBps"],
+                  r["kernel_us"]["route"]), file=sys.stderr, flush=True)
     head = results[(args.T, args.tau)]
 
     # ---- traffic from the committed rocprofv3 counter summary, if it is current
@@ -203,7 +204,8 @@ def main():
     roof = {"bound": "hbm", "achieved": head["gateup_GBps"], "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": head["gateup_GBps"] / HBM_PEAK_GBPS if head["gateup_GBps"] else None,
-            "traffic": traffic, "kernel": "gateup_k (gate/up projections + SiLU product)",
+            "traffic": traffic,
+            "kernel": "gateup_dec_k (gate/up projections + SiLU product)",
             "algorithmic_bytes_per_launch": head["gateup_bytes"],
             "avg_launch_us": head["kernel_us"]["gateup"]}
 
@@ -227,8 +229,7 @@ def main():
                          "headline batch at tau=%g, repeated %d times in %.1f s" % (
                              T, args.tau, n, el)}
 
-    sweep = [{k: v for k, v in r.items() if k not in ("gateup_bytes", "down_bytes")}
-             for r in results.values()]
+    sweep = list(results.values())
     out = {
         "metric": "sparse-FFN decode tokens/s/layer",
         "value": head["tokens_per_s_layer"],

@@ -1,0 +1,323 @@
+// Gate/up projections of one group (one expert with up to 64 of its tokens)
+// over one K-slice, shared by the decode and prefill kernels: Eq. (ffn)'s
+// x W_gate and x W_up for the kept expert, Eq. (moefication_decomp).
+//
+// The group's token rows are staged in LDS in MFMA B-operand order; gate and
+// up fragments stream from HBM as contiguous 1 KiB wavefront loads
+// (expert-major repack), double buffered in registers, into bf16 MFMA
+// 16x16x32 with fp32 accumulation.  With one K-slice the epilogue forms
+// h = SiLU(a) * b [* sigmoid(g_e)] directly; with several, partial (a, b) rows
+// are handed to the slice that arrives last, which sums them in slice order.
+// h is stored as two bf16 numbers, hi = bf16(h) and lo = bf16(h - hi), so the
+// down projection keeps ~16 significant bits of h.
+#pragma once
+#include "pp_internal.h"
+
+namespace pp {
+namespace {
+
+constexpr int kXBufBytes = 64 * 1024;
+constexpr int kGuThreads = 512;
+constexpr int kPF = 2;          // K-steps per register buffer in gateup_k (two buffers)
+
+struct GUParams {
+    const uint16_t *x;
+    int T, d, E, NS;
+    const uint16_t *Wgu;
+    const float *gsig;
+    uint32_t flags;
+    PlanView plan;
+    const unsigned long long *emask;  // decode: tokens that kept each expert
+    float *abpart;
+    size_t abpart_rows;
+    uint32_t *cnt;
+    uint16_t *h_hi;
+    uint16_t *h_lo;
+};
+
+__device__ __forceinline__ void split_bf16(float h, uint16_t &hi, uint16_t &lo) {
+    hi = f32_to_bf16(h);
+    lo = f32_to_bf16(h - bf16_to_f32(hi));
+}
+
+// ------------------------------------------------------------------ gate/up
+
+// Stage token rows of a K sub-chunk into LDS in B-operand order:
+// xf[(j * nsc + step) * 64 + lane] holds token slot 16 j + lane % 16,
+// columns 32 (sc + step) + 8 (lane / 16) .. +7.  All loads are issued first.
+template <int NT>
+__device__ __forceinline__ void stage_x(const GUParams &P, const int *stok, int n, int sc, int nsc,
+                                        uint4 *xf) {
+    constexpr int kPerThread = kXBufBytes / 16 / kGuThreads;
+    constexpr int kBatch = 4;  // loads in flight per thread (register budget)
+    const int per_tok = nsc * 4;
+    const int total = NT * 16 * per_tok;
+    const uint4 z = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int i0 = 0; i0 < kPerThread; i0 += kBatch) {
+        if (threadIdx.x + kGuThreads * i0 >= total) break;
+        uint4 v[kBatch];
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            const int c = threadIdx.x + kGuThreads * (i0 + i);
+            v[i] = z;
+            if (c < total) {
+                const int q = c / per_tok, r = c - q * per_tok;
+                if (q < n)
+                    v[i] = ldg16(P.x + (size_t)stok[q] * P.d + (sc + (r >> 2)) * kKStep + 8 * (r & 3));
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            const int c = threadIdx.x + kGuThreads * (i0 + i);
+            if (c < total) {
+                const int q = c / per_tok, r = c - q * per_tok;
+                xf[((q >> 4) * nsc + (r >> 2)) * 64 + (q & 15) + 16 * (r & 3)] = v[i];
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void load_wgu(const uint16_t *wb, int step, int last, uint4 (&G)[kPF],
+                                         uint4 (&U)[kPF]) {
+#pragma unroll
+    for (int i = 0; i < kPF; ++i) {
+        const uint16_t *p = wb + (size_t)min(step + i, last) * 1024;
+        G[i] = ldg16(p);
+        U[i] = ldg16(p + 512);
+    }
+}
+
+template <int NT>
+__device__ __forceinline__ void mfma_wgu(const uint4 *xf, int nsc, int sl0, int nvalid,
+                                         const uint4 (&G)[kPF], const uint4 (&U)[kPF],
+                                         f32x4 (&ag)[NT], f32x4 (&au)[NT], int lane) {
+#pragma unroll
+    for (int i = 0; i < kPF; ++i) {
+        if (i < nvalid) {
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                const uint4 b = xf[(j * nsc + sl0 + i) * 64 + lane];
+                ag[j] = mfma16(G[i], b, ag[j]);
+                au[j] = mfma16(U[i], b, au[j]);
+            }
+        }
+    }
+}
+
+template <int NT>
+__device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int ks, int KS,
+                            int npairs, const int *stok, uint4 *xf, int *flag) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int s0 = (int)((long)ks * P.NS / KS), s1 = (int)((long)(ks + 1) * P.NS / KS);
+    constexpr int nsc_max = kXBufBytes / (NT * 16 * 64);
+    f32x4 ag[NT], au[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        ag[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        au[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const uint16_t *wb = P.Wgu + (size_t)(e * 8 + wv) * P.NS * 1024 + lane * 8;
+    for (int sc = s0; sc < s1; sc += nsc_max) {
+        const int nsc = min(nsc_max, s1 - sc), last = sc + nsc - 1;
+        uint4 G0[kPF], U0[kPF], G1[kPF], U1[kPF];
+        load_wgu(wb, sc, last, G0, U0);  // weights do not wait for the token staging
+        stage_x<NT>(P, stok, n, sc, nsc, xf);
+        __syncthreads();
+        for (int b = 0; b < nsc; b += 2 * kPF) {
+            if (b + kPF < nsc) load_wgu(wb, sc + b + kPF, last, G1, U1);
+            mfma_wgu<NT>(xf, nsc, b, min(kPF, nsc - b), G0, U0, ag, au, lane);
+            if (b + 2 * kPF < nsc) load_wgu(wb, sc + b + 2 * kPF, last, G0, U0);
+            if (b + kPF < nsc) mfma_wgu<NT>(xf, nsc, b + kPF, min(kPF, nsc - b - kPF), G1, U1, ag, au, lane);
+        }
+        __syncthreads();
+    }
+    // lane holds neurons r0..r0+3 of token slot q = 16 j + lane % 16
+    const bool sig = (P.flags & PP_AGG_SIGMOID) != 0;
+    const int r0 = wv * 16 + 4 * (lane >> 4);
+    if (KS == 1) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const int q = 16 * j + (lane & 15);
+            if (q < n) {
+                const float scl = sig ? P.gsig[(size_t)stok[q] * P.E + e] : 1.0f;
+                uint16_t hi[4], lo[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) split_bf16(silu(ag[j][i]) * au[j][i] * scl, hi[i], lo[i]);
+                const size_t row = (size_t)(p0 + q) * kExpertWidth + r0;
+                *reinterpret_cast<uint2 *>(P.h_hi + row) =
+                    make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+                *reinterpret_cast<uint2 *>(P.h_lo + row) =
+                    make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        const int q = 16 * j + (lane & 15);
+        if (q < n) {
+            float *row = P.abpart + ((size_t)ks * npairs + p0 + q) * 256 + r0;
+            st_dev2(row, ag[j][0], ag[j][1]);
+            st_dev2(row + 2, ag[j][2], ag[j][3]);
+            st_dev2(row + 128, au[j][0], au[j][1]);
+            st_dev2(row + 130, au[j][2], au[j][3]);
+        }
+    }
+    if (!arrive_last(&P.cnt[g], (unsigned)KS, flag)) return;
+    // (a, b) of the group's n x 128 block = sum of the slice partials in slice
+    // order; a thread owns up to kRedPer float2 of it and issues the loads of
+    // kRedSlices slices at once
+    constexpr int kRedPer = 2;
+    constexpr int kRedSlices = 4;
+    const int nel = n * (kExpertWidth / 2);
+    const size_t slice = (size_t)npairs * 256;
+    for (int i0 = 0; i0 < nel; i0 += kRedPer * kGuThreads) {
+        float2 a[kRedPer], b[kRedPer];
+        int off[kRedPer];
+        const int nq = (nel - i0 - tid + kGuThreads - 1) / kGuThreads;
+#pragma unroll
+        for (int q = 0; q < kRedPer; ++q) {
+            const int i = min(i0 + tid + kGuThreads * q, nel - 1);
+            off[q] = (p0 + (i >> 6)) * 256 + 2 * (i & 63);
+            a[q] = b[q] = make_float2(0.f, 0.f);
+        }
+        for (int k0 = 0; k0 < KS; k0 += kRedSlices) {
+            float2 u[kRedSlices][kRedPer], v[kRedSlices][kRedPer];
+#pragma unroll
+            for (int k = 0; k < kRedSlices; ++k) {
+                const float *base = P.abpart + (size_t)min(k0 + k, KS - 1) * slice;
+#pragma unroll
+                for (int q = 0; q < kRedPer; ++q) {
+                    u[k][q] = q < nq ? ld_dev2(base + off[q]) : make_float2(0.f, 0.f);
+                    v[k][q] = q < nq ? ld_dev2(base + off[q] + 128) : make_float2(0.f, 0.f);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kRedSlices; ++k)
+                if (k0 + k < KS)
+#pragma unroll
+                    for (int q = 0; q < kRedPer; ++q) {
+                        a[q].x += u[k][q].x;
+                        a[q].y += u[k][q].y;
+                        b[q].x += v[k][q].x;
+                        b[q].y += v[k][q].y;
+                    }
+        }
+#pragma unroll
+        for (int q = 0; q < kRedPer; ++q) {
+            if (q < nq) {
+                const int i = i0 + tid + kGuThreads * q;
+                const int qq = i >> 6, r = 2 * (i & 63);
+                const float scl = sig ? P.gsig[(size_t)stok[qq] * P.E + e] : 1.0f;
+                uint16_t h0, l0, h1, l1;
+                split_bf16(silu(a[q].x) * b[q].x * scl, h0, l0);
+                split_bf16(silu(a[q].y) * b[q].y * scl, h1, l1);
+                const size_t o = (size_t)(p0 + qq) * kExpertWidth + r;
+                *reinterpret_cast<uint32_t *>(P.h_hi + o) = h0 | ((uint32_t)h1 << 16);
+                *reinterpret_cast<uint32_t *>(P.h_lo + o) = l0 | ((uint32_t)l1 << 16);
+            }
+        }
+    }
+}
+
+// Decode plan, derived by every workgroup from the per-expert token masks:
+// groups = experts kept by at least one token, ascending; group u owns pair
+// rows [pair_u, pair_u + popcount(mask_u)), tokens ascending.  With GLOBAL,
+// workgroup 0 also stores it in the plan arrays.
+struct DecodePlan {
+    unsigned long long mask[kMaxExperts];
+    int e[kMaxExperts];
+    int pair[kMaxExperts];
+    int scan[2 * (kGuThreads / 64)];
+    int nG, npairs;
+};
+
+template <bool GLOBAL>
+__device__ void decode_plan(const GUParams &P, DecodePlan &D) {
+    const int tid = threadIdx.x, e = tid;
+    const unsigned long long m = (e < P.E) ? P.emask[e] : 0ull;
+    const int act = m != 0ull ? 1 : 0, pc = __popcll(m);
+    int slot, poff, nG, npairs;
+    block_excl_scan2(act, pc, &slot, &poff, &nG, &npairs, D.scan);
+    if (act) {
+        D.mask[slot] = m;
+        D.e[slot] = e;
+        D.pair[slot] = poff;
+        if (GLOBAL && blockIdx.x == 0) {
+            P.plan.grp_e[slot] = e;
+            P.plan.grp_pair[slot] = poff;
+            P.plan.grp_n[slot] = pc;
+            P.plan.grp_tok[slot] = poff;
+            int r = 0;
+            for (unsigned long long mm = m; mm; mm &= mm - 1)
+                P.plan.toklist[poff + r++] = __builtin_ctzll(mm);
+        }
+    }
+    if (tid == 0) {
+        D.nG = nG;
+        D.npairs = npairs;
+        if (GLOBAL && blockIdx.x == 0) {
+            P.plan.head[0] = nG;
+            P.plan.head[1] = npairs;
+        }
+    }
+    __syncthreads();
+}
+
+// One group's gate/up unit, dispatched on its number of 16-token tiles.
+__device__ __forceinline__ void gateup_group(const GUParams &P, int e, int n, int p0, int g,
+                                             int ks, int KS, int npairs, const int *stok,
+                                             uint4 *xf, int *flag) {
+    switch ((n + 15) >> 4) {
+    case 1: gateup_unit<1>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
+    case 2: gateup_unit<2>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
+    case 3: gateup_unit<3>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
+    default: gateup_unit<4>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
+    }
+}
+
+// K-slices per group: as many as keep all nG * KS units within `slots`
+// workgroups, each slice at least kMinStepsPerSlice K-steps, and the partial
+// rows within the abpart scratch.
+__device__ __forceinline__ int choose_ks(const GUParams &P, int nG, int npairs, int slots) {
+    int KS = nG > 0 ? slots / nG : 1;
+    const int max_ks = P.NS / kMinStepsPerSlice > 0 ? P.NS / kMinStepsPerSlice : 1;
+    if (KS > max_ks) KS = max_ks;
+    if (KS > 1 && (size_t)KS * npairs > P.abpart_rows) KS = (int)(P.abpart_rows / npairs);
+    return KS < 1 ? 1 : KS;
+}
+
+// Resident workgroups per CU of a kernel (1 if the query fails).
+template <typename K>
+int resident(K kernel, int threads) {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1)
+        n = 1;
+    return n;
+}
+
+inline GUParams gu_params(pp_layer *L, const uint16_t *x, int T, bool prefill) {
+    const pp_dims &dm = L->dm;
+    const counter_layout cl = counters_for(dm, L->max_tokens);
+    GUParams P;
+    P.x = x;
+    P.T = T;
+    P.d = dm.d;
+    P.E = dm.E;
+    P.NS = dm.NS;
+    P.Wgu = L->Wgu;
+    P.gsig = L->gsig;
+    P.flags = L->flags;
+    P.plan = plan_view(L, prefill);
+    P.emask = L->emask;
+    P.abpart = L->abpart;
+    P.abpart_rows = kAbPartRows;
+    P.cnt = L->counters + cl.gateup_base();
+    P.h_hi = L->h_hi;
+    P.h_lo = L->h_lo;
+    return P;
+}
+
+}  // namespace
+}  // namespace pp

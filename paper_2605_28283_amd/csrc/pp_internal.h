@@ -87,13 +87,17 @@ struct pp_layer {
 
 namespace pp {
 
-// Counter regions inside pp_layer::counters.
+// Counter regions inside pp_layer::counters (all zero at create; every
+// arrival counter is reset by its last arriver).
 struct counter_layout {
     size_t route;     // none
-    size_t gateup;    // one per group
-    size_t down;      // one per 64-row block
-    size_t dispatch;  // one
+    size_t gateup;    // one per group: K-slice arrivals
+    size_t down;      // one per 64-row block: decode expert-chunk arrivals
+    size_t dispatch;  // one: prefill bucketing arrivals
     size_t total;
+    size_t gateup_base() const { return route; }
+    size_t down_base() const { return route + gateup; }
+    size_t dispatch_base() const { return route + gateup + down; }
 };
 counter_layout counters_for(const pp_dims &dm, int max_tokens);
 
