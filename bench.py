@@ -40,6 +40,8 @@ def parse_args():
                     help="target duration of the CPU-oracle baseline (0 = skip)")
     ap.add_argument("--no-stack", action="store_true",
                     help="skip the 32-layer stacked decode measurement")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the 2048-token prefill measurement")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (5 times), the "
                          "reference dispatch for scaling HBM byte counters")
@@ -257,6 +259,8 @@ def main():
         pp.prunepath_destroy(h)
     handles = []
     torch.cuda.empty_cache()
+    if not args.no_prefill:
+        out["prefill"] = bench_prefill(args, torch, np, pp)
     if not args.no_stack:
         out["stack"] = bench_stack(args, torch, np, pp)
     if args.calibrate_copy_mib > 0:
@@ -268,6 +272,83 @@ def main():
         torch.cuda.synchronize()
         out["calibration_copy_bytes"] = 4 * n
     print(json.dumps(out), flush=True)
+
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def bench_prefill(args, torch, np, pp):
+    """One LLaMA-3-8B-shaped layer, T=2048 prefill (rows scaled by
+    LogNormal(0, 0.5)), tau in {0.7, 0.9}; calls rotate over 3 layer copies
+    (1.06 GB) so the Infinity Cache cannot hold the weights.  Reports MFMA
+    utilisation on algorithmic flops (router 2*E*d*T + 6*128*d*sum_t k_t)
+    against the dense bf16 peak, beside the attainable roofline
+    min(peak, HBM peak x algorithmic intensity)."""
+    from paper_2605_28283_amd.workloads import WORKLOADS, workload_tokens
+    w = WORKLOADS["llama8b_prefill"]
+    d, d_ff, E, T = w.d, w.d_ff, w.E, w.T[0]
+    handles = []
+    for c in range(3):
+        Wt = device_layer(torch, d, d_ff, E, 2000 + c)
+        handles.append(pp.prunepath_create(d, d_ff, E, T, *Wt))
+        del Wt
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    x_np, _ = workload_tokens(w, T, 0)
+    x = torch.from_numpy(x_np.view(np.int16)).cuda()
+    y = torch.empty((T, d), dtype=torch.float32, device="cuda")
+    idx = torch.empty((T, E), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((T,), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    steps = max(5, args.steps // 10)
+    res = []
+    for tau in w.taus:
+        for i in range(3):
+            pp.prunepath_ffn_prefill(handles[i % 3], x, T, tau, None, y, idx, cnt, stream=stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(steps):
+            pp.prunepath_ffn_prefill(handles[i % 3], x, T, tau, None, y, idx, cnt, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        for h in handles:
+            pp.prunepath_profile_begin(h, 8 * steps)
+        for i in range(steps):
+            pp.prunepath_ffn_prefill(handles[i % 3], x, T, tau, None, y, idx, cnt, stream=stream)
+        torch.cuda.synchronize()
+        kms = [0.0] * pp.PP_KERNEL_COUNT
+        for h in handles:
+            a, _ = pp.prunepath_profile_end(h)
+            kms = [u + v for u, v in zip(kms, a)]
+        kus = {name: kms[k] / steps * 1e3 for name, k in (
+            ("route", pp.PP_KERNEL_ROUTE), ("dispatch", pp.PP_KERNEL_DISPATCH),
+            ("gateup", pp.PP_KERNEL_GATEUP), ("down", pp.PP_KERNEL_DOWN))}
+        ks = []
+        for h in handles:
+            pp.prunepath_route(h, x, T, tau, None, idx, cnt, stream=stream)
+            torch.cuda.synchronize()
+            ks.append(int(cnt.sum().item()))
+        pairs = float(np.mean(ks))
+        flops = 2.0 * E * d * T + 6.0 * 128 * d * pairs
+        nbytes = E * d * 2 + E * 6 * 128 * d + 2 * T * d + 4 * T * d
+        tflops = flops / (ms * 1e-3) / 1e12
+        attainable = min(MFMA_BF16_PEAK_TFLOPS, HBM_PEAK_GBPS * 1e-3 * flops / nbytes)
+        res.append({"T": T, "tau": tau, "ms_per_call": ms, "tokens_per_s": T / (ms * 1e-3),
+                    "k_mean": pairs / T, "algorithmic_tflop": flops / 1e12,
+                    "achieved_tflops": tflops, "mfma_util": tflops / MFMA_BF16_PEAK_TFLOPS,
+                    "attainable_tflops": attainable, "frac_attainable": tflops / attainable,
+                    "effective_GBps": nbytes / (ms * 1e-3) / 1e9, "kernel_us": kus})
+        print("# prefill T=%d tau=%.2f: %.3f ms/call, %.0f tokens/s, k %.2f, %.1f TFLOP/s "
+              "(%.1f%% of bf16 peak, %.1f%% of the attainable %.0f)  [%s]" % (
+                  T, tau, ms, T / (ms * 1e-3), pairs / T, tflops, 100 * tflops / MFMA_BF16_PEAK_TFLOPS,
+                  100 * tflops / attainable, attainable,
+                  " ".join("%s %.1f us" % kv for kv in kus.items())), file=sys.stderr, flush=True)
+    for h in handles:
+        pp.prunepath_destroy(h)
+    torch.cuda.empty_cache()
+    return res
 
 
 def bench_stack(args, torch, np, pp):

@@ -12,8 +12,9 @@
 //                 expert to finish.
 //   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
 //                 SiLU product of one group (shared with the decode kernel).
-//   down_pf_k   : unit = (group, 256 rows); the group's h is staged in LDS
-//                 once, its outputs are added into y with fp32 atomics.
+//   down_pf_k   : unit = (group, 128 rows); the group's h is staged in LDS,
+//                 its outputs are added into y with fp32 atomics, 64
+//                 consecutive floats of one token row per instruction.
 #include "pp_gateup.h"
 
 namespace pp {
@@ -93,27 +94,39 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
     }
 }
 
-template <int MT>
+// Unit = (group, 128 rows of d).  Each of the 4 wavefronts owns two 16-row
+// tiles: it loads their down fragments, the group's h (hi and lo, MFMA B
+// order) is staged in LDS, and every wavefront multiplies.  The 64 x 128
+// result is then transposed through the same LDS so that each atomic add
+// instruction covers 64 consecutive floats of one token's row of y (two
+// cache lines) instead of sixteen scattered rows.
 __global__ __launch_bounds__(256) void down_pf_k(DNParams P) {
-    __shared__ uint4 hfh[4 * 4 * 64];
-    __shared__ uint4 hfl[4 * 4 * 64];
+    constexpr int kRows = 128, MT = 2;
+    __shared__ union {
+        struct {
+            uint4 hi[4 * 4 * 64];  // [token tile][K-step][lane]
+            uint4 lo[4 * 4 * 64];
+        } h;
+        float y[kGroupTokens][kRows];
+    } S;
     __shared__ int stok[kGroupTokens];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int nG = P.plan.head[0];
-    const int RB = 64 * MT, n_rb = P.d / RB;
+    const int n_rb = (P.d + kRows - 1) / kRows;  // the last block has 64 rows if d % 128 == 64
     const int units = nG * n_rb;
     const int RT = P.d / 16;
     const uint4 z = make_uint4(0, 0, 0, 0);
 
     for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
         const int g = unit / n_rb, rb = unit - g * n_rb;
+        const int nrows = min(kRows, P.d - rb * kRows);
         const int e = P.plan.grp_e[g], n = P.plan.grp_n[g], p0 = P.plan.grp_pair[g];
         const int tk = P.plan.grp_tok[g];
         if (tid < n) stok[tid] = P.plan.toklist[tk + tid];
         uint4 w[MT][4];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const int rt = (rb * 4 + wv) * MT + mt;
+            const int rt = min(rb * (kRows / 16) + wv * MT + mt, RT - 1);  // past d: unused rows
             const uint16_t *wp = P.Wd + (((size_t)e * RT + rt) * 4 * 64 + lane) * 8;
 #pragma unroll
             for (int s = 0; s < 4; ++s) w[mt][s] = ldg16(wp + s * 512);
@@ -134,8 +147,8 @@ __global__ __launch_bounds__(256) void down_pf_k(DNParams P) {
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                hfh[tid + 256 * k] = hv[k];
-                hfl[tid + 256 * k] = lv[k];
+                S.h.hi[tid + 256 * k] = hv[k];
+                S.h.lo[tid + 256 * k] = lv[k];
             }
         }
         __syncthreads();
@@ -150,8 +163,8 @@ __global__ __launch_bounds__(256) void down_pf_k(DNParams P) {
             if (j < NT) {
 #pragma unroll
                 for (int s = 0; s < 4; ++s) {
-                    const uint4 bh = hfh[(j * 4 + s) * 64 + lane];
-                    const uint4 bl = hfl[(j * 4 + s) * 64 + lane];
+                    const uint4 bh = S.h.hi[(j * 4 + s) * 64 + lane];
+                    const uint4 bl = S.h.lo[(j * 4 + s) * 64 + lane];
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) {
                         acc[mt][j] = mfma16(w[mt][s], bh, acc[mt][j]);
@@ -160,20 +173,24 @@ __global__ __launch_bounds__(256) void down_pf_k(DNParams P) {
                 }
             }
         }
+        __syncthreads();  // h no longer needed: its LDS becomes the transpose buffer
+        // lane holds rows 4 (lane / 16) + i of its tile, token slot 16 j + lane % 16
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const int r0 = ((rb * 4 + wv) * MT + mt) * 16 + 4 * (lane >> 4);
+            const int r0 = (wv * MT + mt) * 16 + 4 * (lane >> 4);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int q = 16 * j + (lane & 15);
-                if (j < NT && q < n) {
-                    float *yr = P.y + (size_t)stok[q] * P.d + r0;
-                    atomicAdd(yr + 0, acc[mt][j][0]);
-                    atomicAdd(yr + 1, acc[mt][j][1]);
-                    atomicAdd(yr + 2, acc[mt][j][2]);
-                    atomicAdd(yr + 3, acc[mt][j][3]);
-                }
+                if (j < NT)
+                    *reinterpret_cast<float4 *>(&S.y[q][r0]) =
+                        make_float4(acc[mt][j][0], acc[mt][j][1], acc[mt][j][2], acc[mt][j][3]);
             }
+        }
+        __syncthreads();
+        for (int q = wv; q < n; q += 4) {
+            float *yr = P.y + (size_t)stok[q] * P.d + (size_t)rb * kRows;
+            atomicAdd(yr + lane, S.y[q][lane]);
+            if (64 + lane < nrows) atomicAdd(yr + 64 + lane, S.y[q][64 + lane]);
         }
         __syncthreads();
     }
@@ -224,17 +241,9 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     const DNParams dp = dn_params(L, T, y);
-    int mt = 4;
-    while (mt > 1 && (dm.d / 64) % mt != 0) mt >>= 1;
-    static const int occ4 = resident(down_pf_k<4>, 256), occ2 = resident(down_pf_k<2>, 256),
-                     occ1 = resident(down_pf_k<1>, 256);
+    static const int occ_dn = resident(down_pf_k, 256);
     prof_mark(L, PP_KERNEL_DOWN, s, true);
-    if (mt == 4)
-        hipLaunchKernelGGL((down_pf_k<4>), dim3(occ4 * L->num_cu), dim3(256), 0, s, dp);
-    else if (mt == 2)
-        hipLaunchKernelGGL((down_pf_k<2>), dim3(occ2 * L->num_cu), dim3(256), 0, s, dp);
-    else
-        hipLaunchKernelGGL((down_pf_k<1>), dim3(occ1 * L->num_cu), dim3(256), 0, s, dp);
+    hipLaunchKernelGGL(down_pf_k, dim3(occ_dn * L->num_cu), dim3(256), 0, s, dp);
     prof_mark(L, PP_KERNEL_DOWN, s, false);
     return hipGetLastError();
 }
