@@ -177,7 +177,7 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     chk(dev_alloc(&L->ypart, L->ypart_elems));
     chk(dev_alloc(&L->ecount, (size_t)E));
     chk(dev_alloc(&L->tokl, (size_t)E * max_tokens));
-    chk(dev_alloc(&L->plan, (size_t)4 + 4 * (size_t)plan_max_groups(L->dm, max_tokens)));
+    chk(dev_alloc(&L->plan, (size_t)4 + 4 * (size_t)plan_max_groups(L->dm, max_tokens) + E + 1));
     chk(dev_alloc(&L->dec_tok, (size_t)kDecodeTile * E));
     chk(dev_alloc(&L->emask, (size_t)E));
     if (a != hipSuccess) {

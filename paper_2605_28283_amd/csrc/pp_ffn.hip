@@ -12,9 +12,11 @@
 //                 expert to finish.
 //   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
 //                 SiLU product of one group (shared with the decode kernel).
-//   down_pf_k   : unit = (group, 128 rows); the group's h is staged in LDS,
-//                 its outputs are added into y with fp32 atomics, 64
-//                 consecutive floats of one token row per instruction.
+//   down_pf_k   : unit = (expert, 256 rows); the expert's down block stays in
+//                 registers across its token groups; outputs are added into y
+//                 with fp32 atomics, 64 consecutive floats of one token row per
+//                 instruction.
+// Units of one expert are placed on one XCD (shared weights or h in L2).
 #include "pp_gateup.h"
 
 namespace pp {
@@ -38,7 +40,12 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
     const int npairs = P.plan.head[1];
     const int KS = choose_ks(P, nG, npairs, (int)gridDim.x);
     const int units = nG * KS;
-    for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
+    // consecutive units (K-slices of a group, then the groups of one expert)
+    // go to the same XCD, where they share the expert's weights in L2
+    const int slots = 8 * ((units + 7) / 8);
+    for (int slot = blockIdx.x; slot < slots; slot += gridDim.x) {
+        const int unit = xcd_order(slot, units);
+        if (unit >= units) continue;
         const int g = unit / KS, ks = unit - g * KS;
         const int e = P.plan.grp_e[g];
         const int n = P.plan.grp_n[g];
@@ -81,6 +88,8 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
     const int nch = (c + kGroupTokens - 1) / kGroupTokens;
     int cb, off, nG, npairs;
     block_excl_scan2(nch, c, &cb, &off, &nG, &npairs, scan);
+    if (tid < E) plan.egrp[tid] = cb;
+    if (tid == 0) plan.egrp[E] = nG;
     for (int ch = 0; ch < nch; ++ch) {
         const int g = cb + ch;
         plan.grp_e[g] = tid;
@@ -94,45 +103,51 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
     }
 }
 
-// Unit = (group, 128 rows of d).  Each of the 4 wavefronts owns two 16-row
-// tiles: it loads their down fragments, the group's h (hi and lo, MFMA B
-// order) is staged in LDS, and every wavefront multiplies.  The 64 x 128
-// result is then transposed through the same LDS so that each atomic add
-// instruction covers 64 consecutive floats of one token's row of y (two
-// cache lines) instead of sixteen scattered rows.
-__global__ __launch_bounds__(256) void down_pf_k(DNParams P) {
-    constexpr int kRows = 128, MT = 2;
+// Unit = (expert, 256 rows of d): the four wavefronts hold the expert's
+// 256 x 128 down block in registers (four 16-row tiles each, loaded once) and
+// run it over the expert's token groups of 64.  A group's h (hi and lo, MFMA B
+// order) is staged in LDS while the next group's is being loaded; the
+// 64 x 256 result is transposed through LDS so that each fp32 atomic add
+// instruction covers 64 consecutive floats of one token's row of y.  Units of
+// one expert share its h rows and go to the same XCD.
+constexpr int kPfRows = 256;
+__global__ __launch_bounds__(256, 2) void down_pf_k(DNParams P) {
+    constexpr int MT = 4;
     __shared__ union {
         struct {
             uint4 hi[4 * 4 * 64];  // [token tile][K-step][lane]
             uint4 lo[4 * 4 * 64];
         } h;
-        float y[kGroupTokens][kRows];
+        float y[kGroupTokens][kPfRows];
     } S;
     __shared__ int stok[kGroupTokens];
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int nG = P.plan.head[0];
-    const int n_rb = (P.d + kRows - 1) / kRows;  // the last block has 64 rows if d % 128 == 64
-    const int units = nG * n_rb;
+    const int n_rb = (P.d + kPfRows - 1) / kPfRows;
+    const int units = P.E * n_rb;
+    const int slots = 8 * ((units + 7) / 8);
     const int RT = P.d / 16;
     const uint4 z = make_uint4(0, 0, 0, 0);
 
-    for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
-        const int g = unit / n_rb, rb = unit - g * n_rb;
-        const int nrows = min(kRows, P.d - rb * kRows);
-        const int e = P.plan.grp_e[g], n = P.plan.grp_n[g], p0 = P.plan.grp_pair[g];
-        const int tk = P.plan.grp_tok[g];
-        if (tid < n) stok[tid] = P.plan.toklist[tk + tid];
+    for (int slot = blockIdx.x; slot < slots; slot += gridDim.x) {
+        const int unit = xcd_order(slot, units);
+        if (unit >= units) continue;
+        const int e = unit / n_rb, rb = unit - e * n_rb;
+        const int g0 = P.plan.egrp[e], g1 = P.plan.egrp[e + 1];
+        if (g0 >= g1) continue;
+        const int nrows = min(kPfRows, P.d - rb * kPfRows);
         uint4 w[MT][4];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const int rt = min(rb * (kRows / 16) + wv * MT + mt, RT - 1);  // past d: unused rows
+            const int rt = min(rb * (kPfRows / 16) + wv * MT + mt, RT - 1);  // past d: unused
             const uint16_t *wp = P.Wd + (((size_t)e * RT + rt) * 4 * 64 + lane) * 8;
 #pragma unroll
             for (int s = 0; s < 4; ++s) w[mt][s] = ldg16(wp + s * 512);
         }
-        {
-            uint4 hv[4], lv[4];
+        // h of one group in B-fragment order: thread slot i = tid + 256 k holds
+        // token tile i / 256, K-step (i / 64) % 4, lane i % 64
+        uint4 hv[4], lv[4];
+        auto load_h = [&](int g) {
+            const int n = P.plan.grp_n[g], p0 = P.plan.grp_pair[g];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int i = tid + 256 * k;
@@ -145,54 +160,59 @@ __global__ __launch_bounds__(256) void down_pf_k(DNParams P) {
                     lv[k] = ldg16(P.h_lo + o);
                 }
             }
+        };
+        load_h(g0);
+        for (int g = g0; g < g1; ++g) {
+            const int n = P.plan.grp_n[g];
+            __syncthreads();  // the previous group's atomics have read S.y
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 S.h.hi[tid + 256 * k] = hv[k];
                 S.h.lo[tid + 256 * k] = lv[k];
             }
-        }
-        __syncthreads();
-        const int NT = (n + 15) >> 4;
-        f32x4 acc[MT][4];
+            if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
+            __syncthreads();
+            if (g + 1 < g1) load_h(g + 1);
+            const int NT = (n + 15) >> 4;
+            f32x4 acc[MT][4];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+            for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int j = 0; j < 4; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            if (j < NT) {
+            for (int j = 0; j < 4; ++j) {
+                if (j < NT) {
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    const uint4 bh = S.h.hi[(j * 4 + s) * 64 + lane];
-                    const uint4 bl = S.h.lo[(j * 4 + s) * 64 + lane];
+                    for (int s = 0; s < 4; ++s) {
+                        const uint4 bh = S.h.hi[(j * 4 + s) * 64 + lane];
+                        const uint4 bl = S.h.lo[(j * 4 + s) * 64 + lane];
 #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) {
-                        acc[mt][j] = mfma16(w[mt][s], bh, acc[mt][j]);
-                        acc[mt][j] = mfma16(w[mt][s], bl, acc[mt][j]);
+                        for (int mt = 0; mt < MT; ++mt) {
+                            acc[mt][j] = mfma16(w[mt][s], bh, acc[mt][j]);
+                            acc[mt][j] = mfma16(w[mt][s], bl, acc[mt][j]);
+                        }
                     }
                 }
             }
-        }
-        __syncthreads();  // h no longer needed: its LDS becomes the transpose buffer
-        // lane holds rows 4 (lane / 16) + i of its tile, token slot 16 j + lane % 16
+            __syncthreads();  // h is no longer read: its LDS becomes the transpose buffer
+            // lane holds rows 4 (lane / 16) + i of its tile, token slot 16 j + lane % 16
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const int r0 = (wv * MT + mt) * 16 + 4 * (lane >> 4);
+            for (int mt = 0; mt < MT; ++mt) {
+                const int r0 = (wv * MT + mt) * 16 + 4 * (lane >> 4);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int q = 16 * j + (lane & 15);
-                if (j < NT)
-                    *reinterpret_cast<float4 *>(&S.y[q][r0]) =
-                        make_float4(acc[mt][j][0], acc[mt][j][1], acc[mt][j][2], acc[mt][j][3]);
+                for (int j = 0; j < 4; ++j)
+                    if (j < NT)
+                        *reinterpret_cast<float4 *>(&S.y[16 * j + (lane & 15)][r0]) = make_float4(
+                            acc[mt][j][0], acc[mt][j][1], acc[mt][j][2], acc[mt][j][3]);
+            }
+            __syncthreads();
+            for (int q = wv; q < n; q += 4) {
+                float *yr = P.y + (size_t)stok[q] * P.d + (size_t)rb * kPfRows;
+#pragma unroll
+                for (int c = 0; c < kPfRows / 64; ++c)
+                    if (64 * c + lane < nrows) atomicAdd(yr + 64 * c + lane, S.y[q][64 * c + lane]);
             }
         }
-        __syncthreads();
-        for (int q = wv; q < n; q += 4) {
-            float *yr = P.y + (size_t)stok[q] * P.d + (size_t)rb * kRows;
-            atomicAdd(yr + lane, S.y[q][lane]);
-            if (64 + lane < nrows) atomicAdd(yr + 64 + lane, S.y[q][64 + lane]);
-        }
-        __syncthreads();
     }
 }
 

@@ -39,7 +39,18 @@ struct PlanView {
     int32_t *grp_n;
     int32_t *grp_tok;
     int32_t *toklist;
+    int32_t *egrp;  // prefill: expert e owns groups [egrp[e], egrp[e + 1])
 };
+
+// Work-unit order for persistent grids whose size is a multiple of 8: the
+// workgroups of one XCD (blockIdx % 8 on MI355X's eight XCDs) take one
+// contiguous range of unit indices, so neighbouring units -- which share
+// inputs, e.g. one expert's weights or h rows -- meet in the same L2.
+// Returns the unit that linear slot `u` of `n` stands for.
+__host__ __device__ inline int xcd_order(int u, int n) {
+    const int per = (n + 7) / 8;
+    return (u % 8) * per + u / 8;
+}
 
 // Largest number of groups a call can produce.
 inline int plan_max_groups(const pp_dims &dm, int max_tokens) {
@@ -79,7 +90,7 @@ struct pp_layer {
     size_t ypart_elems;
     int32_t *ecount;    // [E] tokens per expert (prefill)
     int32_t *tokl;      // [E][max_tokens] token ids per expert (prefill)
-    int32_t *plan;      // PlanView storage: 4 + 4 * plan_max_groups ints
+    int32_t *plan;      // PlanView storage: 4 + 4 * plan_max_groups + E + 1 ints
     int32_t *dec_tok;   // [64 * E] token ids of the decode plan, pair order
     unsigned long long *emask;  // [E] decode: tokens that kept each expert (zero between calls)
     pp::profiler *prof; // non-NULL while per-kernel timing is recorded
@@ -121,6 +132,7 @@ inline PlanView plan_view(pp_layer *L, bool prefill) {
     v.grp_n = v.grp_pair + G;
     v.grp_tok = v.grp_n + G;
     v.toklist = prefill ? L->tokl : L->dec_tok;
+    v.egrp = v.grp_tok + G;
     return v;
 }
 
