@@ -1,13 +1,17 @@
 // Router: Eq. (routing_logits) GEMV, Eq. (softmax_prob), the descending order
 // pi, the cumulative mass C and the tau cut of Eq. (tau_thresh_activate).
 //
-// logits_k : one workgroup of 16 wavefronts per (16-token tile, 16-expert
-//            tile, K-slice of 16 K-steps = 512 columns of d).  Wavefront w does
-//            K-step w of the slice with one bf16 MFMA; the 16 results are summed
-//            in wavefront order and stored as the slice's partial logits.
-//            select_k sums the slices in slice order.  The summation order
-//            depends on d only, never on T, so a token's logits are the same
-//            bits in any batch: routing is batch-invariant.
+// logits_k : one workgroup per (64-token block, K-slice of 16 K-steps = 512
+//            columns of d).  The block's token rows are staged in LDS as MFMA
+//            operands; wavefront w takes expert tile w (16 experts) for all
+//            four token tiles and accumulates the slice's 16 K-steps in order
+//            in the MFMA accumulators (bf16 MFMA 16x16x32, fp32), storing the
+//            slice's partial logits.  select_k sums the slices in slice order.
+//            Every logit is formed in an order that depends on d only, never on
+//            T or on the other tokens, so a token's logits are the same bits in
+//            any batch: routing is batch-invariant.  Batches of up to 64 tokens
+//            use logits_small_k (one wavefront per token tile x expert tile x
+//            slice, the same MFMA chain).
 // select_k : one workgroup per token.  pi orders experts by descending g,
 //            equal g by ascending expert index (ordering g orders p: softmax is
 //            monotone).  With e_i = exp(g_i - g_max), S = sum e and
@@ -27,7 +31,8 @@
 namespace pp {
 namespace {
 
-constexpr int kRouteWaves = 16;
+constexpr int kRouteWaves = 16;  // K-steps per slice (also wavefronts per logits workgroup)
+constexpr int kLgTiles = 4;       // 16-token tiles per logits workgroup
 constexpr int kMaxSlices = kMaxWidth / kKStep / kRouteWaves;  // K-slices of the largest d
 
 struct RouteParams {
@@ -50,32 +55,87 @@ struct RouteParams {
 };
 
 __global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
-    __shared__ f32x4 red[kRouteWaves][64];
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    __shared__ uint4 xs[kLgTiles][kRouteWaves][64];  // [token tile][K-step][lane]: A fragments
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int tb = blockIdx.x / P.KSr, ks = blockIdx.x - tb * P.KSr;
+    if (P.build_plan && blockIdx.x == 0 && tid < P.E) P.emask[tid] = 0ull;
+    const int s_end = min(kRouteWaves, P.NS - ks * kRouteWaves);  // K-steps in this slice
+    // stage the block's token rows of this slice as MFMA A fragments
+    const uint4 z = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < kLgTiles; ++i) {
+        const int j = i, s = wv, l = lane;  // thread (wv, lane) stages K-step wv of every tile
+        const int t = tb * 16 * kLgTiles + 16 * j + (l & 15);
+        xs[j][s][l] = (t < P.T && s < s_end)
+                          ? ldg16(P.x + (size_t)t * P.d + (ks * kRouteWaves + s) * kKStep + 8 * (l >> 4))
+                          : z;
+    }
+    __syncthreads();
+    if (wv >= P.nEt) return;
+    // wavefront wv: expert tile wv for every token tile, K-steps of the slice
+    // accumulated in order in the MFMA accumulators
+    const int ec = wv * kRouteTile + (lane & 15);
+    const bool ve = ec < P.E;
+    f32x4 acc[kLgTiles];
+#pragma unroll
+    for (int j = 0; j < kLgTiles; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int ntile = min(kLgTiles, (P.T - tb * 16 * kLgTiles + 15) / 16);
+#pragma unroll
+    for (int s = 0; s < kRouteWaves; ++s) {
+        if (s < s_end) {
+            const uint4 b = ve ? ldg16(P.Wr + (size_t)ec * P.d + (ks * kRouteWaves + s) * kKStep +
+                                       8 * (lane >> 4))
+                               : z;
+#pragma unroll
+            for (int j = 0; j < kLgTiles; ++j)
+                if (j < ntile) acc[j] = mfma16(xs[j][s][lane], b, acc[j]);
+        }
+    }
+    // lane holds tokens 4 (lane / 16) + i of each tile, expert ec
+    if (!ve) return;
+#pragma unroll
+    for (int j = 0; j < kLgTiles; ++j) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int t = tb * 16 * kLgTiles + 16 * j + 4 * (lane >> 4) + i;
+            if (t < P.T) P.gpart[((size_t)ks * P.T + t) * P.E + ec] = acc[j][i];
+        }
+    }
+}
+
+// The same arithmetic for small batches, with more parallelism: one
+// wavefront per (16-token tile, 16-expert tile, K-slice), operands straight
+// from memory.  Each partial logit is the same chain of MFMAs as in logits_k,
+// so both kernels give identical bits.
+__global__ __launch_bounds__(64) void logits_small_k(RouteParams P) {
+    const int lane = threadIdx.x;
     const int per_tile = P.nEt * P.KSr;
     const int tt = blockIdx.x / per_tile;
     const int rem = blockIdx.x - tt * per_tile;
     const int et = rem / P.KSr, ks = rem - et * P.KSr;
-    if (P.build_plan && blockIdx.x == 0 && threadIdx.x < P.E) P.emask[threadIdx.x] = 0ull;
-    const int tr = tt * kRouteTile + (lane & 15);
-    const int ec = et * kRouteTile + (lane & 15);
-    const int koff = 8 * (lane >> 4);
-    const int s = ks * kRouteWaves + wv;  // one K-step per wavefront
-    const bool va = tr < P.T && s < P.NS, vb = ec < P.E && s < P.NS;
+    if (P.build_plan && blockIdx.x == 0) {
+        for (int e = lane; e < P.E; e += 64) P.emask[e] = 0ull;
+    }
+    const int s_end = min(kRouteWaves, P.NS - ks * kRouteWaves);
+    const int t = tt * 16 + (lane & 15), ec = et * kRouteTile + (lane & 15);
+    const bool vt = t < P.T, ve = ec < P.E;
     const uint4 z = make_uint4(0, 0, 0, 0);
-    const uint4 a = va ? ldg16(P.x + (size_t)tr * P.d + koff + s * kKStep) : z;
-    const uint4 b = vb ? ldg16(P.Wr + (size_t)ec * P.d + koff + s * kKStep) : z;
-    red[wv][lane] = mfma16(a, b, f32x4{0.f, 0.f, 0.f, 0.f});
-    __syncthreads();
-    if (wv != 0 || ec >= P.E) return;
-    f32x4 r = red[0][lane];
+    const size_t col0 = (size_t)ks * kRouteWaves * kKStep + 8 * (lane >> 4);
+    uint4 a[kRouteWaves], b[kRouteWaves];
 #pragma unroll
-    for (int w = 1; w < kRouteWaves; ++w) r += red[w][lane];
-    // MFMA 16x16 result: lane holds rows 4*(lane/16)+i (tokens), column lane%16 (expert)
+    for (int s = 0; s < kRouteWaves; ++s) {
+        a[s] = (vt && s < s_end) ? ldg16(P.x + (size_t)t * P.d + col0 + s * kKStep) : z;
+        b[s] = (ve && s < s_end) ? ldg16(P.Wr + (size_t)ec * P.d + col0 + s * kKStep) : z;
+    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < kRouteWaves; ++s)
+        if (s < s_end) acc = mfma16(a[s], b[s], acc);
+    if (!ve) return;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int t = tt * kRouteTile + 4 * (lane >> 4) + i;
-        if (t < P.T) P.gpart[((size_t)ks * P.T + t) * P.E + ec] = r[i];
+        const int tr = tt * 16 + 4 * (lane >> 4) + i;
+        if (tr < P.T) P.gpart[((size_t)ks * P.T + tr) * P.E + ec] = acc[i];
     }
 }
 
@@ -252,9 +312,14 @@ hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const 
     P.gsig = L->gsig;
     P.build_plan = (build_plan && T <= kDecodeTile) ? 1 : 0;
     P.emask = L->emask;
-    const int nTt = (T + kRouteTile - 1) / kRouteTile;
     prof_mark(L, PP_KERNEL_ROUTE, s, true);
-    hipLaunchKernelGGL(logits_k, dim3(nTt * P.nEt * P.KSr), dim3(1024), 0, s, P);
+    if (T <= kDecodeTile) {
+        const int nTt = (T + 15) / 16;
+        hipLaunchKernelGGL(logits_small_k, dim3(nTt * P.nEt * P.KSr), dim3(64), 0, s, P);
+    } else {
+        const int nTb = (T + 16 * kLgTiles - 1) / (16 * kLgTiles);
+        hipLaunchKernelGGL(logits_k, dim3(nTb * P.KSr), dim3(1024), 0, s, P);
+    }
     hipLaunchKernelGGL(select_k, dim3(T), dim3(kSelThreads), 0, s, P);
     prof_mark(L, PP_KERNEL_ROUTE, s, false);
     return hipGetLastError();

@@ -143,17 +143,22 @@ def test_invalid_calls_leave_outputs_untouched(tiny):
 
 
 def test_routing_is_batch_invariant(oracle_mod):
-    """A token's selection does not depend on the batch it is routed in."""
+    """A token's selection, and the bits of its gate weights sigmoid(g), do not
+    depend on the batch it is routed in (batches above 64 tokens use the
+    large-batch logits kernel, smaller ones the per-tile kernel)."""
     L = make_layer(1024, 24 * 128, 24, 17)
-    x, _ = make_tokens(70, 1024, 18)
-    with DevLayer(L, 128) as dl:
+    x, _ = make_tokens(200, 1024, 18)
+    with DevLayer(L, 256, flags=SIG) as dl:
         full = dl.run("route", x, 0.8)
-        for t in (0, 13, 69):
+        for t in (0, 13, 69, 199):
             one = dl.run("route", x[t:t + 1], 0.8)
             np.testing.assert_array_equal(one[0][0], full[0][t])
             assert one[1][0] == full[1][t]
-        part = dl.run("route", x[5:40], 0.8)
-        np.testing.assert_array_equal(part[0], full[0][5:40])
+            np.testing.assert_array_equal(one[2][0].view(np.uint32), full[2][t].view(np.uint32))
+        for a, b in ((5, 40), (60, 130), (130, 200)):
+            part = dl.run("route", x[a:b], 0.8)
+            np.testing.assert_array_equal(part[0], full[0][a:b])
+            np.testing.assert_array_equal(part[2].view(np.uint32), full[2][a:b].view(np.uint32))
 
 
 def test_decode_deterministic_and_matches_prefill(tiny):
