@@ -155,7 +155,6 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     L->gpart_elems = (size_t)((L->dm.NS + 15) / 16) * max_tokens * E;
     L->n_counters = cl.total;
     L->max_pairs = (size_t)max_tokens * E;
-    L->ypart_elems = (size_t)32 * kDecodeTile * d;  // at most 32 expert chunks of a 64-token slice
 
     hipError_t a = hipSuccess;
     auto chk = [&](hipError_t r) {
@@ -174,7 +173,7 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     chk(dev_alloc(&L->abpart, kAbPartRows * 256));
     chk(dev_alloc(&L->h_hi, L->max_pairs * kExpertWidth));
     chk(dev_alloc(&L->h_lo, L->max_pairs * kExpertWidth));
-    chk(dev_alloc(&L->ypart, L->ypart_elems));
+    chk(dev_alloc(&L->ypart, (size_t)kDecodeChunks * kDecodeTile * d));
     chk(dev_alloc(&L->ecount, (size_t)E));
     chk(dev_alloc(&L->tokl, (size_t)E * max_tokens));
     chk(dev_alloc(&L->plan, (size_t)4 + 4 * (size_t)plan_max_groups(L->dm, max_tokens) + E + 1));

@@ -9,23 +9,27 @@
 //                 SiLU product of one group (code shared with prefill); the
 //                 K-split is chosen so that all units fit in one round of
 //                 resident workgroups.
-//   down_dec_k  : unit = (64 rows of d, chunk of groups); each wavefront takes
-//                 every fourth group of the chunk, multiplies its 64x128 down
-//                 block with the group's compact token tiles (two MFMAs per
-//                 fragment: hi and lo) and adds the result into its own LDS
-//                 accumulator [tokens][64 rows] -- no synchronisation inside
-//                 the chunk; the next half-group's fragments are loaded while
-//                 the current one is multiplied.  The four accumulators are
-//                 summed in wavefront order; chunks are summed in chunk order by
-//                 the last to arrive.  No float atomics: decode is deterministic.
+//   down_dec_k  : sparse groups (<= 8 tokens per group on average): unit = one
+//                 16-row tile of d over all groups; each of the 8 wavefronts
+//                 takes every eighth group, tile by tile of 16 tokens (three
+//                 in flight), multiplies the 16x128 down block with the tokens'
+//                 h (two MFMAs per fragment: hi and lo) and adds into its own
+//                 LDS accumulator [tokens][16 rows]; the accumulators are
+//                 summed in wavefront order and y written once.
+//                 Dense groups: unit = (128 rows, chunk of groups), h staged
+//                 once in LDS for all 8 wavefronts, chunk partials summed in
+//                 chunk order by the last chunk to arrive.
+//                 No float atomics: decode is deterministic.
 #include "pp_gateup.h"
 
 namespace pp {
 namespace {
 
-constexpr int kDnRows = 64;        // rows of d per down unit
-constexpr int kMaxChunks = 32;     // expert chunks per row block, at most
-constexpr int kDnMinPerChunk = 8;  // groups per chunk at least (two per wavefront)
+constexpr int kDnThreads = 512;    // down projection: 8 wavefronts per workgroup
+constexpr int kDnR = 1;            // 16-row tiles per down item (sparse groups)
+constexpr int kShRows = 128;       // dense groups: rows per unit (8 wavefronts x 16)
+constexpr int kShYS = kShRows + 4;
+constexpr int kShTiles = kDecodeTile / 16;
 
 struct DNParams {
     int T, d, E;
@@ -33,9 +37,8 @@ struct DNParams {
     const uint16_t *h_hi;
     const uint16_t *h_lo;
     float *y;
-    float *ypart;
-    size_t ypart_elems;
-    uint32_t *cnt;
+    float *ypart;      // [kDecodeChunks][T][d] chunk partials (dense groups)
+    uint32_t *dn_cnt;  // [ceil(d / 128)] chunk arrivals per row block
     PlanView plan;
 };
 
@@ -64,185 +67,307 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
 
 // ------------------------------------------------------------------ down
 
-// Half of one expert's decode down work, as held in registers by a
-// wavefront: 32 rows of its 64-row down block (2 row tiles x 4 K-steps of A
-// fragments) and the B fragments (h hi and lo) of its first 16 tokens.
-struct DownItem {
-    uint4 w[2][4];
+// One (group, 16-token tile) of work in one 16-row tile of d, as held in
+// registers by a wavefront: the tile's down fragments (4 K-steps of A) and
+// the tokens' B fragments (h hi and lo).
+template <int R>
+struct RowItem {
+    uint4 w[R][4];
     uint4 bh[4], bl[4];
-    int tok, n, p0, tk, half;
+    int tok;  // token of this lane's slot, -1 if the slot is empty
+    bool live;
 };
 
-__device__ __forceinline__ void load_down_item(const DNParams &P, int u, int half, int rb, int RT,
-                                               int lane, DownItem &it) {
-    const uint4 z = make_uint4(0, 0, 0, 0);
-    const int e = P.plan.grp_e[u];
-    it.n = P.plan.grp_n[u];
-    it.p0 = P.plan.grp_pair[u];
-    it.tk = P.plan.grp_tok[u];
-    it.half = half;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-        const uint16_t *wp =
-            P.Wd + (((size_t)e * RT + rb * 4 + 2 * half + mt) * 4 * 64 + lane) * 8;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) it.w[mt][s] = ldg16(wp + s * 512);
+// Walks a wavefront's items: groups u = first, first + stride, ..., and the
+// 16-token tiles of each group.
+struct RowCursor {
+    int u, j, n, p0, tk, e;
+    int stride, nU;
+    __device__ void enter(const PlanView &pl) {
+        if (u < nU) {
+            n = pl.grp_n[u];
+            p0 = pl.grp_pair[u];
+            tk = pl.grp_tok[u];
+            e = pl.grp_e[u];
+        }
     }
-    const int slot = lane & 15;
-    const bool ok = slot < it.n;
+    __device__ void advance(const PlanView &pl) {
+        if (16 * ++j >= n) {
+            u += stride;
+            j = 0;
+            enter(pl);
+        }
+    }
+};
+
+template <int R>
+__device__ __forceinline__ void load_row_item(const DNParams &P, RowCursor &c, int rt, int RT,
+                                              int lane, RowItem<R> &it) {
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    it.live = c.u < c.nU;
+    if (!it.live) return;
+#pragma unroll
+    for (int m = 0; m < R; ++m) {
+        const uint16_t *wp = P.Wd + (((size_t)c.e * RT + rt + m) * 4 * 64 + lane) * 8;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) it.w[m][s] = ldg16(wp + s * 512);
+    }
+    const int slot = 16 * c.j + (lane & 15);
+    const bool ok = slot < c.n;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-        const size_t o = (size_t)(it.p0 + slot) * kExpertWidth + s * kKStep + 8 * (lane >> 4);
+        const size_t o = (size_t)(c.p0 + slot) * kExpertWidth + s * kKStep + 8 * (lane >> 4);
         it.bh[s] = ok ? ldg16(P.h_hi + o) : z;
         it.bl[s] = ok ? ldg16(P.h_lo + o) : z;
     }
-    it.tok = ok ? P.plan.toklist[it.tk + slot] : 0;
+    it.tok = ok ? P.plan.toklist[c.tk + slot] : -1;
+    c.advance(P.plan);
 }
 
-// acc[t][32 rows of the item's half] += the item's 32 x n block (the first
-// tile of 16 tokens comes with the item; further tiles are loaded here).
-template <int YS>
-__device__ __forceinline__ void apply_down_item(const DNParams &P, const DownItem &it, int lane,
-                                                float (*acc)[YS]) {
-    const uint4 z = make_uint4(0, 0, 0, 0);
-    for (int j = 0; j * 16 < it.n; ++j) {
-        uint4 bh[4], bl[4];
-        int t;
-        const int slot = 16 * j + (lane & 15);
-        const bool ok = slot < it.n;
-        if (j == 0) {
+// acc[t][16 R rows] += the item's 16 R x 16 block.
+template <int R, int YS>
+__device__ __forceinline__ void apply_row_item(const RowItem<R> &it, int lane, float (*acc)[YS]) {
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                bh[s] = it.bh[s];
-                bl[s] = it.bl[s];
-            }
-            t = it.tok;
-        } else {
+    for (int m = 0; m < R; ++m) {
+        f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const size_t o =
-                    (size_t)(it.p0 + slot) * kExpertWidth + s * kKStep + 8 * (lane >> 4);
-                bh[s] = ok ? ldg16(P.h_hi + o) : z;
-                bl[s] = ok ? ldg16(P.h_lo + o) : z;
-            }
-            t = ok ? P.plan.toklist[it.tk + slot] : 0;
+        for (int s = 0; s < 4; ++s) {
+            a = mfma16(it.w[m][s], it.bh[s], a);
+            a = mfma16(it.w[m][s], it.bl[s], a);
         }
-#pragma unroll
-        for (int mt = 0; mt < 2; ++mt) {
-            f32x4 a = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                a = mfma16(it.w[mt][s], bh[s], a);
-                a = mfma16(it.w[mt][s], bl[s], a);
-            }
-            if (ok) {
-                float4 *dst = reinterpret_cast<float4 *>(
-                    &acc[t][(2 * it.half + mt) * 16 + 4 * (lane >> 4)]);
-                float4 v = *dst;
-                v.x += a[0];
-                v.y += a[1];
-                v.z += a[2];
-                v.w += a[3];
-                *dst = v;
-            }
+        // lane holds rows 4 (lane / 16) + i of tile m, token slot lane % 16
+        if (it.tok >= 0) {
+            float4 *dst = reinterpret_cast<float4 *>(&acc[it.tok][16 * m + 4 * (lane >> 4)]);
+            float4 v = *dst;
+            v.x += a[0];
+            v.y += a[1];
+            v.z += a[2];
+            v.w += a[3];
+            *dst = v;
         }
     }
 }
 
-template <int TB>
-__global__ __launch_bounds__(256, 2) void down_dec_k(DNParams P) {
-    constexpr int YS = kDnRows + 4;  // padded row stride of an accumulator
-    __shared__ float yacc[4][TB][YS];
-    __shared__ int s_flag;
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int nU = P.plan.head[0];
-    const int n_rb = P.d / kDnRows, RT = P.d / 16;
-    // expert chunks: enough units for the resident workgroups, but at least
-    // kDnMinPerChunk experts per chunk so each wavefront streams a pipeline
-    int ES = (int)gridDim.x / n_rb;
-    if (ES > nU / kDnMinPerChunk) ES = nU / kDnMinPerChunk;
-    if (ES > kMaxChunks) ES = kMaxChunks;
-    if (ES > 1 && (size_t)ES * P.T * P.d > P.ypart_elems) ES = (int)(P.ypart_elems / ((size_t)P.T * P.d));
-    if (ES < 1) ES = 1;
-    const int Uc = (nU + ES - 1) / ES;
-    ES = (nU + Uc - 1) / Uc;
-    const int units = n_rb * ES;
-    float(*acc_w)[YS] = yacc[wv];
+// Unit = one 16-row tile of d over every group of the plan; wavefront w takes
+// groups w, w + 8, ..., tile by tile of 16 tokens, with three tiles in
+// flight, and adds into its own LDS accumulator [tokens][16 rows].  The eight accumulators are summed in
+// wavefront order and the rows of y written once: no partial outputs, no
+// cross-workgroup hand-off, every unit the same amount of work.
+// ---- dense groups (many tokens per group): h shared through LDS
 
-    for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
-        const int c = unit / n_rb, rb = unit - c * n_rb;
-        for (int i = lane; i < P.T * YS; i += 64) acc_w[i / YS][i % YS] = 0.0f;
-        // this wavefront's items: q -> (group c*Uc + wv + 4*(q/2), half q%2);
-        // two items in flight, so the next item's loads overlap this one's math
-        const int u0 = c * Uc + wv, u1 = min(nU, (c + 1) * Uc);
-        const int nq = u0 < u1 ? 2 * ((u1 - u0 + 3) / 4) : 0;
-        DownItem A, B;
-        if (nq > 0) load_down_item(P, u0, 0, rb, RT, lane, A);
-        for (int q = 0; q < nq; q += 2) {
-            load_down_item(P, u0 + 4 * (q >> 1), 1, rb, RT, lane, B);
-            apply_down_item<YS>(P, A, lane, acc_w);
-            if (q + 2 < nq) load_down_item(P, u0 + 4 * ((q + 2) >> 1), 0, rb, RT, lane, A);
-            apply_down_item<YS>(P, B, lane, acc_w);
+struct DnShared {
+    float yacc[kDecodeTile][kShYS];
+    uint4 hb[kShTiles][8][64];  // [token tile][hi s0..3, lo s0..3][lane]: B fragments
+};
+template <int TB, int R>
+struct DnRow {
+    float yacc[kDnThreads / 64][TB][16 * R + 4];
+};
+
+// This wavefront's 16 x 128 block of group u's down weights.
+__device__ __forceinline__ void sh_load_w(const DNParams &P, int u, int rt, int RT, int lane,
+                                          uint4 (&w)[4]) {
+    const uint16_t *wp = P.Wd + (((size_t)P.plan.grp_e[u] * RT + rt) * 4 * 64 + lane) * 8;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) w[s] = ldg16(wp + s * 512);
+}
+
+// Piece wv (hi/lo x K-step) of group u's h B fragments and the tokens of
+// this lane's slot, for every 16-token tile.
+__device__ __forceinline__ void sh_load_h(const DNParams &P, int u, int wv, int lane,
+                                          uint4 (&hp)[kShTiles], int (&tp)[kShTiles]) {
+    const int n = P.plan.grp_n[u], p0 = P.plan.grp_pair[u], tk = P.plan.grp_tok[u];
+    const uint16_t *src = (wv < 4) ? P.h_hi : P.h_lo;
+    const int col = (wv & 3) * kKStep + 8 * (lane >> 4);
+#pragma unroll
+    for (int j = 0; j < kShTiles; ++j) {
+        const int slot = 16 * j + (lane & 15);
+        const bool ok = slot < n;
+        hp[j] = ok ? ldg16(src + (size_t)(p0 + slot) * kExpertWidth + col) : make_uint4(0, 0, 0, 0);
+        tp[j] = ok ? P.plan.toklist[tk + slot] : -1;
+    }
+}
+
+// One group of a dense unit: stage its h in LDS, reuse hp for group u + 2's
+// h, multiply, reuse wc for group u + 2's weights (both two groups ahead).
+__device__ __forceinline__ void sh_group(const DNParams &P, DnShared &S, int u, int u1, int rt,
+                                         int RT, bool rows_ok, int wv, int lane,
+                                         uint4 (&hp)[kShTiles], int (&tp)[kShTiles],
+                                         uint4 (&wc)[4]) {
+    const int nt = (P.plan.grp_n[u] + 15) >> 4;
+    int tok[kShTiles];
+    __syncthreads();  // every wavefront is done with the previous group's h
+#pragma unroll
+    for (int j = 0; j < kShTiles; ++j) {
+        if (j < nt) S.hb[j][wv][lane] = hp[j];
+        tok[j] = tp[j];
+    }
+    __syncthreads();
+    if (u + 2 < u1) sh_load_h(P, u + 2, wv, lane, hp, tp);
+    if (!rows_ok) return;
+    for (int j = 0; j < nt; ++j) {
+        f32x4 a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            a = mfma16(wc[s], S.hb[j][s][lane], a);
+            a = mfma16(wc[s], S.hb[j][4 + s][lane], a);
         }
-        __syncthreads();
-        // sum the four accumulators in wavefront order
-        for (int i = tid; i < P.T * (kDnRows / 4); i += blockDim.x) {
-            const int t = i / (kDnRows / 4), r = 4 * (i - t * (kDnRows / 4));
-            float4 s = *reinterpret_cast<const float4 *>(&yacc[0][t][r]);
+        int t = tok[0];
 #pragma unroll
-            for (int w = 1; w < 4; ++w) {
-                const float4 v = *reinterpret_cast<const float4 *>(&yacc[w][t][r]);
-                s.x += v.x;
-                s.y += v.y;
-                s.z += v.z;
-                s.w += v.w;
-            }
-            const size_t col = (size_t)rb * kDnRows + r;
-            if (ES == 1) {
-                *reinterpret_cast<float4 *>(P.y + (size_t)t * P.d + col) = s;
-            } else {
-                float *dst = P.ypart + ((size_t)c * P.T + t) * P.d + col;
-                st_dev2(dst, s.x, s.y);
-                st_dev2(dst + 2, s.z, s.w);
-            }
+        for (int q = 1; q < kShTiles; ++q)
+            if (j == q) t = tok[q];
+        // lane holds rows 4 (lane / 16) + i of the wavefront's tile, token slot lane % 16
+        if (t >= 0) {
+            float4 *dst = reinterpret_cast<float4 *>(&S.yacc[t][wv * 16 + 4 * (lane >> 4)]);
+            float4 v = *dst;
+            v.x += a[0];
+            v.y += a[1];
+            v.z += a[2];
+            v.w += a[3];
+            *dst = v;
         }
-        if (ES > 1 && arrive_last(&P.cnt[rb], (unsigned)ES, &s_flag)) {
-            // y[t][64 rows] = sum of the chunk partials in chunk order; every
-            // thread owns up to kRedPer float2 of the block and issues the
-            // loads of kRedChunks chunks at once
-            constexpr int kRedPer = kDecodeTile * (kDnRows / 2) / 256;
-            constexpr int kRedChunks = 4;
-            const int nel = P.T * (kDnRows / 2);
-            float2 acc[kRedPer];
-            int off[kRedPer];
+    }
+    if (u + 2 < u1) sh_load_w(P, u + 2, rt, RT, lane, wc);
+}
+
+// Dense unit = (chunk c of Uc groups, 128 rows of d): the 8 wavefronts own 16
+// rows each and walk the chunk's groups together; the chunk's partial is
+// summed with the other chunks' in chunk order by the last to arrive.
+__device__ void sh_unit(const DNParams &P, DnShared &S, int c, int rb, int Uc, int nU, int ES,
+                        int *flag) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int T = P.T, d = P.d, RT = d / 16;
+    const int rt = rb * (kShRows / 16) + wv;
+    const bool rows_ok = rt < RT;
+    const int nrows = min(kShRows, d - rb * kShRows);
+    for (int i = tid; i < T * kShYS; i += blockDim.x) S.yacc[i / kShYS][i % kShYS] = 0.0f;
+    const int u0 = c * Uc, u1 = min(nU, u0 + Uc);
+    uint4 w0[4], w1[4], hp0[kShTiles], hp1[kShTiles];
+    int tp0[kShTiles], tp1[kShTiles];
+    if (rows_ok) {
+        sh_load_w(P, u0, rt, RT, lane, w0);
+        if (u0 + 1 < u1) sh_load_w(P, u0 + 1, rt, RT, lane, w1);
+    }
+    sh_load_h(P, u0, wv, lane, hp0, tp0);
+    if (u0 + 1 < u1) sh_load_h(P, u0 + 1, wv, lane, hp1, tp1);
+    for (int u = u0; u < u1; u += 2) {
+        sh_group(P, S, u, u1, rt, RT, rows_ok, wv, lane, hp0, tp0, w0);
+        if (u + 1 >= u1) break;
+        sh_group(P, S, u + 1, u1, rt, RT, rows_ok, wv, lane, hp1, tp1, w1);
+    }
+    __syncthreads();
+    const int nq = nrows / 4;
+    for (int i = tid; i < T * nq; i += blockDim.x) {
+        const int t = i / nq, r = 4 * (i - t * nq);
+        const float4 v = *reinterpret_cast<const float4 *>(&S.yacc[t][r]);
+        const size_t col = (size_t)rb * kShRows + r;
+        if (ES == 1) {
+            *reinterpret_cast<float4 *>(P.y + (size_t)t * d + col) = v;
+        } else {
+            float *dst = P.ypart + ((size_t)c * T + t) * d + col;
+            st_dev2(dst, v.x, v.y);
+            st_dev2(dst + 2, v.z, v.w);
+        }
+    }
+    if (ES == 1 || !arrive_last(&P.dn_cnt[rb], (unsigned)ES, flag)) return;
+    // last chunk to arrive: y = sum of the chunk partials in chunk order, all
+    // of a thread's loads for kRedChunks chunks issued at once
+    constexpr int kRedPer = kDecodeTile * (kShRows / 2) / kDnThreads;
+    constexpr int kRedChunks = 4;
+    const int nh = nrows / 2, nel = T * nh;
+    int off[kRedPer];
+    float2 acc[kRedPer];
 #pragma unroll
-            for (int q = 0; q < kRedPer; ++q) {
-                const int i = min(tid + 256 * q, nel - 1), t = i / (kDnRows / 2);
-                off[q] = t * P.d + rb * kDnRows + 2 * (i - t * (kDnRows / 2));
-                acc[q] = make_float2(0.f, 0.f);
-            }
-            const int nq = (nel - tid + 255) / 256;  // float2 owned by this thread
-            for (int k0 = 0; k0 < ES; k0 += kRedChunks) {
-                float2 v[kRedChunks][kRedPer];
+    for (int q = 0; q < kRedPer; ++q) {
+        const int i = min(tid + kDnThreads * q, nel - 1), t = i / nh;
+        off[q] = t * d + rb * kShRows + 2 * (i - t * nh);
+        acc[q] = make_float2(0.f, 0.f);
+    }
+    const int nown = (nel - tid + kDnThreads - 1) / kDnThreads;
+    for (int k0 = 0; k0 < ES; k0 += kRedChunks) {
+        float2 v[kRedChunks][kRedPer];
 #pragma unroll
-                for (int k = 0; k < kRedChunks; ++k) {
-                    const float *base = P.ypart + (size_t)min(k0 + k, ES - 1) * P.T * P.d;
-#pragma unroll
-                    for (int q = 0; q < kRedPer; ++q)
-                        v[k][q] = q < nq ? ld_dev2(base + off[q]) : make_float2(0.f, 0.f);
-                }
-#pragma unroll
-                for (int k = 0; k < kRedChunks; ++k)
-                    if (k0 + k < ES)
-#pragma unroll
-                        for (int q = 0; q < kRedPer; ++q) {
-                            acc[q].x += v[k][q].x;
-                            acc[q].y += v[k][q].y;
-                        }
-            }
+        for (int k = 0; k < kRedChunks; ++k) {
+            const float *base = P.ypart + (size_t)min(k0 + k, ES - 1) * T * d;
 #pragma unroll
             for (int q = 0; q < kRedPer; ++q)
-                if (q < nq) *reinterpret_cast<float2 *>(P.y + off[q]) = acc[q];
+                v[k][q] = q < nown ? ld_dev2(base + off[q]) : make_float2(0.f, 0.f);
+        }
+#pragma unroll
+        for (int k = 0; k < kRedChunks; ++k)
+            if (k0 + k < ES)
+#pragma unroll
+                for (int q = 0; q < kRedPer; ++q) {
+                    acc[q].x += v[k][q].x;
+                    acc[q].y += v[k][q].y;
+                }
+    }
+#pragma unroll
+    for (int q = 0; q < kRedPer; ++q)
+        if (q < nown) *reinterpret_cast<float2 *>(P.y + off[q]) = acc[q];
+}
+
+template <int TB, int R>
+__global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
+    constexpr int YS = 16 * R + 4;  // padded accumulator row (floats)
+    constexpr int NW = kDnThreads / 64;
+    __shared__ union {
+        DnShared sh;
+        DnRow<TB, R> rw;
+    } S;
+    __shared__ int s_flag;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int nU = P.plan.head[0], npairs = P.plan.head[1];
+    const int RT = P.d / 16;
+    // Dense groups (more than 8 tokens per group on average): reading h once
+    // per 16-row tile would cost more than the weights, so share it through
+    // LDS across 128-row units, with the groups split into chunks.
+    if (npairs > 8 * nU) {
+        const int n_rb = (P.d + kShRows - 1) / kShRows;
+        int ES = (int)gridDim.x / n_rb;
+        if (ES > nU / 2) ES = nU / 2;
+        if (ES > kDecodeChunks) ES = kDecodeChunks;
+        if (ES < 1) ES = 1;
+        const int Uc = (nU + ES - 1) / ES;
+        ES = (nU + Uc - 1) / Uc;
+        for (int unit = blockIdx.x; unit < ES * n_rb; unit += gridDim.x) {
+            const int c = unit / n_rb, rb = unit - c * n_rb;
+            sh_unit(P, S.sh, c, rb, Uc, nU, ES, &s_flag);
+            __syncthreads();
+        }
+        return;
+    }
+    float(*acc)[YS] = S.rw.yacc[wv];
+    for (int rt = blockIdx.x * R; rt < RT; rt += gridDim.x * R) {
+        for (int i = lane; i < P.T * YS; i += 64) acc[i / YS][i % YS] = 0.0f;
+        RowCursor c;
+        c.u = wv;
+        c.j = 0;
+        c.n = 0;
+        c.stride = NW;
+        c.nU = nU;
+        c.enter(P.plan);
+        RowItem<R> I0, I1, I2;
+        load_row_item<R>(P, c, rt, RT, lane, I0);
+        load_row_item<R>(P, c, rt, RT, lane, I1);
+        for (;;) {
+            if (!I0.live) break;
+            load_row_item<R>(P, c, rt, RT, lane, I2);
+            apply_row_item<R, YS>(I0, lane, acc);
+            if (!I1.live) break;
+            load_row_item<R>(P, c, rt, RT, lane, I0);
+            apply_row_item<R, YS>(I1, lane, acc);
+            if (!I2.live) break;
+            load_row_item<R>(P, c, rt, RT, lane, I1);
+            apply_row_item<R, YS>(I2, lane, acc);
+        }
+        __syncthreads();
+        for (int i = tid; i < P.T * 16 * R; i += blockDim.x) {
+            const int t = i / (16 * R), r = i - t * 16 * R;
+            float v = S.rw.yacc[0][t][r];
+#pragma unroll
+            for (int w = 1; w < NW; ++w) v += S.rw.yacc[w][t][r];
+            P.y[(size_t)t * P.d + rt * 16 + r] = v;
         }
         __syncthreads();
     }
@@ -252,15 +377,17 @@ __global__ __launch_bounds__(256, 2) void down_dec_k(DNParams P) {
 
 template <int TB>
 void launch_down_dec_tb(const DNParams &P, int num_cu, hipStream_t s) {
-    static const int occ = resident(down_dec_k<TB>, 256);
-    hipLaunchKernelGGL(down_dec_k<TB>, dim3(occ * num_cu), dim3(256), 0, s, P);
+    constexpr int R = kDnR;
+    static const int occ = resident(down_dec_k<TB, R>, kDnThreads);
+    const int units = P.d / (16 * R);
+    const int grid = units < occ * num_cu ? units : occ * num_cu;
+    hipLaunchKernelGGL((down_dec_k<TB, R>), dim3(grid), dim3(kDnThreads), 0, s, P);
 }
 
 }  // namespace
 
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s) {
     static const int occ = resident(gateup_dec_k, kGuThreads);
-    const counter_layout cl = counters_for(L->dm, L->max_tokens);
     const GUParams gp = gu_params(L, x, T, false);
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
     hipLaunchKernelGGL(gateup_dec_k, dim3(occ * L->num_cu), dim3(kGuThreads), 0, s, gp);
@@ -276,8 +403,7 @@ hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hi
     dp.h_lo = L->h_lo;
     dp.y = y;
     dp.ypart = L->ypart;
-    dp.ypart_elems = L->ypart_elems;
-    dp.cnt = L->counters + cl.down_base();
+    dp.dn_cnt = L->counters + counters_for(L->dm, L->max_tokens).down_base();
     dp.plan = plan_view(L, false);
     prof_mark(L, PP_KERNEL_DOWN, s, true);
     if (T <= 16)

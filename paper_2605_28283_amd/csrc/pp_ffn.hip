@@ -8,8 +8,8 @@
 // a group.
 //
 //   dispatch_k  : per expert, the ascending list of tokens that kept it (block
-//                 scan + scatter), y := 0, and the plan, written by the last
-//                 expert to finish.
+//                 scan + scatter) and the plan, written by the last expert to
+//                 finish; further workgroups clear y.
 //   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
 //                 SiLU product of one group (shared with the decode kernel).
 //   down_pf_k   : unit = (expert, 256 rows); the expert's down block stays in
@@ -67,6 +67,13 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
     __shared__ int scan[8];
     __shared__ int s_flag;
     const int e = blockIdx.x, tid = threadIdx.x;
+    if (e >= E) {  // workgroups past the experts clear y
+        float4 *y4 = reinterpret_cast<float4 *>(y);
+        const size_t nz = (size_t)(gridDim.x - E) * blockDim.x;
+        for (size_t i = (size_t)(e - E) * blockDim.x + tid; i < ny4; i += nz)
+            y4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        return;
+    }
     const int w = e >> 5, b = e & 31;
     int base = 0;
     for (int t0 = 0; t0 < T; t0 += blockDim.x) {
@@ -78,10 +85,6 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
         base += tot;
     }
     if (tid == 0) st_dev_u32(reinterpret_cast<uint32_t *>(ecount + e), (uint32_t)base);
-    float4 *y4 = reinterpret_cast<float4 *>(y);
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + tid; i < ny4;
-         i += (size_t)gridDim.x * blockDim.x)
-        y4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (!arrive_last(cnt, (unsigned)E, &s_flag)) return;
     // prefill plan: expert e's bucket becomes ceil(c_e / 64) groups
     const int c = (tid < E) ? (int)ld_dev_u32(reinterpret_cast<uint32_t *>(ecount + tid)) : 0;
@@ -237,7 +240,7 @@ counter_layout counters_for(const pp_dims &dm, int max_tokens) {
     counter_layout c;
     c.route = 0;
     c.gateup = (size_t)plan_max_groups(dm, max_tokens);
-    c.down = (size_t)(dm.d / 64);
+    c.down = (size_t)((dm.d + 127) / 128);
     c.dispatch = 1;
     c.total = c.route + c.gateup + c.down + c.dispatch;
     return c;
@@ -247,7 +250,8 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     const pp_dims &dm = L->dm;
     const counter_layout cl = counters_for(dm, L->max_tokens);
     prof_mark(L, PP_KERNEL_DISPATCH, s, true);
-    hipLaunchKernelGGL(dispatch_k, dim3(dm.E), dim3(256), 0, s, L->selmask, T, dm.E, L->ecount,
+    hipLaunchKernelGGL(dispatch_k, dim3(dm.E + L->num_cu), dim3(256), 0, s, L->selmask, T, dm.E,
+                       L->ecount,
                        L->tokl, L->max_tokens, y, (size_t)T * dm.d / 4,
                        L->counters + cl.dispatch_base(), plan_view(L, true));
     prof_mark(L, PP_KERNEL_DISPATCH, s, false);

@@ -14,6 +14,7 @@ constexpr int kExpertWidth = 128;      // neurons per expert (de)
 constexpr int kKStep = 32;             // K per bf16 MFMA 16x16x32
 constexpr int kMaxExperts = 256;
 constexpr int kDecodeTile = 64;        // tokens per decode slice (one u64 token mask)
+constexpr int kDecodeChunks = 16;      // expert chunks of the dense-group decode down projection
 constexpr int kRouteTile = 16;         // tokens / experts per router MFMA tile
 constexpr int kMaxWidth = 8192;        // largest supported d
 constexpr int kGroupTokens = 64;       // tokens per prefill expert group
@@ -86,8 +87,7 @@ struct pp_layer {
     uint16_t *h_hi;     // [pairs][128] bf16 high part of h
     uint16_t *h_lo;     // [pairs][128] bf16 low part of h (h - hi)
     size_t max_pairs;
-    float *ypart;       // [ypart_elems] expert-split partial outputs (decode)
-    size_t ypart_elems;
+    float *ypart;       // [kDecodeChunks][kDecodeTile][d] chunk partial outputs (decode, dense groups)
     int32_t *ecount;    // [E] tokens per expert (prefill)
     int32_t *tokl;      // [E][max_tokens] token ids per expert (prefill)
     int32_t *plan;      // PlanView storage: 4 + 4 * plan_max_groups + E + 1 ints
@@ -103,7 +103,7 @@ namespace pp {
 struct counter_layout {
     size_t route;     // none
     size_t gateup;    // one per group: K-slice arrivals
-    size_t down;      // one per 64-row block: decode expert-chunk arrivals
+    size_t down;      // one per 128-row block: decode chunk arrivals
     size_t dispatch;  // one: prefill bucketing arrivals
     size_t total;
     size_t gateup_base() const { return route; }

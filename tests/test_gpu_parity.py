@@ -94,6 +94,20 @@ def test_single_and_max_experts(oracle_mod):
                         assert (res["cnt"] == 1).all()
 
 
+def test_decode_down_modes_ragged_rows(oracle_mod):
+    """d = 576 is not a multiple of 128: the decode down projection's last
+    128-row block has 64 rows.  tau = 0.3 gives sparse groups (row-tile
+    path), tau = 1 dense groups (shared-h path, several expert chunks)."""
+    L = make_layer(576, 40 * 128, 40, 31)
+    for T in (24, 64):
+        x, _ = make_tokens(T, 576, 32 + T)
+        with DevLayer(L, 64) as dl:
+            for tau in (0.3, 1.0):
+                a = parity(oracle_mod, dl, "decode", x, tau)
+                b = dl.run("decode", x, tau)
+                np.testing.assert_array_equal(a["y"], b[2])  # deterministic
+
+
 def test_tau_edges_and_counts(oracle_mod, tiny):
     L, _ = tiny
     x, _ = make_tokens(20, L.d, 13)
