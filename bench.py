@@ -42,6 +42,8 @@ def parse_args():
                     help="skip the 32-layer stacked decode measurement")
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the 2048-token prefill measurement")
+    ap.add_argument("--no-rules", action="store_true",
+                    help="skip the comparison selection rules (strict, top-k, LTE)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (5 times), the "
                          "reference dispatch for scaling HBM byte counters")
@@ -259,6 +261,8 @@ def main():
         pp.prunepath_destroy(h)
     handles = []
     torch.cuda.empty_cache()
+    if not args.no_rules:
+        out["rules"] = bench_rules(args, torch, np, pp, x, n_copies)
     if not args.no_prefill:
         out["prefill"] = bench_prefill(args, torch, np, pp)
     if not args.no_stack:
@@ -275,6 +279,59 @@ def main():
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def bench_rules(args, torch, np, pp, x, n_copies):
+    """The selection rules beside the default nucleus cut, on the same
+    LLaMA-3-8B decode workload (T=32, layer copies drawn on the GPU):
+    the printed strict rule at tau=0.7, forced top-4, and LTE's sigmoid
+    threshold delta=0.95."""
+    from paper_2605_28283_amd.workloads import WORKLOADS
+    w = WORKLOADS["llama8b_decode"]
+    d, d_ff, E, T = w.d, w.d_ff, w.E, args.T
+    res = []
+    for name, flags, p in (("strict", pp.PP_SELECT_STRICT, 0.7), ("topk", pp.PP_SELECT_TOPK, 4.0),
+                           ("lte", pp.PP_SELECT_LTE, 0.95)):
+        hs = []
+        for c in range(n_copies):
+            Wt = device_layer(torch, d, d_ff, E, 3000 + c)
+            hs.append(pp.prunepath_create(d, d_ff, E, T, *Wt, flags=flags))
+            del Wt
+        torch.cuda.synchronize()
+        y = torch.empty((T, d), dtype=torch.float32, device="cuda")
+        idx = torch.empty((T, E), dtype=torch.int32, device="cuda")
+        cnt = torch.empty((T,), dtype=torch.int32, device="cuda")
+        stream = torch.cuda.current_stream()
+        for i in range(args.warmup):
+            pp.prunepath_ffn_decode(hs[i % n_copies], x, T, p, None, y, idx, cnt, stream=stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(args.steps):
+            pp.prunepath_ffn_decode(hs[i % n_copies], x, T, p, None, y, idx, cnt, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        ks, us = [], []
+        for h in hs:
+            pp.prunepath_route(h, x, T, p, None, idx, cnt, stream=stream)
+            torch.cuda.synchronize()
+            ii = idx[:T].cpu().numpy()
+            ks.append(float(cnt[:T].float().mean().item()))
+            us.append(len(np.unique(ii[ii >= 0])))
+        for h in hs:
+            pp.prunepath_destroy(h)
+        torch.cuda.empty_cache()
+        U = float(np.mean(us))
+        nbytes = E * d * 2 + U * 6 * 128 * d + 6 * T * d
+        r = {"rule": name, "param": p, "T": T, "ms_per_step": ms,
+             "tokens_per_s_layer": T / (ms * 1e-3), "k_mean": float(np.mean(ks)),
+             "union_experts": U, "effective_GBps": nbytes / (ms * 1e-3) / 1e9}
+        res.append(r)
+        print("# rule %-6s %5.2f  T=%d  %8.1f us/step  %9.0f tok/s/layer  k %.2f  |U| %.1f  %7.1f GB/s"
+              % (name, p, T, ms * 1e3, r["tokens_per_s_layer"], r["k_mean"], U,
+                 r["effective_GBps"]), file=sys.stderr, flush=True)
+    return res
 
 
 def bench_prefill(args, torch, np, pp):

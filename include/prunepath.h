@@ -53,9 +53,21 @@ typedef enum {
  *  PP_SELECT_NUCLEUS: keep the smallest prefix pi_1..pi_k with C_k >= tau (the
  *    top-p reading named next to the equation); tau >= 1 keeps all E experts,
  *    tau = 0 keeps pi_1.
- *  PP_SELECT_STRICT: the printed rule {pi_1} U {pi_i : C_i < tau}, C_E = 1. */
+ *  PP_SELECT_STRICT: the printed rule {pi_1} U {pi_i : C_i < tau}, C_E = 1.
+ * Two comparison rules run on the same kernels, the call's `tau` argument
+ * then carrying their parameter:
+ *  PP_SELECT_TOPK: the k experts ranked first by the router, pi_1..pi_k, with
+ *    k = tau rounded to the nearest integer and clamped to [1, E] (the forced
+ *    top-k budget of the paper's reconstruction analysis, Sec. 5 "Top-k
+ *    Reconstruction Analysis").
+ *  PP_SELECT_LTE: the independent threshold of Eq. (lte_hard_set),
+ *    {e : sigmoid(g_e) > delta} with delta = tau; a token may keep no expert
+ *    (count 0, y row 0).  The kept experts are still listed in pi order.
+ * At most one PP_SELECT_* bit may be set. */
 #define PP_SELECT_NUCLEUS 0u
 #define PP_SELECT_STRICT 1u
+#define PP_SELECT_TOPK 4u
+#define PP_SELECT_LTE 8u
 /* Aggregation: PP_AGG_SUM = plain sum of the kept experts' outputs (the
  * all-expert case is the dense FFN, Eq. moefication_decomp);
  * PP_AGG_SIGMOID = each kept expert scaled by sigmoid(g_e), Eq. moe_output. */
@@ -78,7 +90,8 @@ typedef enum {
  *                perm[128e .. 128e+127]), or NULL for the identity; it must be
  *                a permutation of 0..d_ff-1 (PP_EINVAL otherwise).
  *   router_bias: [E] fp32 added to the logits (g = W_r x + b), or NULL.
- *   flags      : PP_SELECT_* | PP_AGG_*.
+ *   flags      : one PP_SELECT_* rule | PP_AGG_* (PP_EINVAL for unknown bits or
+ *                two selection rules).
  * The weights are copied and repacked into library-owned device memory; the
  * call synchronises `hip_stream` before returning, after which the caller may
  * free its arrays.  On failure *out is set to NULL. */
@@ -90,12 +103,13 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
 /* prunepath_route -- routing only (Eqs. routing_logits, softmax_prob,
  * tau_thresh_activate).
  *   x          : [T, d] bf16 tokens, 1 <= T <= max_tokens.
- *   tau        : budget, >= 0 (NaN or negative: PP_EINVAL).
+ *   tau        : budget, >= 0 (NaN or negative: PP_EINVAL): the cumulative
+ *                mass (nucleus, strict), k (top-k) or delta (LTE).
  *   inv_temp   : [T] fp32 per-token inverse temperature, or NULL (= 1):
  *                g = (W_r x + b) * inv_temp[t].
  *   expert_idx : [T, E] int32 out; row t holds the kept experts pi_1..pi_k in
  *                descending-logit order, then -1.
- *   count      : [T] int32 out; k for each token.
+ *   count      : [T] int32 out; k for each token (>= 1 except with LTE).
  *   gate_w     : [T, E] fp32 out or NULL; weight applied to the expert in the
  *                same slot of expert_idx (sigmoid(g_e) with PP_AGG_SIGMOID,
  *                else 1), 0 in unused slots. */

@@ -21,6 +21,8 @@ from . import build as _build
 
 SELECT_NUCLEUS = 0
 SELECT_STRICT = 1
+SELECT_TOPK = 4
+SELECT_LTE = 8
 AGG_SUM = 0
 AGG_SIGMOID = 2
 
@@ -145,9 +147,18 @@ def near_tie(cum, tau, band=1e-5, flags=0):
     keeps every expert regardless of C (nucleus with tau >= 1, strict with
     tau > 1)."""
     cum = np.asarray(cum)
+    if flags & (SELECT_TOPK | SELECT_LTE):
+        return np.zeros(cum.shape[0], bool)  # these rules do not read C
     if (flags & SELECT_STRICT and tau > 1.0) or (not flags & SELECT_STRICT and tau >= 1.0):
         return np.zeros(cum.shape[0], bool)
     return (np.abs(cum[:, :-1] - tau) <= band).any(axis=1)
+
+
+def lte_tie(g, delta, band=1e-6):
+    """Tokens with an expert whose sigmoid score lies within `band` of delta:
+    their LTE decision may differ between fp32 and fp64 evaluation."""
+    s = 1.0 / (1.0 + np.exp(-np.asarray(g, np.float64)))
+    return (np.abs(s - delta) <= band).any(axis=1)
 
 
 def order_tie(g, idx, count, band=1e-5):

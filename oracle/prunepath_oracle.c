@@ -23,6 +23,10 @@
  *    reaches tau; tau >= 1 keeps all E experts (exact-arithmetic result: every
  *    softmax probability is positive).  Flag PPO_SELECT_STRICT: the rule as
  *    printed, {pi_1} U {pi_i : C_i < tau}, with C_E = 1 by definition.
+ *    Comparison rules on the same router: PPO_SELECT_TOPK keeps pi_1..pi_k,
+ *    k = tau rounded to nearest and clamped to [1, E] (the forced top-k of the
+ *    reconstruction analysis); PPO_SELECT_LTE keeps {e : sigmoid(g_e) > tau},
+ *    Eq. (lte_hard_set), possibly empty, listed in pi order.
  *  - Ties in the ordering: the lower expert index comes first.  The order is
  *    taken on g, which is equivalent to ordering p (softmax is monotone).
  *  - Aggregation.  Default: plain sum (Eq. moefication_decomp, whose all-expert
@@ -42,6 +46,8 @@
 
 #define PPO_SELECT_STRICT 1u
 #define PPO_AGG_SIGMOID 2u
+#define PPO_SELECT_TOPK 4u
+#define PPO_SELECT_LTE 8u
 
 /* Exact value of a bf16 bit pattern: its bits are the top half of an IEEE
  * binary32 number. */
@@ -153,6 +159,17 @@ int ppo_route(int64_t T, int64_t d, int64_t E, const uint16_t *x, const uint16_t
         ppo_order(E, gt, pi);
         for (int64_t i = 0; i < E; ++i) ps[i] = p[pi[i]];
         int64_t k = ppo_cut(E, ps, tau, flags, cum + t * E);
+        if (flags & PPO_SELECT_TOPK) {
+            double r = floor(tau + 0.5);
+            k = r < 1.0 ? 1 : (r > (double)E ? E : (int64_t)r);
+        } else if (flags & PPO_SELECT_LTE) {
+            /* Eq. (lte_hard_set): independent sigmoid scores against delta = tau;
+             * the kept experts are the ones ranked first, since sigmoid is
+             * increasing */
+            k = 0;
+            for (int64_t e = 0; e < E; ++e)
+                if (1.0 / (1.0 + exp(-gt[e])) > tau) ++k;
+        }
         count[t] = (int32_t)k;
         for (int64_t i = 0; i < E; ++i) idx[t * E + i] = i < k ? pi[i] : -1;
         free(p);

@@ -6,7 +6,8 @@ synthetic-input generators (``workloads``).
 """
 from ._lib import (EXPORTED, PP_AGG_SIGMOID, PP_AGG_SUM, PP_EHIP, PP_EINVAL, PP_ENOMEM,  # noqa: F401
                    PP_EUNSUPPORTED, PP_KERNEL_COUNT, PP_KERNEL_DISPATCH, PP_KERNEL_DOWN,
-                   PP_KERNEL_GATEUP, PP_KERNEL_ROUTE, PP_OK, PP_SELECT_NUCLEUS, PP_SELECT_STRICT,
-                   PrunePathError, load, prunepath_create, prunepath_destroy, prunepath_ffn_decode,
-                   prunepath_ffn_prefill, prunepath_profile_begin, prunepath_profile_end,
-                   prunepath_residual_rmsnorm, prunepath_route, prunepath_status_string)
+                   PP_KERNEL_GATEUP, PP_KERNEL_ROUTE, PP_OK, PP_SELECT_LTE, PP_SELECT_NUCLEUS,
+                   PP_SELECT_STRICT, PP_SELECT_TOPK, PrunePathError, load, prunepath_create,
+                   prunepath_destroy, prunepath_ffn_decode, prunepath_ffn_prefill,
+                   prunepath_profile_begin, prunepath_profile_end, prunepath_residual_rmsnorm,
+                   prunepath_route, prunepath_status_string)

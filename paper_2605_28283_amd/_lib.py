@@ -21,6 +21,8 @@ PP_EUNSUPPORTED = 4
 
 PP_SELECT_NUCLEUS = 0
 PP_SELECT_STRICT = 1
+PP_SELECT_TOPK = 4
+PP_SELECT_LTE = 8
 PP_AGG_SUM = 0
 PP_AGG_SIGMOID = 2
 

@@ -114,7 +114,12 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     if (!W_r || !W_gate || !W_up || !W_down) return PP_EINVAL;
     if (d < 1 || d_ff < 1 || E < 1 || max_tokens < 1 || max_tokens > kMaxTokensLimit)
         return PP_EINVAL;
-    if (flags & ~(PP_SELECT_STRICT | PP_AGG_SIGMOID)) return PP_EINVAL;
+    if (flags & ~(PP_SELECT_STRICT | PP_SELECT_TOPK | PP_SELECT_LTE | PP_AGG_SIGMOID))
+        return PP_EINVAL;
+    {
+        const uint32_t sel = flags & (PP_SELECT_STRICT | PP_SELECT_TOPK | PP_SELECT_LTE);
+        if (sel & (sel - 1u)) return PP_EINVAL;  // more than one selection rule
+    }
     if (d_ff % E != 0) return PP_EINVAL;
     if (E > kMaxExperts) return PP_EUNSUPPORTED;
     if (d_ff / E != kExpertWidth) return PP_EUNSUPPORTED;

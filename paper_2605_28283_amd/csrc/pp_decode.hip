@@ -7,8 +7,8 @@
 //
 //   gateup_dec_k: unit = (group, K-slice), the gate/up projections and the
 //                 SiLU product of one group (code shared with prefill); the
-//                 K-split is chosen so that all units fit in one round of
-//                 resident workgroups.
+//                 K-split (one slice more for some groups) makes the units
+//                 fill the resident workgroups exactly, one round.
 //   down_dec_k  : sparse groups (<= 8 tokens per group on average): unit = one
 //                 16-row tile of d over all groups; each of the 8 wavefronts
 //                 takes every eighth group, tile by tile of 16 tokens (three
@@ -52,15 +52,34 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     const int tid = threadIdx.x;
     decode_plan<true>(P, D);
     const int nG = D.nG, npairs = D.npairs;
-    const int KS = choose_ks(P, nG, npairs, (int)gridDim.x);
-    const int units = nG * KS;
-    for (int unit = (int)blockIdx.x; unit < units; unit += (int)gridDim.x) {
-        const int g = unit / KS, ks = unit - g * KS;
+    // K-slices: KS per group, and one more for the first `extra` groups, so
+    // that the units fill the resident workgroups exactly -- every CU then
+    // streams the same number of units (with units left over, the CUs that
+    // hold one unit fewer finish early and the rest form a tail)
+    const int slots = (int)gridDim.x;
+    const int KS = choose_ks(P, nG, npairs, slots);
+    const int max_ks = P.NS / kMinStepsPerSlice > 0 ? P.NS / kMinStepsPerSlice : 1;
+    int extra = 0;
+    if (KS < max_ks && (size_t)(KS + 1) * npairs <= P.abpart_rows)
+        extra = min(nG, max(0, slots - nG * KS));
+    const int big = extra * (KS + 1);
+    const int units = nG * KS + extra;
+    for (int unit = (int)blockIdx.x; unit < units; unit += slots) {
+        int g, ks, ksg;
+        if (unit < big) {
+            g = unit / (KS + 1);
+            ks = unit - g * (KS + 1);
+            ksg = KS + 1;
+        } else {
+            const int v = unit - big;
+            g = extra + v / KS;
+            ks = v - (g - extra) * KS;
+            ksg = KS;
+        }
         const unsigned long long m = D.mask[g];
         if (tid < 64 && ((m >> tid) & 1ull)) stok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
         __syncthreads();
-        gateup_group(P, D.e[g], __popcll(m), D.pair[g], g, ks, KS, npairs, stok, xf,
-                            &s_flag);
+        gateup_group(P, D.e[g], __popcll(m), D.pair[g], g, ks, ksg, npairs, stok, xf, &s_flag);
         __syncthreads();
     }
 }

@@ -159,7 +159,8 @@ __device__ __forceinline__ unsigned long long pi_key(float g, int i) {
 //   4. nucleus: expert i is kept iff rank_i == 0 or B_i / S < tau (every
 //      expert when tau >= 1), so k = #kept = min{i : C_i >= tau};
 //      strict: m = #{i : rank_i < E - 1, (B_i + e_i) / S < tau},
-//      k = max(1, m + [tau > 1]); kept iff rank_i < k.
+//      k = max(1, m + [tau > 1]); top-k: k = round(tau) in [1, E];
+//      LTE: k = #{i : sigmoid(g_i) > tau}.  Kept iff rank_i < k.
 // Floating-point addition is monotone, so B grows with the rank and the kept
 // set is always a prefix of pi.  The work is O(E^2 / threads) with no
 // dependence on k; all orders of summation are fixed, independent of T.
@@ -253,15 +254,23 @@ __global__ __launch_bounds__(kSelThreads) void select_k(RouteParams P) {
             rank += __float_as_int(pq.y);
         }
     }
+    const bool topk = (P.flags & PP_SELECT_TOPK) != 0;
+    const bool lte = (P.flags & PP_SELECT_LTE) != 0;
+    const float sg = 1.0f / (1.0f + expf(-g));  // sigmoid(g_e): LTE score and gate
     int cond = 0;
     if (tid < E) {
-        if (strict)
+        if (lte)
+            cond = sg > P.tau ? 1 : 0;
+        else if (strict)
             cond = (rank < E - 1 && (B + ex) / S < P.tau) ? 1 : 0;
         else
             cond = (all || rank == 0 || B / S < P.tau) ? 1 : 0;
     }
     int k = __syncthreads_count(cond);
-    if (strict) {
+    if (topk) {
+        k = (int)fminf(floorf(P.tau + 0.5f), (float)E);
+        k = k < 1 ? 1 : k;
+    } else if (strict) {
         k += P.tau > 1.0f ? 1 : 0;
         k = k < 1 ? 1 : k;
     }
@@ -269,7 +278,7 @@ __global__ __launch_bounds__(kSelThreads) void select_k(RouteParams P) {
     if (tid < E) {
         const bool kept = rank < k;
         const bool sig = (P.flags & PP_AGG_SIGMOID) != 0;
-        const float w = sig ? 1.0f / (1.0f + expf(-g)) : 1.0f;
+        const float w = sig ? sg : 1.0f;
         P.idx[(size_t)t * E + rank] = kept ? tid : -1;
         if (P.gate_w) P.gate_w[(size_t)t * E + rank] = kept ? w : 0.0f;
         if (kept) {

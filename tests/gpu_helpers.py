@@ -6,6 +6,7 @@ import paper_2605_28283_amd as pp
 
 TOL = 1e-2          # max |y - y_ref| <= TOL * RMS(y_ref)  (global RMS of the call)
 TIE_BAND = 1e-5     # cumulative-mass / logit band treated as a tie
+LTE_BAND = 1e-6     # sigmoid-score band around delta treated as a tie (LTE rule)
 
 
 def torch():
@@ -87,24 +88,45 @@ def check_tie_token(g, C, tau, flags, kept, oracle):
     assert (np.diff(g[kept]) <= TIE_BAND).all()
 
 
+def check_rule_tie_token(g, tau, flags, kept, oracle):
+    """Top-k / LTE token inside a tie band: the kept set is a prefix of the
+    logit order up to TIE_BAND, of the right size (top-k) or with every kept
+    score above and every dropped score below delta up to LTE_BAND (LTE)."""
+    E = len(g)
+    rest = np.setdiff1d(np.arange(E), kept)
+    if len(kept) and len(rest):
+        assert g[kept].min() >= g[rest].max() - TIE_BAND
+    if flags & oracle.SELECT_TOPK:
+        assert len(kept) == min(E, max(1, int(np.floor(tau + 0.5))))
+    else:
+        s = 1.0 / (1.0 + np.exp(-g))
+        assert (s[kept] >= tau - LTE_BAND).all() and (s[rest] <= tau + LTE_BAND).all()
+
+
 def check_selection(oracle, L, x, tau, flags, idx_g, cnt_g, inv_temp=None):
     """Bit-exact selections except tokens whose cumulative mass (or logit order
     at the cut) lies within TIE_BAND; those are counted and their GPU result
     is checked for validity.  Returns (oracle route dict, exempt mask)."""
     r = oracle.route(x, L.W_r, tau, flags=flags, bias=L.bias, inv_temp=inv_temp)
-    sel_flags = flags & oracle.SELECT_STRICT
+    sel_flags = flags & (oracle.SELECT_STRICT | oracle.SELECT_TOPK | oracle.SELECT_LTE)
+    lte = bool(flags & oracle.SELECT_LTE)
     exempt = oracle.near_tie(r["cum"], tau, TIE_BAND, flags=sel_flags) | \
         oracle.order_tie(r["g"], r["idx"], r["count"], TIE_BAND)
+    if lte:
+        exempt |= oracle.lte_tie(r["g"], tau, LTE_BAND)
     T, E = idx_g.shape
     bad = []
     for t in range(T):
         k = int(cnt_g[t])
-        assert 1 <= k <= E, (t, k)
+        assert (0 if lte else 1) <= k <= E, (t, k)
         kept = idx_g[t, :k]
         assert len(set(kept.tolist())) == k and (kept >= 0).all() and (kept < E).all(), t
         assert (idx_g[t, k:] == -1).all(), t
         if exempt[t]:
-            check_tie_token(r["g"][t], r["cum"][t], tau, flags, kept, oracle)
+            if lte or flags & oracle.SELECT_TOPK:
+                check_rule_tie_token(r["g"][t], tau, flags, kept, oracle)
+            else:
+                check_tie_token(r["g"][t], r["cum"][t], tau, flags, kept, oracle)
             continue
         if k != r["count"][t] or not (kept == r["idx"][t, :k]).all():
             bad.append(t)
@@ -121,6 +143,9 @@ def check_output(oracle, L, x, flags, idx_g, cnt_g, y_g, g_ref, rows=None):
     err = np.abs(y_g[rows].astype(np.float64) - y_ref)
     rms = float(np.sqrt(np.mean(y_ref ** 2)))
     assert np.isfinite(y_g[rows]).all()
+    if rms == 0.0:  # no token kept an expert (LTE): y must be exactly zero
+        assert (y_g[rows] == 0).all()
+        return 0.0
     worst = float(err.max()) / rms
     assert worst <= TOL, "max|dy|/RMS = %.3g" % worst
     return worst

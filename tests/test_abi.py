@@ -61,7 +61,9 @@ def _create(**kw):
     (dict(d=0), pp.PP_EINVAL),
     (dict(max_tokens=0), pp.PP_EINVAL),
     (dict(max_tokens=70000), pp.PP_EINVAL),
-    (dict(flags=4), pp.PP_EINVAL),
+    (dict(flags=16), pp.PP_EINVAL),               # unknown flag bit
+    (dict(flags=pp.PP_SELECT_STRICT | pp.PP_SELECT_TOPK), pp.PP_EINVAL),   # two rules
+    (dict(flags=pp.PP_SELECT_TOPK | pp.PP_SELECT_LTE | pp.PP_AGG_SIGMOID), pp.PP_EINVAL),
     (dict(d_ff=2050), pp.PP_EINVAL),
     (dict(d_ff=4096), pp.PP_EUNSUPPORTED),        # experts of 256 neurons
     (dict(E=512, d_ff=512 * 128), pp.PP_EUNSUPPORTED),

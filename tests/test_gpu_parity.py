@@ -16,6 +16,7 @@ from gpu_helpers import DevLayer, check_output, check_selection, parity, to_dev
 pytestmark = pytest.mark.gpu
 
 NUC, STRICT, SUM, SIG = pp.PP_SELECT_NUCLEUS, pp.PP_SELECT_STRICT, pp.PP_AGG_SUM, pp.PP_AGG_SIGMOID
+TOPK, LTE = pp.PP_SELECT_TOPK, pp.PP_SELECT_LTE
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -92,6 +93,37 @@ def test_single_and_max_experts(oracle_mod):
                     res = parity(oracle_mod, dl, mode, x, tau)
                     if E == 1:
                         assert (res["cnt"] == 1).all()
+
+
+@pytest.mark.parametrize("flags,params", [
+    (TOPK | SUM, (1, 2, 5, 16, 40)),
+    (TOPK | SIG, (3,)),
+    (LTE | SUM, (0.0, 0.3, 0.6, 0.9, 0.999, 1.0)),
+    (LTE | SIG, (0.5,)),
+])
+@pytest.mark.parametrize("mode", ["decode", "prefill", "route"])
+def test_comparison_rules(oracle_mod, flags, params, mode):
+    """Forced top-k and the LTE sigmoid threshold on the same kernels: the
+    selections and outputs against the oracle; LTE may keep no expert."""
+    L = make_layer(512, 16 * 128, 16, 41)
+    x, _ = make_tokens(70, 512, 42)
+    with DevLayer(L, 80, flags=flags) as dl:
+        for p in params:
+            if mode == "route":
+                idx, cnt, gw = dl.run("route", x, p)
+                r, _ = check_selection(oracle_mod, L, x, p, flags, idx, cnt)
+                continue
+            res = parity(oracle_mod, dl, mode, x, p)
+            if flags & LTE and p >= 1.0:
+                assert (res["cnt"] == 0).all() and (res["y"] == 0).all()
+
+
+def test_comparison_rules_llama8b_decode(oracle_mod, llama8b):
+    L, w, _ = llama8b
+    x, _ = workload_tokens(w, 32, 0)
+    for flags, p in ((TOPK, 4), (LTE, 0.95), (STRICT, 0.7)):
+        with DevLayer(L, 64, flags=flags) as dl:
+            parity(oracle_mod, dl, "decode", x, p, rows=np.arange(0, 32, 5))
 
 
 def test_decode_down_modes_ragged_rows(oracle_mod):

@@ -383,3 +383,61 @@ def test_rmsnorm_invariants(oracle_mod):
     # the bits are the nearest bf16 values of u
     back = bf16_to_f32(bits).astype(np.float64)
     assert (np.abs(back - u) <= np.abs(u) * 2.0 ** -8 + 1e-300).all()
+
+
+# ------------------------------------------ comparison rules: top-k and LTE
+
+def _exact_logit_layer(gvals):
+    """A router whose logits for the one-hot token x = e_0 are exactly gvals
+    (bf16-representable values placed in column 0 of W_r)."""
+    E, d = len(gvals), 64
+    W_r = np.zeros((E, d), np.float32)
+    W_r[:, 0] = gvals
+    x = np.zeros((1, d), np.float32)
+    x[0, 0] = 1.0
+    return bf16_bits(x), bf16_bits(W_r)
+
+
+def test_lte_worked_cases(oracle_mod):
+    """Eq. (lte_hard_set) by hand: g = (0, 1, -1, 2) gives sigmoid scores
+    (0.5, 0.731, 0.269, 0.881); experts listed by descending g: 3, 1, 0, 2."""
+    x, W_r = _exact_logit_layer([0.0, 1.0, -1.0, 2.0])
+    for delta, kept in ((0.2, [3, 1, 0, 2]), (0.3, [3, 1, 0]), (0.5, [3, 1]),
+                        (0.8, [3]), (0.9, []), (1.0, []), (0.0, [3, 1, 0, 2])):
+        r = oracle_mod.route(x, W_r, delta, flags=oracle_mod.SELECT_LTE)
+        k = int(r["count"][0])
+        assert r["idx"][0, :k].tolist() == kept, delta
+        assert (r["idx"][0, k:] == -1).all()
+
+
+def test_topk_worked_cases(oracle_mod):
+    x, W_r = _exact_logit_layer([0.0, 1.0, -1.0, 2.0])
+    for k_arg, kept in ((2, [3, 1]), (0.4, [3]), (2.5, [3, 1, 0]), (2.49, [3, 1]),
+                        (100, [3, 1, 0, 2]), (0, [3])):
+        r = oracle_mod.route(x, W_r, k_arg, flags=oracle_mod.SELECT_TOPK)
+        k = int(r["count"][0])
+        assert r["idx"][0, :k].tolist() == kept, k_arg
+
+
+def test_rules_share_the_order(oracle_mod):
+    """Every rule keeps a prefix of the same order pi; top-k with the nucleus
+    count reproduces the nucleus selection; LTE counts fall as delta rises."""
+    L = small_layer(d=128, E=10, seed=21)
+    x, _ = make_tokens(40, 128, 22)
+    nuc = oracle_mod.route(x, L.W_r, 0.6)
+    full = oracle_mod.route(x, L.W_r, 1.0)
+    for t in range(40):
+        k = int(nuc["count"][t])
+        top = oracle_mod.route(x[t:t + 1], L.W_r, float(k), flags=oracle_mod.SELECT_TOPK)
+        assert top["idx"][0, :k].tolist() == nuc["idx"][t, :k].tolist()
+    prev = None
+    for delta in (0.05, 0.2, 0.5, 0.8, 0.95, 0.999):
+        r = oracle_mod.route(x, L.W_r, delta, flags=oracle_mod.SELECT_LTE)
+        for t in range(40):
+            k = int(r["count"][t])
+            assert r["idx"][t, :k].tolist() == full["idx"][t, :k].tolist()
+            s = 1.0 / (1.0 + np.exp(-r["g"][t]))
+            assert k == int((s > delta).sum())
+        if prev is not None:
+            assert (r["count"] <= prev).all()
+        prev = r["count"]
