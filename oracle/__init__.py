@@ -5,7 +5,8 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 never calls the HIP library; the two share only the seeded bf16 inputs.
 
 The arithmetic lives in ``prunepath_oracle.c`` (fp64, per token, following the
-paper's Sec. 3.1 equations in order); this module only marshals numpy arrays.
+paper's Sec. 3.1 equations in order, and the Sec. 3.2 / Sec. 4.2.3 routing
+regularisers with their gradient); this module only marshals numpy arrays.
 
 Readings taken where the paper is open are stated in the C file's header.
 Every function here is pinned by ``tests/test_oracle_pins.py`` against closed
@@ -53,6 +54,9 @@ def _load():
         lib.ppo_bf16_round_n.restype = None
         lib.ppo_rmsnorm.argtypes = [I64, I64, P, ctypes.c_double, P, P]
         lib.ppo_rmsnorm.restype = ctypes.c_int
+        lib.ppo_router_loss.argtypes = [I64, I64, P, ctypes.c_double, ctypes.c_double,
+                                        ctypes.c_double, ctypes.c_double, P, P]
+        lib.ppo_router_loss.restype = ctypes.c_int
         lib.ppo_num_threads.argtypes = []
         lib.ppo_num_threads.restype = ctypes.c_int
         _lib = lib
@@ -194,3 +198,18 @@ def rmsnorm(x, eps=1e-5):
     if _load().ppo_rmsnorm(T, d, _ptr(x), float(eps), _ptr(u), _ptr(bits)) != 0:
         raise ValueError("oracle rmsnorm: bad arguments")
     return u, bits
+
+
+def router_loss(g, eps=1e-8, eta=1.0, lam=1.0, gamma=0.0, grad=True):
+    """Routing regularisers over a batch of router logits g [B, E] (Sec. 3.2
+    and Sec. 4.2.3): returns (losses, dg) with losses = [L_ent, L_bal, L_gate,
+    eta L_ent + lam L_bal + gamma L_gate] and dg = dL/dg [B, E] (None when
+    grad is False)."""
+    g = _c(g, np.float64)
+    B, E = g.shape
+    losses = np.empty(4)
+    dg = np.empty_like(g) if grad else None
+    if _load().ppo_router_loss(B, E, _ptr(g), float(eps), float(eta), float(lam), float(gamma),
+                               _ptr(losses), _ptr(dg)) != 0:
+        raise ValueError("oracle router_loss: bad arguments")
+    return losses, dg

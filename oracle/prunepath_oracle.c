@@ -292,3 +292,77 @@ int ppo_rmsnorm(int64_t T, int64_t d, const double *x, double eps, double *u, ui
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Routing regularisers of the training objective, forward and gradient.
+ *
+ *   p_ij   = softmax_j(g_i)                              Eq. (softmax_prob)
+ *   L_ent  = -(1/B) sum_i sum_j p_ij log(p_ij + eps)     Eq. (entropy_loss), Sec. 3.2
+ *   L_bal  = E sum_j (m_j)^2, m_j = (1/B) sum_i p_ij     Eq. (load_balance_loss), Sec. 3.2
+ *   L_gate = (1/(B E)) sum_i sum_j sigmoid(g_ij)         gate-magnitude term, Sec. 4.2.3
+ *   L      = eta L_ent + lambda L_bal + gamma L_gate     Eq. (train_loss) with the Sec. 4.2.3 term
+ *
+ * (the task loss of Eq. (train_loss) is not part of this function).
+ * losses = [L_ent, L_bal, L_gate, L].  dg (optional) = dL/dg by the chain
+ * rule through the full softmax Jacobian dp_ij/dg_ik = p_ij (delta_jk - p_ik).
+ * Reading for p_ij = 0 (possible only with eps = 0): the term p log p is 0,
+ * its limit.
+ * ------------------------------------------------------------------------ */
+int ppo_router_loss(int64_t B, int64_t E, const double *g, double eps, double eta, double lambda,
+                    double gamma, double *losses, double *dg) {
+    if (B < 1 || E < 1 || !g || !losses || !(eps >= 0.0)) return -1;
+    double *p = (double *)malloc(sizeof(double) * (size_t)(B * E));
+    double *m = (double *)calloc((size_t)E, sizeof(double));
+    double *dldp = (double *)malloc(sizeof(double) * (size_t)E);
+    if (!p || !m || !dldp) {
+        free(p);
+        free(m);
+        free(dldp);
+        return -2;
+    }
+    for (int64_t i = 0; i < B; ++i) ppo_softmax(E, g + i * E, p + i * E);
+
+    double ent = 0.0, gate = 0.0;
+    for (int64_t i = 0; i < B; ++i)
+        for (int64_t j = 0; j < E; ++j) {
+            double pij = p[i * E + j];
+            if (pij > 0.0) ent += pij * log(pij + eps);
+            gate += 1.0 / (1.0 + exp(-g[i * E + j]));
+        }
+    double l_ent = -ent / (double)B;
+    for (int64_t j = 0; j < E; ++j) {
+        for (int64_t i = 0; i < B; ++i) m[j] += p[i * E + j];
+        m[j] /= (double)B;
+    }
+    double l_bal = 0.0;
+    for (int64_t j = 0; j < E; ++j) l_bal += m[j] * m[j];
+    l_bal *= (double)E;
+    double l_gate = gate / ((double)B * (double)E);
+    losses[0] = l_ent;
+    losses[1] = l_bal;
+    losses[2] = l_gate;
+    losses[3] = eta * l_ent + lambda * l_bal + gamma * l_gate;
+
+    if (dg) {
+        for (int64_t i = 0; i < B; ++i) {
+            const double *pi = p + i * E;
+            /* dL/dp_ij: d/dp [p log(p + eps)] = log(p + eps) + p / (p + eps);
+             * dL_bal/dp_ij = 2 E m_j / B */
+            for (int64_t j = 0; j < E; ++j) {
+                double de = pi[j] > 0.0 ? log(pi[j] + eps) + pi[j] / (pi[j] + eps) : 0.0;
+                dldp[j] = -eta * de / (double)B + lambda * 2.0 * (double)E * m[j] / (double)B;
+            }
+            for (int64_t k = 0; k < E; ++k) {
+                double acc = 0.0;
+                for (int64_t j = 0; j < E; ++j)
+                    acc += dldp[j] * pi[j] * ((j == k ? 1.0 : 0.0) - pi[k]);
+                double s = 1.0 / (1.0 + exp(-g[i * E + k]));
+                dg[i * E + k] = acc + gamma * s * (1.0 - s) / ((double)B * (double)E);
+            }
+        }
+    }
+    free(p);
+    free(m);
+    free(dldp);
+    return 0;
+}

@@ -441,3 +441,131 @@ def test_rules_share_the_order(oracle_mod):
         if prev is not None:
             assert (r["count"] <= prev).all()
         prev = r["count"]
+
+
+# ------------------------------------------------- routing regularisers (Sec. 3.2)
+def _sig(v):
+    return 1.0 / (1.0 + np.exp(-v))
+
+
+def test_router_loss_uniform_closed_form(oracle_mod):
+    """Equal logits: p = 1/E, so L_ent = log E (eps = 0), L_bal = 1, L_gate =
+    sigmoid(c); uniform routing is a stationary point of L_ent and L_bal, so
+    only the gate term's gradient sigmoid'(c) / (B E) is left."""
+    for B, E, c in [(1, 1, 0.0), (3, 8, 0.7), (16, 112, -2.5), (5, 256, 3.0)]:
+        g = np.full((B, E), c)
+        for eta, lam, gam in [(1.0, 0.0, 0.0), (0.3, 2.0, 0.5)]:
+            L, dg = oracle_mod.router_loss(g, eps=0.0, eta=eta, lam=lam, gamma=gam)
+            s = _sig(c)
+            want = [math.log(E), 1.0, s]
+            np.testing.assert_allclose(L[:3], want, rtol=1e-13, atol=1e-15)
+            assert L[3] == pytest.approx(eta * want[0] + lam * want[1] + gam * want[2], rel=1e-13)
+            np.testing.assert_allclose(dg, gam * s * (1 - s) / (B * E), rtol=1e-9, atol=1e-17)
+
+
+def test_router_loss_two_experts_is_binary_entropy(oracle_mod):
+    """E = 2: softmax of two logits is the logistic function of their
+    difference, so L_ent is the mean binary entropy (scipy.stats.entropy) and
+    m_0 the mean of sigmoid(g_0 - g_1)."""
+    from scipy.stats import entropy
+    rng = np.random.default_rng(11)
+    g = rng.normal(0, 2, (9, 2))
+    L, _ = oracle_mod.router_loss(g, eps=0.0, grad=False)
+    q = _sig(g[:, 0] - g[:, 1])
+    ent = np.mean([entropy([a, 1 - a]) for a in q])
+    m0 = q.mean()
+    assert L[0] == pytest.approx(ent, rel=1e-12)
+    assert L[1] == pytest.approx(2 * (m0 ** 2 + (1 - m0) ** 2), rel=1e-12)
+    assert L[2] == pytest.approx(_sig(g).mean(), rel=1e-12)
+
+
+def test_router_loss_cyclic_rows_are_balanced(oracle_mod):
+    """B = E rows that are the E cyclic shifts of one logit vector: every
+    expert receives the same total mass, so L_bal = 1 exactly, and every row
+    has the entropy of the first (scipy.stats.entropy of scipy's softmax)."""
+    from scipy.stats import entropy
+    rng = np.random.default_rng(5)
+    E = 13
+    v = rng.normal(0, 3, E)
+    g = np.stack([np.roll(v, s) for s in range(E)])
+    L, _ = oracle_mod.router_loss(g, eps=0.0, grad=False)
+    assert L[1] == pytest.approx(1.0, rel=1e-12)
+    assert L[0] == pytest.approx(entropy(sp_softmax(v)), rel=1e-12)
+
+
+def test_router_loss_collapse_and_bounds(oracle_mod):
+    """Sum_j m_j = 1 gives 1 <= L_bal <= E (equality only for uniform m, or
+    all mass on one expert); L_ent lies in [0, log E] for eps = 0, decreases
+    as eps grows, and a one-hot batch gives L_ent = 0, L_bal = E."""
+    rng = np.random.default_rng(8)
+    for E in (2, 7, 64):
+        g = rng.normal(0, 4, (20, E))
+        L0, _ = oracle_mod.router_loss(g, eps=0.0, grad=False)
+        L1, _ = oracle_mod.router_loss(g, eps=1e-2, grad=False)
+        assert 1.0 < L0[1] < E
+        assert 0.0 < L0[0] < math.log(E)
+        assert L1[0] < L0[0] and L1[1] == L0[1]
+        hot = np.full((6, E), -1e4)
+        hot[:, E - 1] = 0.0          # p = e_{E-1} exactly in fp64 (exp underflows)
+        L, dg = oracle_mod.router_loss(hot, eps=0.0, eta=1.0, lam=0.0)
+        assert L[0] == 0.0 and L[1] == pytest.approx(E, rel=1e-15)
+        assert np.isfinite(dg).all()
+
+
+def test_router_loss_batch_normalisation(oracle_mod):
+    """L_ent, L_bal and L_gate are batch means: a batch repeated twice has the
+    same losses, and its gradient is half the single batch's per row."""
+    rng = np.random.default_rng(2)
+    g = rng.normal(0, 1.5, (7, 10))
+    kw = dict(eps=1e-6, eta=0.7, lam=1.3, gamma=0.4)
+    L1, d1 = oracle_mod.router_loss(g, **kw)
+    L2, d2 = oracle_mod.router_loss(np.vstack([g, g]), **kw)
+    np.testing.assert_allclose(L2, L1, rtol=1e-13)
+    np.testing.assert_allclose(d2[:7], d1 / 2, rtol=1e-11, atol=1e-18)
+    np.testing.assert_allclose(d2[7:], d1 / 2, rtol=1e-11, atol=1e-18)
+
+
+def test_router_loss_permutation_equivariance(oracle_mod):
+    """Reordering tokens or relabelling experts leaves the losses unchanged
+    and moves the gradient's rows or columns with them."""
+    rng = np.random.default_rng(4)
+    g = rng.normal(0, 2, (6, 9))
+    kw = dict(eps=1e-4, eta=0.5, lam=2.0, gamma=0.3)
+    L, d = oracle_mod.router_loss(g, **kw)
+    r, c = rng.permutation(6), rng.permutation(9)
+    Lp, dp = oracle_mod.router_loss(g[r][:, c], **kw)
+    np.testing.assert_allclose(Lp, L, rtol=1e-13)
+    np.testing.assert_allclose(dp, d[r][:, c], rtol=1e-11, atol=1e-18)
+
+
+def test_router_loss_gradient_rows_sum_to_zero(oracle_mod):
+    """Softmax is unchanged by adding a constant to a row's logits, so the
+    gradient of L_ent + L_bal sums to zero over each row."""
+    rng = np.random.default_rng(6)
+    g = rng.normal(0, 3, (8, 33))
+    _, d = oracle_mod.router_loss(g, eps=1e-3, eta=0.8, lam=1.7, gamma=0.0)
+    assert np.abs(d.sum(axis=1)).max() < 1e-15 * 33 + 1e-17
+    assert np.abs(d).max() > 1e-4
+
+
+@pytest.mark.parametrize("coef", [(1, 0, 0), (0, 1, 0), (0, 0, 1), (0.6, 1.4, 0.9)])
+def test_router_loss_gradient_finite_differences(oracle_mod, coef):
+    """dL/dg against central differences of the oracle's own forward loss,
+    one term at a time and all together, with eps large enough that the
+    eps-dependent part of d[p log(p + eps)]/dp matters."""
+    eta, lam, gam = coef
+    rng = np.random.default_rng(9)
+    B, E, eps = 4, 6, 5e-2
+    g = rng.normal(0, 1.5, (B, E))
+    _, d = oracle_mod.router_loss(g, eps=eps, eta=eta, lam=lam, gamma=gam)
+    h = 1e-5
+    fd = np.empty_like(g)
+    for i in range(B):
+        for j in range(E):
+            gp, gm = g.copy(), g.copy()
+            gp[i, j] += h
+            gm[i, j] -= h
+            Lp, _ = oracle_mod.router_loss(gp, eps=eps, eta=eta, lam=lam, gamma=gam, grad=False)
+            Lm, _ = oracle_mod.router_loss(gm, eps=eps, eta=eta, lam=lam, gamma=gam, grad=False)
+            fd[i, j] = (Lp[3] - Lm[3]) / (2 * h)
+    np.testing.assert_allclose(d, fd, rtol=1e-6, atol=1e-10)
