@@ -42,6 +42,8 @@ def parse_args():
                     help="skip the 32-layer stacked decode measurement")
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the 2048-token prefill measurement")
+    ap.add_argument("--no-loss", action="store_true",
+                    help="skip the router-loss (training regularisers) leg")
     ap.add_argument("--no-rules", action="store_true",
                     help="skip the comparison selection rules (strict, top-k, LTE)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -267,6 +269,8 @@ def main():
         out["prefill"] = bench_prefill(args, torch, np, pp)
     if not args.no_stack:
         out["stack"] = bench_stack(args, torch, np, pp)
+    if not args.no_loss:
+        out["router_loss"] = bench_loss(args, torch, np, pp)
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -467,6 +471,68 @@ def bench_stack(args, torch, np, pp):
             "k_mean_per_layer": [float(v) for v in cnt.mean(axis=1)],
             "union_per_layer": union,
             "k_histogram": {str(k): int(v) for k, v in enumerate(hist) if v}}
+
+
+def bench_loss(args, torch, np, pp):
+    """Routing regularisers forward + backward over a training batch of
+    B = 16384 logit rows, E = 112 (eta 0.5, lambda 0.05, gamma 0.1, eps 1e-8).
+    Calls rotate over 48 logit/gradient buffer pairs (700 MB), more than the
+    Infinity Cache holds, captured once in a HIP graph and replayed.
+    Algorithmic bytes: g read twice, dg written once, 12 B E per call."""
+    from paper_2605_28283_amd.workloads import ROUTER_LOSS_B, ROUTER_LOSS_E, make_router_logits
+    B, E, ncp = ROUTER_LOSS_B, ROUTER_LOSS_E, 48
+    g0 = torch.from_numpy(make_router_logits(B, E, 0)).cuda()
+    gs = [g0 + 0.01 * c for c in range(ncp)]
+    dgs = [torch.empty_like(g0) for _ in range(ncp)]
+    ws = torch.empty(pp.prunepath_router_loss_workspace(B, E) // 4, dtype=torch.float32,
+                     device="cuda")
+    losses = torch.empty(4, dtype=torch.float32, device="cuda")
+    # one HIP graph holds one call per buffer pair, so the timing sees the
+    # kernels and their boundaries, not the Python launch rate
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for c in range(ncp):
+            pp.prunepath_router_loss(gs[c], B, E, 1e-8, 0.5, 0.05, 0.1, losses, dgs[c], ws,
+                                     stream=side)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for c in range(ncp):
+            pp.prunepath_router_loss(gs[c], B, E, 1e-8, 0.5, 0.05, 0.1, losses, dgs[c], ws,
+                                     stream=torch.cuda.current_stream())
+    stream = torch.cuda.current_stream()
+    reps = max(2, args.steps // ncp)
+    for _ in range(max(1, args.warmup // ncp)):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        pp.prunepath_router_loss(gs[i % ncp], B, E, 1e-8, 0.5, 0.05, 0.1, losses, dgs[i % ncp], ws,
+                                 stream=stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    eager = t0.elapsed_time(t1) / args.steps
+    ms = e0.elapsed_time(e1) / (reps * ncp)
+    nbytes = 12.0 * B * E
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    print("# router loss fwd+bwd B=%d E=%d: %.1f us/call in a graph (%.1f us eager), "
+          "%.0f GB/s (%.1f%% of HBM peak)" % (B, E, ms * 1e3, eager * 1e3, gbps,
+                                              100 * gbps / HBM_PEAK_GBPS),
+          file=sys.stderr, flush=True)
+    return {"workload": "router_loss_llama8b_B16384", "B": B, "E": E, "ms_per_call": ms,
+            "us_per_call": ms * 1e3, "rows_per_s": B / (ms * 1e-3),
+            "algorithmic_bytes": nbytes, "effective_GBps": gbps,
+            "frac_hbm_peak": gbps / HBM_PEAK_GBPS, "launches": 3, "graph": True,
+            "us_per_call_eager": eager * 1e3}
 
 
 if __name__ == "__main__":

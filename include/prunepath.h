@@ -31,6 +31,7 @@
 #ifndef PRUNEPATH_H
 #define PRUNEPATH_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -150,6 +151,33 @@ pp_status prunepath_ffn_prefill(pp_layer *L, const uint16_t *x, int32_t T, float
  * 16-byte aligned or u not 8-byte aligned. */
 pp_status prunepath_residual_rmsnorm(const float *x, const float *y, float *x_out, int32_t T,
                                      int32_t d, float eps, uint16_t *u, void *hip_stream);
+
+/* prunepath_router_loss -- the routing regularisers of the training
+ * objective and their gradient, over a batch of B router-logit rows
+ * (Sec. 3.2, Eqs. (entropy_loss), (load_balance_loss), (train_loss); the
+ * gate-magnitude term of Sec. 4.2.3):
+ *   p_ij   = softmax_j(g_i)                                 Eq. (softmax_prob)
+ *   L_ent  = -(1/B) sum_ij p_ij log(p_ij + eps)
+ *   L_bal  = E sum_j m_j^2,  m_j = (1/B) sum_i p_ij
+ *   L_gate = (1/(B E)) sum_ij sigmoid(g_ij)
+ *   losses = [L_ent, L_bal, L_gate, eta L_ent + lambda L_bal + gamma L_gate]
+ *   dg     = d losses[3] / d g                 (skipped when dg is NULL)
+ * The task loss is not included; a term with p_ij = 0 counts as 0.  Does not
+ * need a handle.
+ *   g         : [B, E] fp32 logits, row-major (device, caller-owned)
+ *   losses    : 4 fp32 (device)
+ *   dg        : [B, E] fp32 (device) or NULL; may not alias g
+ *   workspace : prunepath_router_loss_workspace(B, E) bytes of device memory,
+ *               no initial contents required; overwritten
+ * Every sum is taken in an order fixed by (B, E): repeated calls give
+ * identical bits.  Enqueued on hip_stream (NULL: the null stream).
+ * PP_EINVAL: NULL g, losses or workspace; dg == g; B outside [1, 2^22]; E outside
+ * [1, 256]; eps negative, NaN or infinite; eta, lambda or gamma not finite;
+ * g or dg not 16-byte aligned, losses or workspace not 4-byte aligned. */
+size_t prunepath_router_loss_workspace(int32_t B, int32_t E); /* 0 for bad sizes */
+pp_status prunepath_router_loss(const float *g, int32_t B, int32_t E, float eps, float eta,
+                                float lambda, float gamma, float *losses, float *dg,
+                                void *workspace, void *hip_stream);
 
 /* Kernel kinds reported by prunepath_profile_end. */
 #define PP_KERNEL_ROUTE 0     /* router: logits, softmax, sort, cut */

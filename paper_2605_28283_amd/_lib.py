@@ -34,7 +34,8 @@ PP_KERNEL_COUNT = 4
 
 EXPORTED = ("prunepath_create", "prunepath_route", "prunepath_ffn_decode",
             "prunepath_ffn_prefill", "prunepath_destroy", "prunepath_status_string",
-            "prunepath_profile_begin", "prunepath_profile_end", "prunepath_residual_rmsnorm")
+            "prunepath_profile_begin", "prunepath_profile_end", "prunepath_residual_rmsnorm",
+            "prunepath_router_loss_workspace", "prunepath_router_loss")
 
 
 class PrunePathError(RuntimeError):
@@ -72,6 +73,10 @@ def load():
         lib.prunepath_profile_end.restype = ctypes.c_int
         lib.prunepath_residual_rmsnorm.argtypes = [P, P, P, I32, I32, F32, P, P]
         lib.prunepath_residual_rmsnorm.restype = ctypes.c_int
+        lib.prunepath_router_loss_workspace.argtypes = [I32, I32]
+        lib.prunepath_router_loss_workspace.restype = ctypes.c_size_t
+        lib.prunepath_router_loss.argtypes = [P, I32, I32, F32, F32, F32, F32, P, P, P, P]
+        lib.prunepath_router_loss.restype = ctypes.c_int
         lib.prunepath_status_string.argtypes = [ctypes.c_int]
         lib.prunepath_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -165,6 +170,19 @@ def prunepath_residual_rmsnorm(x, y, x_out, T, d, eps, u=None, stream=None):
     st = load().prunepath_residual_rmsnorm(_ptr(x, "f32"), _ptr(y, "f32"), _ptr(x_out, "f32"),
                                            T, d, eps, _ptr(u, "bf16"), _stream(stream))
     _check(st, "prunepath_residual_rmsnorm")
+
+
+def prunepath_router_loss_workspace(B, E):
+    """Workspace bytes prunepath_router_loss needs (0 for bad sizes)."""
+    return int(load().prunepath_router_loss_workspace(B, E))
+
+
+def prunepath_router_loss(g, B, E, eps, eta, lam, gamma, losses, dg, workspace, stream=None):
+    """losses[4] = [L_ent, L_bal, L_gate, total] and dg = dL/dg (None: skipped)."""
+    st = load().prunepath_router_loss(_ptr(g, "f32"), B, E, eps, eta, lam, gamma,
+                                      _ptr(losses, "f32"), _ptr(dg, "f32"), _ptr(workspace),
+                                      _stream(stream))
+    _check(st, "prunepath_router_loss")
 
 
 def prunepath_profile_begin(handle, capacity):

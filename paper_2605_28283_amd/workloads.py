@@ -18,6 +18,12 @@ these synthetic layers stand in for them):
     per-token temperature ~ U(0.5, 2) passed as its inverse;
   * the skewed workload adds a per-expert router bias ~ Gumbel(0, 1.5);
   * every value is drawn in fp32 and rounded to bf16 with round-to-nearest-even;
+  * router-loss batches: logits [B, E] fp32 ~ N(0, 3^2) (the synthetic
+    routers' logit scale), each row scaled by LogNormal(0, 0.5) so that sharp
+    and flat routing distributions mix, plus a per-expert Gumbel(0, 1) offset
+    so that the batch-mean probabilities are uneven (a non-trivial L_bal);
+    the training-step workload is B = 16384 rows (8 sequences of 2048 tokens)
+    over the LLaMA-3-8B split, E = 112;
   * the 32-layer stack (11.3 GB of weights) draws its layers on the GPU with
     torch's Philox generator, seeded 0x5EED0000 + 64 * seed + layer, in the
     same order and distributions (host PCG64 would take minutes per layer);
@@ -90,6 +96,21 @@ def make_tokens(T: int, d: int, seed, *, row_lognormal_sigma: float = 0.0,
     if temperature:
         inv_temp = (1.0 / rng.uniform(0.5, 2.0, size=T)).astype(np.float32)
     return bf16_bits(x), inv_temp
+
+
+ROUTER_LOSS_B, ROUTER_LOSS_E = 16384, 112
+
+
+def make_router_logits(B: int, E: int, seed, *, std: float = 3.0,
+                       row_lognormal_sigma: float = 0.5, expert_gumbel: float = 1.0) -> np.ndarray:
+    """Router logits [B, E] fp32 for the routing-regulariser kernels."""
+    rng = np.random.default_rng(seed)
+    g = rng.standard_normal((B, E), dtype=np.float32) * np.float32(std)
+    if row_lognormal_sigma > 0.0:
+        g *= rng.lognormal(0.0, row_lognormal_sigma, size=(B, 1)).astype(np.float32)
+    if expert_gumbel > 0.0:
+        g += rng.gumbel(0.0, expert_gumbel, size=(1, E)).astype(np.float32)
+    return np.ascontiguousarray(g, dtype=np.float32)
 
 
 # --------------------------------------------------------------------------

@@ -110,3 +110,42 @@ def test_residual_rmsnorm_rejects_bad_arguments(args):
     lib = pp.load()
     x, y, xo, T, d, eps, u = args
     assert lib.prunepath_residual_rmsnorm(x, y, xo, T, d, eps, u, None) == pp.PP_EINVAL
+
+
+def test_router_loss_workspace_size():
+    lib = pp.load()
+    for B, E in [(1, 1), (16, 112), (17, 112), (16384, 256), (1 << 22, 256)]:
+        nb = -(-B // 64)
+        assert lib.prunepath_router_loss_workspace(B, E) == 4 * (nb * (E + 2) + E)
+    for B, E in [(0, 8), (8, 0), (8, 257), ((1 << 22) + 1, 8), (-1, 8)]:
+        assert lib.prunepath_router_loss_workspace(B, E) == 0
+
+
+INF, NAN = float("inf"), float("nan")
+
+
+@pytest.mark.parametrize("args", [
+    (None, 8, 16, 1e-8, 1.0, 1.0, 0.0, 16, 32, 64),     # g NULL
+    (16, 8, 16, 1e-8, 1.0, 1.0, 0.0, None, 32, 64),     # losses NULL
+    (16, 8, 16, 1e-8, 1.0, 1.0, 0.0, 16, 32, None),     # workspace NULL
+    (16, 8, 16, 1e-8, 1.0, 1.0, 0.0, 48, 16, 64),       # dg aliases g
+    (16, 0, 16, 1e-8, 1.0, 1.0, 0.0, 48, 32, 64),       # B < 1
+    (16, (1 << 22) + 1, 16, 1e-8, 1.0, 1.0, 0.0, 48, 32, 64),  # B too large
+    (16, 8, 0, 1e-8, 1.0, 1.0, 0.0, 48, 32, 64),        # E < 1
+    (16, 8, 257, 1e-8, 1.0, 1.0, 0.0, 48, 32, 64),      # E > 256
+    (16, 8, 16, -1e-8, 1.0, 1.0, 0.0, 48, 32, 64),      # eps < 0
+    (16, 8, 16, NAN, 1.0, 1.0, 0.0, 48, 32, 64),        # eps NaN
+    (16, 8, 16, INF, 1.0, 1.0, 0.0, 48, 32, 64),        # eps infinite
+    (16, 8, 16, 1e-8, NAN, 1.0, 0.0, 48, 32, 64),       # eta NaN
+    (16, 8, 16, 1e-8, 1.0, INF, 0.0, 48, 32, 64),       # lambda infinite
+    (16, 8, 16, 1e-8, 1.0, 1.0, -INF, 48, 32, 64),      # gamma infinite
+    (18, 8, 16, 1e-8, 1.0, 1.0, 0.0, 48, 32, 64),       # g misaligned
+    (16, 8, 16, 1e-8, 1.0, 1.0, 0.0, 48, 32, 66),       # workspace misaligned
+    (16, 8, 16, 1e-8, 1.0, 1.0, 0.0, 48, 40, 64),       # dg not 16-byte aligned
+    (24, 8, 16, 1e-8, 1.0, 1.0, 0.0, 48, 32, 64),       # g not 16-byte aligned
+])
+def test_router_loss_rejects_bad_arguments(args):
+    lib = pp.load()
+    g, B, E, eps, eta, lam, gam, losses, dg, ws = args
+    assert lib.prunepath_router_loss(g, B, E, eps, eta, lam, gam, losses, dg, ws,
+                                     None) == pp.PP_EINVAL
