@@ -59,7 +59,7 @@ typedef enum {
  * then carrying their parameter:
  *  PP_SELECT_TOPK: the k experts ranked first by the router, pi_1..pi_k, with
  *    k = tau rounded to the nearest integer and clamped to [1, E] (the forced
- *    top-k budget of the paper's reconstruction analysis, Sec. 5 "Top-k
+ *    top-k budget of the paper's reconstruction analysis, Sec. 4.3.2 "Top-k
  *    Reconstruction Analysis").
  *  PP_SELECT_LTE: the independent threshold of Eq. (lte_hard_set),
  *    {e : sigmoid(g_e) > delta} with delta = tau; a token may keep no expert

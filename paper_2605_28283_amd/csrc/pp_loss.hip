@@ -11,15 +11,16 @@
 // s = sigmoid(g).  A term with p_ij = 0 (eps = 0 and an underflowed
 // probability) is taken at its limit, 0.
 //
-// HBM-bound: 12 B E bytes (g read twice, dg written once).  Three launches,
+// HBM-bound: 12 B E bytes (g read twice, dg written once).  Two launches,
 // each sum in an order fixed by (B, E), so results are deterministic:
-//   loss_rows_k   64 rows per workgroup, staged in LDS by flat 16-byte loads;
-//                 each row on the 16 lanes of one DPP row (4 rows per
-//                 wavefront, no idle lanes when 16 divides E); per-workgroup
-//                 column sums of p and entropy and sigmoid sums
-//   loss_reduce_k one workgroup: workgroup partials in fp64 -> m and losses
-//   loss_grad_k   16 rows per workgroup, staged the same way; dg is built in
-//                 LDS and stored by flat 16-byte writes
+//   loss_rows_k   each row on the 16 lanes of one DPP row (4 rows per
+//                 wavefront, no idle lanes when 16 divides E), 64 rows per
+//                 workgroup; per-workgroup column sums of p and entropy and
+//                 sigmoid sums
+//   loss_grad_k   every workgroup reduces those partials in fp64 to m (the
+//                 gradient of L_bal needs the batch mean), workgroup 0 writes
+//                 the losses; then dg for 64 rows in the same row layout,
+//                 written straight from registers
 // exp, log and reciprocal use the hardware instructions (1 ulp); kernels are
 // instantiated for each ceil(E / 16).
 #include <array>
@@ -30,12 +31,10 @@
 namespace pp {
 namespace {
 
-constexpr int kRowsWaves = 16;  // loss_rows_k: 64 rows per workgroup
-constexpr int kGradWaves = 4;   // loss_grad_k: 16 rows per workgroup
+constexpr int kLossWaves = 16;       // wavefronts per workgroup, both kernels
 constexpr int kLossRowsPerWave = 4;  // one row per 16-lane DPP row
-constexpr int kRedThreads = 1024;
-constexpr int kRedWaves = kRedThreads / 64;
-constexpr int kRedBatch = 8;  // partial loads in flight per lane
+constexpr int kRowsPerBlock = kLossWaves * kLossRowsPerWave;  // 64
+constexpr int kRedLoads = 32;  // partial loads in flight per lane in the reduction
 constexpr int kMaxLossRows = 1 << 22;
 constexpr float kLog2e = 1.44269504088896341f;
 constexpr float kLn2 = 0.693147180559945309f;
@@ -71,72 +70,26 @@ __device__ __forceinline__ float row16_max(float v) {
     return v;
 }
 
-// A workgroup of W wavefronts owns rows r0 .. r0 + 4W - 1 (r0 = 4W blockIdx.x),
-// a contiguous range of 4W E floats.  It is copied into LDS with flat,
-// coalesced 16-byte loads (all issued before the first LDS store), so the
-// row length never decides the access pattern.  Wavefront w then takes the
-// block's rows w, w + W, w + 2W, w + 3W.
-template <int W>
-struct Tile {
-    static constexpr int kRows = kLossRowsPerWave * W;
-    static constexpr int kThreads = 64 * W;
-    static constexpr int kVec = kRows * kMaxExperts / 4 / kThreads;  // float4 per thread
-    int r0, nr;
-
-    // copy the block's rows of G into t; returns after a barrier
-    __device__ void stage(const float *__restrict__ G, int B, int E, float *t) {
-        r0 = blockIdx.x * kRows;
-        nr = min(kRows, B - r0);
-        const int n = nr * E, n4 = n >> 2;
-        const float *src = G + (size_t)r0 * E;  // 16-byte aligned: r0 E is a multiple of 4
-        const float4 *s4 = reinterpret_cast<const float4 *>(src);
-        float4 *t4 = reinterpret_cast<float4 *>(t);
-        if (n4 > 0) {  // workgroup-uniform
-            // unconditional loads of clamped (in-range) addresses, so that all
-            // of them are in flight before the first wait
-            // (threads past the end copy the last vector again: same value,
-            // same place), so no branch splits the loads from each other
-            float4 v[kVec];
-#pragma unroll
-            for (int u = 0; u < kVec; ++u) v[u] = s4[min((int)threadIdx.x + kThreads * u, n4 - 1)];
-#pragma unroll
-            for (int u = 0; u < kVec; ++u) t4[min((int)threadIdx.x + kThreads * u, n4 - 1)] = v[u];
-        }
-        for (int i = 4 * n4 + threadIdx.x; i < n; i += kThreads) t[i] = src[i];
-        __syncthreads();
-    }
-    // write the staged rows of t to D (after a barrier)
-    __device__ void flush(const float *t, int E, float *__restrict__ D) const {
-        __syncthreads();
-        const int n = nr * E, n4 = n >> 2;
-        float *dst = D + (size_t)r0 * E;
-        if (n4 > 0) {
-            const float4 *t4 = reinterpret_cast<const float4 *>(t);
-            float4 *d4 = reinterpret_cast<float4 *>(dst);
-            float4 v[kVec];
-#pragma unroll
-            for (int u = 0; u < kVec; ++u) v[u] = t4[min((int)threadIdx.x + kThreads * u, n4 - 1)];
-#pragma unroll
-            for (int u = 0; u < kVec; ++u) d4[min((int)threadIdx.x + kThreads * u, n4 - 1)] = v[u];
-        }
-        for (int i = 4 * n4 + threadIdx.x; i < n; i += kThreads) dst[i] = t[i];
-    }
-};
-
-// One row of the tile on the 16 lanes of a DPP row: lane c holds columns
-// c + 16 q, q < NQ = ceil(E / 16), and the row's softmax.  A row past the
-// batch end (live false) reads row nr - 1 and must be ignored by the caller.
+// Row r on the 16 lanes of one DPP row: lane c holds columns c + 16 q,
+// q < NQ = ceil(E / 16), and the row's softmax.  Rows are read straight from
+// HBM, 4 consecutive rows per wavefront (one 16-lane segment of 64 bytes per
+// row and instruction), every load unconditional (clamped address) so all of
+// them are in flight before the first wait.  A row past the batch end reads
+// row B - 1 and must be ignored by the caller.
 template <int NQ>
 struct Row {
     float g[NQ], p[NQ];
-    __device__ void load(const float *t, int lr, int nr, int E, int c) {
-        const int rr = min(lr, nr - 1);
+    // issue the row's loads (no wait)
+    __device__ void fetch(const float *__restrict__ G, int r, int B, int E, int c) {
+        const float *row = G + (size_t)min(r, B - 1) * E;
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) g[q] = row[min(c + 16 * q, E - 1)];
+    }
+    __device__ void softmax(int E, int c) {
         float mx = -INFINITY;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-            const int j = c + 16 * q;
-            const float v = t[rr * E + min(j, E - 1)];
-            g[q] = j < E ? v : -INFINITY;
+            g[q] = c + 16 * q < E ? g[q] : -INFINITY;
             mx = fmaxf(mx, g[q]);
         }
         mx = row16_max(mx);
@@ -152,106 +105,109 @@ struct Row {
     }
 };
 
-// part: [nb][E + 2] = column sums of p over the block's 64 rows, then the
-// block's sums of p log(p + eps) and of sigmoid(g); every sum runs over the
-// rows in ascending order (in four quarters of 16 rows, then the quarters in
-// order).
+// Sum over the four 16-lane rows of a wavefront, (r0 + r1) + (r2 + r3) in
+// every lane.
+__device__ __forceinline__ float wave_rows_sum(float v, int lane) {
+    v += __uint_as_float(xor_lane<16>(__float_as_uint(v), lane));
+    v += __uint_as_float(xor_lane<32>(__float_as_uint(v), lane));
+    return v;
+}
+
+// part: [nb][E + 2] = column sums of p over each workgroup's 64 rows, then
+// its sums of p log(p + eps) and of sigmoid(g).  Fixed order: within a
+// wavefront (r0 + r1) + (r2 + r3), then the 16 wavefronts in order.
 template <int NQ>
-__global__ __launch_bounds__(64 * kRowsWaves) void loss_rows_k(const float *__restrict__ G, int B,
+__global__ __launch_bounds__(64 * kLossWaves) void loss_rows_k(const float *__restrict__ G, int B,
                                                                int E, float eps,
                                                                float *__restrict__ part) {
-    using T = Tile<kRowsWaves>;
-    __shared__ __align__(16) float tile[T::kRows * kMaxExperts];
-    __shared__ float rows_es[2][T::kRows];
-    __shared__ float quart[4][kMaxExperts + 2];
-    const int lane = threadIdx.x & 63, c = lane & 15;
-    const int lr = (threadIdx.x >> 6) * kLossRowsPerWave + (lane >> 4);
-    T tl;
-    tl.stage(G, B, E, tile);
+    __shared__ float ws[kLossWaves][kMaxExperts + 2];
+    const int lane = threadIdx.x & 63, c = lane & 15, wv = threadIdx.x >> 6;
+    const int r = blockIdx.x * kRowsPerBlock + wv * kLossRowsPerWave + (lane >> 4);
+    const bool live = r < B;
     Row<NQ> R;
-    R.load(tile, lr, tl.nr, E, c);
+    R.fetch(G, r, B, E, c);
+    R.softmax(E, c);
     float e = 0.0f, sg = 0.0f;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-        if (c + 16 * q < E) {
-            if (R.p[q] >= kFltMin) e += R.p[q] * flog(R.p[q] + eps);
-            sg += fsig(R.g[q]);
+        const float pv = live ? R.p[q] : 0.0f;
+        if (pv >= kFltMin) e += pv * flog(pv + eps);
+        if (live && c + 16 * q < E) sg += fsig(R.g[q]);
+        R.p[q] = wave_rows_sum(pv, lane);
+    }
+    e = wave_rows_sum(row16_sum(e), lane);
+    sg = wave_rows_sum(row16_sum(sg), lane);
+    if (lane < 16) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+            if (c + 16 * q < E) ws[wv][c + 16 * q] = R.p[q];
+        if (c == 0) {
+            ws[wv][E] = e;
+            ws[wv][E + 1] = sg;
         }
     }
-    e = row16_sum(e);
-    sg = row16_sum(sg);
-    // a row's 16 lanes overwrite only their own row, which they have read
-    const bool live = lr < tl.nr;
+    __syncthreads();
+    float *out = part + (size_t)blockIdx.x * (E + 2);
+    for (int j = threadIdx.x; j < E + 2; j += 64 * kLossWaves) {
+        float v = ws[0][j];
 #pragma unroll
-    for (int q = 0; q < NQ; ++q)
-        if (live && c + 16 * q < E) tile[lr * E + c + 16 * q] = R.p[q];
-    if (c == 0) {
-        rows_es[0][lr] = live ? e : 0.0f;
-        rows_es[1][lr] = live ? sg : 0.0f;
+        for (int w = 1; w < kLossWaves; ++w) v += ws[w][j];
+        out[j] = v;
     }
-    __syncthreads();
-    const int C = E + 2;
-    for (int i = threadIdx.x; i < 4 * C; i += T::kThreads) {
-        const int k = i / C, j = i - k * C;  // quarter k of the rows, column j
-        const int r_end = min(tl.nr, 16 * k + 16);
-        float v = 0.0f;
-        for (int r = 16 * k; r < r_end; ++r)
-            v += j < E ? tile[r * E + j] : rows_es[j - E][r];
-        quart[k][j] = v;
-    }
-    __syncthreads();
-    float *out = part + (size_t)blockIdx.x * C;
-    for (int j = threadIdx.x; j < C; j += T::kThreads)
-        out[j] = ((quart[0][j] + quart[1][j]) + quart[2][j]) + quart[3][j];
 }
 
-// One workgroup.  mout [E] = batch-mean probabilities; losses = [L_ent,
-// L_bal, L_gate, L].  Wavefront w sums blocks w, w + 16, ... of each column
-// in fp64; the 16 wavefront sums are then added in wavefront order, and
-// sum_j m_j^2 is taken by wavefront 0 in a fixed butterfly.
-__global__ __launch_bounds__(kRedThreads) void loss_reduce_k(const float *__restrict__ part, int nb,
-                                                             int B, int E, float eta,
-                                                             float lambda, float gamma,
-                                                             float *__restrict__ mout,
-                                                             float *__restrict__ losses) {
-    __shared__ double red[kRedWaves][kMaxExperts + 2];
+// The reduction of all nb partial rows, run by every workgroup of
+// loss_grad_k (it needs m) -- 117 KB for the 16384 x 112 batch, read from L2
+// after the first workgroup of an XCD has fetched it.  Wavefront w sums
+// partial rows w, w + 16, ... of each column in fp64 (NC = ceil((E + 2) / 64)
+// columns per lane, 32 / NC partial rows per round, all loads of a round in
+// flight at once); the 16 wavefront sums are added in wavefront order.
+// mf [E] receives m_j (fp32); workgroup 0 also writes losses = [L_ent,
+// L_bal, L_gate, L] (sum_j m_j^2 by a fixed butterfly in wavefront 0).
+// Every workgroup takes the same steps in the same order, so all hold the
+// same m.
+template <int NC>
+__device__ void reduce_partials(const float *__restrict__ part, int nb, int B, int E, float eta,
+                                float lambda, float gamma, float *mf,
+                                float *__restrict__ losses) {
+    __shared__ double red[kLossWaves][kMaxExperts + 2];
     __shared__ double col[kMaxExperts + 2];
     __shared__ double sq[kMaxExperts];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int C = E + 2;
-    for (int c0 = 0; c0 < C; c0 += 64) {
-        const int j = c0 + lane;
-        if (j < C) {
-            double acc = 0.0;
-            for (int b0 = wv; b0 < nb; b0 += kRedWaves * kRedBatch) {
-                float v[kRedBatch];
+    constexpr int RB = kRedLoads / NC;  // partial rows per round
+    double acc[NC] = {};
+    for (int b0 = wv; b0 < nb; b0 += kLossWaves * RB) {
+        float v[RB][NC];
 #pragma unroll
-                for (int u = 0; u < kRedBatch; ++u) {
-                    const int b = b0 + kRedWaves * u;
-                    const float x = part[(size_t)min(b, nb - 1) * C + j];
-                    v[u] = b < nb ? x : 0.0f;
-                }
+        for (int u = 0; u < RB; ++u)
 #pragma unroll
-                for (int u = 0; u < kRedBatch; ++u) acc += (double)v[u];
-            }
-            red[wv][j] = acc;
-        }
+            for (int k = 0; k < NC; ++k)
+                v[u][k] = part[(size_t)min(b0 + kLossWaves * u, nb - 1) * C + min(lane + 64 * k, C - 1)];
+#pragma unroll
+        for (int u = 0; u < RB; ++u)
+#pragma unroll
+            for (int k = 0; k < NC; ++k)
+                acc[k] += b0 + kLossWaves * u < nb ? (double)v[u][k] : 0.0;
     }
+#pragma unroll
+    for (int k = 0; k < NC; ++k)
+        if (lane + 64 * k < C) red[wv][lane + 64 * k] = acc[k];
     __syncthreads();
     const double invB = 1.0 / (double)B;
-    for (int j = threadIdx.x; j < C; j += kRedThreads) {
+    for (int j = threadIdx.x; j < C; j += 64 * kLossWaves) {
         double v = red[0][j];
 #pragma unroll
-        for (int w = 1; w < kRedWaves; ++w) v += red[w][j];
+        for (int w = 1; w < kLossWaves; ++w) v += red[w][j];
         col[j] = v;
         if (j < E) {
             const double m = v * invB;
-            mout[j] = (float)m;
+            mf[j] = (float)m;
             sq[j] = m * m;
         }
     }
     __syncthreads();
-    if (wv == 0) {
+    if (blockIdx.x == 0 && wv == 0) {
         double s = 0.0;
 #pragma unroll
         for (int q = 0; q < kMaxExperts / 64; ++q)
@@ -271,29 +227,27 @@ __global__ __launch_bounds__(kRedThreads) void loss_reduce_k(const float *__rest
     }
 }
 
-// dg for the block's 16 rows (4 wavefronts x 4 rows): computed into the LDS
-// tile in place of g, then stored with flat 16-byte writes.
-template <int NQ>
-__global__ __launch_bounds__(64 * kGradWaves) void loss_grad_k(const float *__restrict__ G, int B,
+// dg, 64 rows per workgroup (4 per wavefront), straight from registers to
+// HBM.  The rows' loads are issued before the partials are reduced, so their
+// HBM latency overlaps the reduction.  With dg NULL the kernel runs as one
+// workgroup that only writes the losses.
+template <int NQ, int NC>
+__global__ __launch_bounds__(64 * kLossWaves) void loss_grad_k(const float *__restrict__ G, int B,
                                                                int E, float eps, float eta,
                                                                float lambda, float gamma,
-                                                               const float *__restrict__ m,
+                                                               const float *__restrict__ part,
+                                                               int nb, float *__restrict__ losses,
                                                                float *__restrict__ dg) {
-    using T = Tile<kGradWaves>;
-    __shared__ __align__(16) float tile[T::kRows * kMaxExperts];
+    __shared__ float mf[kMaxExperts];
     const int lane = threadIdx.x & 63, c = lane & 15;
-    const int lr = (threadIdx.x >> 6) * kLossRowsPerWave + (lane >> 4);
+    const int r = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6) * kLossRowsPerWave + (lane >> 4);
+    Row<NQ> R;
+    if (dg) R.fetch(G, r, B, E, c);
+    reduce_partials<NC>(part, nb, B, E, eta, lambda, gamma, mf, losses);
+    if (!dg) return;
     const float ce = -eta / (float)B, cg = gamma / ((float)B * (float)E);
     const float cb = 2.0f * lambda * (float)E / (float)B;
-    float bal[NQ];  // 2 lambda E m_j / B
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) bal[q] = m[min(c + 16 * q, E - 1)];
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) bal[q] = c + 16 * q < E ? cb * bal[q] : 0.0f;
-    T tl;
-    tl.stage(G, B, E, tile);
-    Row<NQ> R;
-    R.load(tile, lr, tl.nr, E, c);
+    R.softmax(E, c);
     float a[NQ], pa = 0.0f;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
@@ -303,40 +257,48 @@ __global__ __launch_bounds__(64 * kGradWaves) void loss_grad_k(const float *__re
             const float pe = pv + eps;
             ent = ce * (flog(pe) + pv * frcp(pe));
         }
-        a[q] = ent + bal[q];
+        a[q] = ent + (c + 16 * q < E ? cb * mf[min(c + 16 * q, E - 1)] : 0.0f);
         pa += pv * a[q];
     }
     pa = row16_sum(pa);
-    if (lr < tl.nr) {  // a row's 16 lanes overwrite only their own row
+    if (r < B) {
+        float *out = dg + (size_t)r * E;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int j = c + 16 * q;
             if (j < E) {
                 const float sv = fsig(R.g[q]);
-                tile[lr * E + j] = R.p[q] * (a[q] - pa) + cg * sv * (1.0f - sv);
+                out[j] = R.p[q] * (a[q] - pa) + cg * sv * (1.0f - sv);
             }
         }
     }
-    tl.flush(tile, E, dg);
 }
 
-inline int rows_blocks(int B) { return (B + Tile<kRowsWaves>::kRows - 1) / Tile<kRowsWaves>::kRows; }
-inline int grad_blocks(int B) { return (B + Tile<kGradWaves>::kRows - 1) / Tile<kGradWaves>::kRows; }
+inline int rows_blocks(int B) { return (B + kRowsPerBlock - 1) / kRowsPerBlock; }
 
+template <int NQ, int NC>
+void launch_loss_nc(const float *g, int B, int E, float eps, float eta, float lambda, float gamma,
+                    float *losses, float *dg, float *part, hipStream_t s) {
+    const int nb = rows_blocks(B);
+    hipLaunchKernelGGL(loss_rows_k<NQ>, dim3(nb), dim3(64 * kLossWaves), 0, s, g, B, E, eps, part);
+    hipLaunchKernelGGL((loss_grad_k<NQ, NC>), dim3(dg ? nb : 1), dim3(64 * kLossWaves), 0, s, g, B,
+                       E, eps, eta, lambda, gamma, part, nb, losses, dg);
+}
+
+// NC = ceil((E + 2) / 64) follows from NQ = ceil(E / 16) except at the
+// boundaries E = 63, 127, 191, 255 (E + 2 crosses a multiple of 64).
 template <int NQ>
 void launch_loss(const float *g, int B, int E, float eps, float eta, float lambda, float gamma,
-                 float *losses, float *dg, float *part, float *m, hipStream_t s) {
-    const int nb = rows_blocks(B);
-    hipLaunchKernelGGL(loss_rows_k<NQ>, dim3(nb), dim3(64 * kRowsWaves), 0, s, g, B, E, eps, part);
-    hipLaunchKernelGGL(loss_reduce_k, dim3(1), dim3(kRedThreads), 0, s, part, nb, B, E, eta,
-                       lambda, gamma, m, losses);
-    if (dg)
-        hipLaunchKernelGGL(loss_grad_k<NQ>, dim3(grad_blocks(B)), dim3(64 * kGradWaves), 0, s, g, B,
-                           E, eps, eta, lambda, gamma, m, dg);
+                 float *losses, float *dg, float *part, hipStream_t s) {
+    constexpr int lo = (16 * (NQ - 1) + 1 + 2 + 63) / 64, hi = (16 * NQ + 2 + 63) / 64;
+    if ((E + 2 + 63) / 64 == lo)
+        launch_loss_nc<NQ, lo>(g, B, E, eps, eta, lambda, gamma, losses, dg, part, s);
+    else
+        launch_loss_nc<NQ, hi>(g, B, E, eps, eta, lambda, gamma, losses, dg, part, s);
 }
 
 using LossLauncher = void (*)(const float *, int, int, float, float, float, float, float *,
-                              float *, float *, float *, hipStream_t);
+                              float *, float *, hipStream_t);
 template <int... Q>
 constexpr auto make_launchers(std::integer_sequence<int, Q...>) {
     return std::array<LossLauncher, sizeof...(Q)>{launch_loss<Q + 1>...};
@@ -348,7 +310,7 @@ constexpr auto kLaunchers = make_launchers(std::make_integer_sequence<int, kMaxE
 
 extern "C" size_t prunepath_router_loss_workspace(int32_t B, int32_t E) {
     if (B < 1 || B > pp::kMaxLossRows || E < 1 || E > pp::kMaxExperts) return 0;
-    return sizeof(float) * ((size_t)pp::rows_blocks(B) * ((size_t)E + 2) + (size_t)E);
+    return sizeof(float) * (size_t)pp::rows_blocks(B) * ((size_t)E + 2);
 }
 
 extern "C" pp_status prunepath_router_loss(const float *g, int32_t B, int32_t E, float eps,
@@ -363,9 +325,7 @@ extern "C" pp_status prunepath_router_loss(const float *g, int32_t B, int32_t E,
         ((reinterpret_cast<uintptr_t>(losses) | reinterpret_cast<uintptr_t>(workspace)) & 3))
         return PP_EINVAL;
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
-    const int nb = pp::rows_blocks(B);
-    float *part = static_cast<float *>(workspace);
-    float *m = part + (size_t)nb * ((size_t)E + 2);
-    pp::kLaunchers[(E + 15) / 16 - 1](g, B, E, eps, eta, lambda, gamma, losses, dg, part, m, s);
+    pp::kLaunchers[(E + 15) / 16 - 1](g, B, E, eps, eta, lambda, gamma, losses, dg,
+                                      static_cast<float *>(workspace), s);
     return hipGetLastError() == hipSuccess ? PP_OK : PP_EHIP;
 }

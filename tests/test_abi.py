@@ -116,7 +116,7 @@ def test_router_loss_workspace_size():
     lib = pp.load()
     for B, E in [(1, 1), (16, 112), (17, 112), (16384, 256), (1 << 22, 256)]:
         nb = -(-B // 64)
-        assert lib.prunepath_router_loss_workspace(B, E) == 4 * (nb * (E + 2) + E)
+        assert lib.prunepath_router_loss_workspace(B, E) == 4 * nb * (E + 2)
     for B, E in [(0, 8), (8, 0), (8, 257), ((1 << 22) + 1, 8), (-1, 8)]:
         assert lib.prunepath_router_loss_workspace(B, E) == 0
 
