@@ -54,6 +54,10 @@ def _load():
         lib.ppo_bf16_round_n.restype = None
         lib.ppo_rmsnorm.argtypes = [I64, I64, P, ctypes.c_double, P, P]
         lib.ppo_rmsnorm.restype = ctypes.c_int
+        lib.ppo_mlp.argtypes = [I64, I64, I64, I64, P, P, P, P, P, P, P, P, P, ctypes.c_uint, P]
+        lib.ppo_mlp.restype = ctypes.c_int
+        lib.ppo_gelu_n.argtypes = [I64, P, P]
+        lib.ppo_gelu_n.restype = None
         lib.ppo_router_loss.argtypes = [I64, I64, P, ctypes.c_double, ctypes.c_double,
                                         ctypes.c_double, ctypes.c_double, P, P]
         lib.ppo_router_loss.restype = ctypes.c_int
@@ -134,6 +138,33 @@ def ffn(x, W_gate, W_up, W_down, idx, count, flags=0, g=None, perm=None):
                          _ptr(_c(count, np.int32)), _ptr(_c(g, np.float64)), int(flags), _ptr(y))
     if rc != 0:
         raise ValueError("oracle ffn: bad arguments")
+    return y
+
+
+def gelu(a):
+    """GPT-2's tanh-form GELU, elementwise, fp64."""
+    a = _c(a, np.float64)
+    out = np.empty_like(a)
+    _load().ppo_gelu_n(a.size, _ptr(a), _ptr(out))
+    return out
+
+
+def mlp(x, W_fc, b_fc, W_proj, b_proj, idx, count, flags=0, g=None, perm=None):
+    """Non-gated GELU MLP variant: y [T,d] fp64 for a given selection; b_fc
+    [d_ff] / b_proj [d] fp32 or None."""
+    x = _c(x, np.uint16)
+    T, d = x.shape
+    d_ff = W_fc.shape[0]
+    E = idx.shape[1]
+    assert W_fc.shape == (d_ff, d) and W_proj.shape == (d, d_ff)
+    y = np.empty((T, d), np.float64)
+    rc = _load().ppo_mlp(T, d, d_ff, E, _ptr(x), _ptr(_c(W_fc, np.uint16)),
+                         _ptr(_c(b_fc, np.float32)), _ptr(_c(W_proj, np.uint16)),
+                         _ptr(_c(b_proj, np.float32)), _ptr(_c(perm, np.int32)),
+                         _ptr(_c(idx, np.int32)), _ptr(_c(count, np.int32)),
+                         _ptr(_c(g, np.float64)), int(flags), _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle mlp: bad arguments")
     return y
 
 

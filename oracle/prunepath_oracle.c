@@ -17,6 +17,8 @@
  *   A_tau(x) from C and tau             Eq. (tau_thresh_activate), nucleus reading
  *   y = sum_{e in A} [sigmoid(g_e)] FFN_e(x)   Eqs. (moefication_decomp), (moe_output)
  *   FFN_e(x) = (phi(x Wg^(e)) . x Wu^(e)) Wd^(e), phi = SiLU   Eq. (ffn)
+ *   non-gated variant (GPT-2 MLP): GELU(x W_fc^(e) + b_fc^(e)) W_proj^(e),
+ *   plus b_proj once per token                                  Sec. 2.1
  *
  * Readings of points the paper leaves open (each is listed in the design notes):
  *  - Selection rule.  Default (nucleus): the smallest prefix of pi whose mass
@@ -234,6 +236,76 @@ int ppo_ffn(int64_t T, int64_t d, int64_t d_ff, int64_t E, const uint16_t *x,
             const uint16_t *wd = Wd + i * d_ff;
             double acc = 0.0;
             for (int64_t q = 0; q < k * de; ++q) acc += bf16_value(wd[nsel[q]]) * h[q];
+            yt[i] = acc;
+        }
+        free(nsel);
+        free(h);
+        free(xv);
+    }
+    return bad ? -1 : 0;
+}
+
+/* GELU as used by GPT-2, the paper's GPT-2 Medium target (Sec. 4.2.2,
+ * Sec. 4.5): the tanh form 0.5 a (1 + tanh(sqrt(2/pi) (a + 0.044715 a^3))). */
+double ppo_gelu(double a) {
+    const double c = sqrt(2.0 / 3.14159265358979323846);
+    return 0.5 * a * (1.0 + tanh(c * (a + 0.044715 * a * a * a)));
+}
+
+void ppo_gelu_n(int64_t n, const double *a, double *out) {
+    for (int64_t i = 0; i < n; ++i) out[i] = ppo_gelu(a[i]);
+}
+
+/* Non-gated MLP variant (Sec. 2.1: the decomposition holds for any FFN whose
+ * intermediate neurons are separable): FFN(x) = GELU(x W_fc + b_fc) W_proj +
+ * b_proj with GPT-2's layouts transposed to the API's, W_fc [d_ff, d],
+ * W_proj [d, d_ff].  Neuron n's input bias b_fc[n] belongs to its expert;
+ * the output bias b_proj is added once per token, whatever the selection:
+ *   h_n = GELU(W_fc[n,:] . x + b_fc[n]) [* sigmoid(g_e)]
+ *   y_i = b_proj[i] + sum over selected neurons n of W_proj[i, n] h_n.
+ * b_fc / b_proj may be NULL (zero).  Other arguments as for ppo_ffn. */
+int ppo_mlp(int64_t T, int64_t d, int64_t d_ff, int64_t E, const uint16_t *x,
+            const uint16_t *Wfc, const float *bfc, const uint16_t *Wproj, const float *bproj,
+            const int32_t *perm, const int32_t *idx, const int32_t *count, const double *g,
+            unsigned flags, double *y) {
+    if (T < 0 || d < 1 || E < 1 || d_ff % E != 0 || !x || !Wfc || !Wproj || !idx || !count || !y)
+        return -1;
+    if ((flags & PPO_AGG_SIGMOID) && !g) return -1;
+    const int64_t de = d_ff / E;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (int64_t t = 0; t < T; ++t) {
+        const uint16_t *xt = x + t * d;
+        double *yt = y + t * d;
+        int64_t k = count[t];
+        int32_t *nsel = (int32_t *)malloc(sizeof(int32_t) * (size_t)(k * de + 1));
+        double *h = (double *)malloc(sizeof(double) * (size_t)(k * de + 1));
+        double *xv = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!nsel || !h || !xv || k < 0 || k > E) {
+            bad = 1;
+            free(nsel);
+            free(h);
+            free(xv);
+            continue;
+        }
+        for (int64_t j = 0; j < d; ++j) xv[j] = bf16_value(xt[j]);
+        for (int64_t s = 0; s < k; ++s) {
+            int64_t e = idx[t * E + s];
+            double scale = 1.0;
+            if (flags & PPO_AGG_SIGMOID) scale = 1.0 / (1.0 + exp(-g[t * E + e]));
+            for (int64_t r = 0; r < de; ++r) {
+                int64_t n = perm ? perm[e * de + r] : e * de + r;
+                const uint16_t *w = Wfc + n * d;
+                double a = bfc ? (double)bfc[n] : 0.0;
+                for (int64_t j = 0; j < d; ++j) a += bf16_value(w[j]) * xv[j];
+                nsel[s * de + r] = (int32_t)n;
+                h[s * de + r] = ppo_gelu(a) * scale;
+            }
+        }
+        for (int64_t i = 0; i < d; ++i) {
+            const uint16_t *wp = Wproj + i * d_ff;
+            double acc = bproj ? (double)bproj[i] : 0.0;
+            for (int64_t q = 0; q < k * de; ++q) acc += bf16_value(wp[nsel[q]]) * h[q];
             yt[i] = acc;
         }
         free(nsel);

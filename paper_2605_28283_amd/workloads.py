@@ -114,7 +114,7 @@ def make_router_logits(B: int, E: int, seed, *, std: float = 3.0,
 
 
 # --------------------------------------------------------------------------
-# The five workloads.  Token streams use seed + 1000 so that changing T never
+# The workloads.  Token streams use seed + 1000 so that changing T never
 # changes the weights.
 
 @dataclass(frozen=True)
@@ -128,6 +128,7 @@ class Workload:
     layers: int = 1
     skewed: bool = False
     row_lognormal_sigma: float = 0.0
+    mlp: bool = False      # non-gated GELU MLP with biases (GPT-2) instead of SwiGLU
     notes: str = ""
 
 
@@ -142,10 +143,41 @@ WORKLOADS: Dict[str, Workload] = {
     "llama8b_prefill": Workload("llama8b_prefill", 4096, 14336, 112, (2048,), (0.7, 0.9),
                                 row_lognormal_sigma=0.5,
                                 notes="prefill, rows scaled by LogNormal(0, 0.5)"),
+    "gpt2m_decode": Workload("gpt2m_decode", 1024, 4096, 32, (1, 8, 32, 64), (0.5, 0.7, 0.9, 1.0),
+                             mlp=True, notes="GPT-2 Medium MLP layer (GELU, biases), decode batches"),
     "qwen7b_skewed": Workload("qwen7b_skewed", 3584, 18944, 148, (64,), (0.5, 0.9),
                               skewed=True,
                               notes="Gumbel(0,1.5) router bias, per-token temperature U(0.5,2)"),
 }
+
+
+@dataclass
+class MlpLayer:
+    """Non-gated GELU MLP (GPT-2 style) with its linear router."""
+    d: int
+    d_ff: int
+    E: int
+    W_r: np.ndarray      # [E, d]    bf16 bits
+    W_fc: np.ndarray     # [d_ff, d] bf16 bits
+    b_fc: np.ndarray     # [d_ff]    fp32
+    W_proj: np.ndarray   # [d, d_ff] bf16 bits
+    b_proj: np.ndarray   # [d]       fp32
+    perm: Optional[np.ndarray] = None
+
+
+def make_mlp_layer(d: int, d_ff: int, E: int, seed, *, weight_std: float = 0.02,
+                   bias_std: float = 0.02, perm: bool = False) -> MlpLayer:
+    """GPT-2-style MLP layer: weights N(0, 0.02^2) (GPT-2's initialisation
+    scale) rounded to bf16, biases N(0, 0.02^2) in fp32, router as in
+    make_layer; drawn in the order W_r, W_fc, b_fc, W_proj, b_proj[, perm]."""
+    rng = np.random.default_rng(seed)
+    W_r = bf16_bits(rng.standard_normal((E, d), dtype=np.float32) * np.float32(3.0 / np.sqrt(d)))
+    W_fc = bf16_bits(rng.standard_normal((d_ff, d), dtype=np.float32) * np.float32(weight_std))
+    b_fc = (rng.standard_normal(d_ff, dtype=np.float32) * np.float32(bias_std)).astype(np.float32)
+    W_proj = bf16_bits(rng.standard_normal((d, d_ff), dtype=np.float32) * np.float32(weight_std))
+    b_proj = (rng.standard_normal(d, dtype=np.float32) * np.float32(bias_std)).astype(np.float32)
+    p = rng.permutation(d_ff).astype(np.int32) if perm else None
+    return MlpLayer(d, d_ff, E, W_r, W_fc, b_fc, W_proj, b_proj, p)
 
 
 def make_layer_device(d: int, d_ff: int, E: int, seed: int, device="cuda", *,
@@ -171,11 +203,13 @@ def stack_layer_seed(layer: int, seed: int = 0) -> int:
     return 0x5EED0000 + 64 * seed + layer
 
 
-def workload_layer(w: Workload, seed: int = 0, layer: int = 0) -> Layer:
+def workload_layer(w: Workload, seed: int = 0, layer: int = 0):
     if w.layers > 1:
         s = np.random.SeedSequence(seed).spawn(w.layers + 1)[layer]
     else:
         s = seed
+    if w.mlp:
+        return make_mlp_layer(w.d, w.d_ff, w.E, s)
     return make_layer(w.d, w.d_ff, w.E, s, skewed=w.skewed)
 
 

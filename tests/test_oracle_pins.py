@@ -569,3 +569,113 @@ def test_router_loss_gradient_finite_differences(oracle_mod, coef):
             Lm, _ = oracle_mod.router_loss(gm, eps=eps, eta=eta, lam=lam, gamma=gam, grad=False)
             fd[i, j] = (Lp[3] - Lm[3]) / (2 * h)
     np.testing.assert_allclose(d, fd, rtol=1e-6, atol=1e-10)
+
+
+# ------------------------------------------- non-gated GELU MLP variant (Sec. 2.1)
+def test_gelu_matches_torch_tanh_form(oracle_mod):
+    """The oracle's GELU against torch's tanh-form GELU in float64, and the
+    identity GELU(a) - GELU(-a) = a (the tanh term is odd)."""
+    import torch
+    a = np.concatenate([np.linspace(-12, 12, 401), [0.0, 1e-8, -1e-8, 30.0, -30.0]])
+    ref = torch.nn.functional.gelu(torch.from_numpy(a), approximate="tanh").numpy()
+    got = oracle_mod.gelu(a)
+    # 1 + tanh(u) cancels for large negative a: absolute error ~ |a| ulp there
+    np.testing.assert_allclose(got, ref, rtol=1e-14, atol=1e-14)
+    np.testing.assert_allclose(got - oracle_mod.gelu(-a), a, rtol=1e-13, atol=1e-15)
+    assert oracle_mod.gelu(np.array([0.0]))[0] == 0.0
+
+
+def dense_mlp(x, L):
+    """GELU(x W_fc^T + b_fc) W_proj^T + b_proj, numpy float64 with torch's
+    GELU, no experts."""
+    import torch
+    X, Wf, Wp = f64(x), f64(L.W_fc), f64(L.W_proj)
+    a = X @ Wf.T + L.b_fc.astype(np.float64)
+    h = torch.nn.functional.gelu(torch.from_numpy(a), approximate="tanh").numpy()
+    return h @ Wp.T + L.b_proj.astype(np.float64)
+
+
+def all_experts(T, E):
+    return np.tile(np.arange(E, dtype=np.int32), (T, 1)), np.full(T, E, np.int32)
+
+
+@pytest.mark.parametrize("perm", [False, True])
+def test_mlp_all_experts_equal_dense(oracle_mod, perm):
+    """Eq. (moefication_decomp) for the non-gated MLP: all experts (in any
+    order, after any neuron permutation) give the dense MLP, biases included."""
+    from paper_2605_28283_amd.workloads import make_mlp_layer
+    L = make_mlp_layer(64, 128 * 5, 5, 7, perm=perm)
+    x, _ = make_tokens(6, 64, 8)
+    idx, cnt = all_experts(6, 5)
+    idx = idx[:, ::-1].copy()
+    y = oracle_mod.mlp(x, L.W_fc, L.b_fc, L.W_proj, L.b_proj, idx, cnt, perm=L.perm)
+    np.testing.assert_allclose(y, dense_mlp(x, L), rtol=1e-11, atol=1e-13)
+
+
+def test_mlp_partial_selection_and_bias_once(oracle_mod):
+    """A partial selection equals the dense MLP with the other neurons' h set
+    to zero; b_proj is added once (a token that keeps no expert gets
+    y = b_proj); disjoint selections add up after removing b_proj; sigmoid
+    aggregation scales each expert's block."""
+    import torch
+    from paper_2605_28283_amd.workloads import make_mlp_layer
+    E, d = 6, 64
+    L = make_mlp_layer(d, 128 * E, E, 9)
+    x, _ = make_tokens(3, d, 10)
+    X = f64(x)
+    a = X @ f64(L.W_fc).T + L.b_fc.astype(np.float64)
+    h = torch.nn.functional.gelu(torch.from_numpy(a), approximate="tanh").numpy()
+    sel = [[4, 1], [0], []]
+    idx = np.full((3, E), -1, np.int32)
+    cnt = np.array([len(s) for s in sel], np.int32)
+    for t, s in enumerate(sel):
+        idx[t, :len(s)] = s
+    y = oracle_mod.mlp(x, L.W_fc, L.b_fc, L.W_proj, L.b_proj, idx, cnt)
+    g = np.random.default_rng(0).normal(0, 2, (3, E))
+    ys = oracle_mod.mlp(x, L.W_fc, L.b_fc, L.W_proj, L.b_proj, idx, cnt, flags=2, g=g)
+    for t, s in enumerate(sel):
+        mask = np.zeros(128 * E)
+        scl = np.zeros(128 * E)
+        for e in s:
+            mask[128 * e:128 * e + 128] = 1.0
+            scl[128 * e:128 * e + 128] = 1.0 / (1.0 + np.exp(-g[t, e]))
+        ref = (h[t] * mask) @ f64(L.W_proj).T + L.b_proj
+        np.testing.assert_allclose(y[t], ref, rtol=1e-11, atol=1e-13)
+        np.testing.assert_allclose(ys[t], (h[t] * scl) @ f64(L.W_proj).T + L.b_proj,
+                                   rtol=1e-11, atol=1e-13)
+    np.testing.assert_array_equal(y[2], L.b_proj.astype(np.float64))
+    i1 = np.array([[4, -1, -1, -1, -1, -1]], np.int32)
+    i2 = np.array([[1, -1, -1, -1, -1, -1]], np.int32)
+    one = np.array([1], np.int32)
+    y1 = oracle_mod.mlp(x[:1], L.W_fc, L.b_fc, L.W_proj, L.b_proj, i1, one)
+    y2 = oracle_mod.mlp(x[:1], L.W_fc, L.b_fc, L.W_proj, L.b_proj, i2, one)
+    np.testing.assert_allclose((y1 - L.b_proj) + (y2 - L.b_proj), y[:1] - L.b_proj,
+                               rtol=1e-11, atol=1e-13)
+
+
+def test_mlp_scalar_closed_form(oracle_mod):
+    """One-hot weights: y_i = b_proj[i] + W_proj[i, n] GELU(x_j W_fc[n, j] +
+    b_fc[n]) for the single live neuron n, written out by hand."""
+    from paper_2605_28283_amd.workloads import MlpLayer, bf16_bits
+    d, E = 64, 1
+    d_ff = 128
+    W_r = bf16_bits(np.zeros((E, d), np.float32))
+    W_fc = np.zeros((d_ff, d), np.float32)
+    W_proj = np.zeros((d, d_ff), np.float32)
+    W_fc[37, 5] = 1.5
+    W_proj[11, 37] = -0.75
+    b_fc = np.zeros(d_ff, np.float32)
+    b_fc[37] = 0.25
+    b_proj = np.zeros(d, np.float32)
+    b_proj[3] = 0.5
+    L = MlpLayer(d, d_ff, E, W_r, bf16_bits(W_fc), b_fc, bf16_bits(W_proj), b_proj)
+    xv = np.zeros((1, d), np.float32)
+    xv[0, 5] = 2.0
+    y = oracle_mod.mlp(bf16_bits(xv), L.W_fc, L.b_fc, L.W_proj, L.b_proj,
+                       np.zeros((1, 1), np.int32), np.ones(1, np.int32))
+    a = 2.0 * 1.5 + 0.25
+    gelu_a = 0.5 * a * (1 + math.tanh(math.sqrt(2 / math.pi) * (a + 0.044715 * a ** 3)))
+    want = np.zeros(d)
+    want[3] = 0.5
+    want[11] = -0.75 * gelu_a
+    np.testing.assert_allclose(y[0], want, rtol=1e-14, atol=1e-15)
