@@ -42,6 +42,8 @@ def parse_args():
                     help="skip the 32-layer stacked decode measurement")
     ap.add_argument("--no-prefill", action="store_true",
                     help="skip the 2048-token prefill measurement")
+    ap.add_argument("--no-mlp", action="store_true",
+                    help="skip the GPT-2 Medium (non-gated GELU MLP) decode leg")
     ap.add_argument("--no-loss", action="store_true",
                     help="skip the router-loss (training regularisers) leg")
     ap.add_argument("--no-rules", action="store_true",
@@ -269,6 +271,8 @@ def main():
         out["prefill"] = bench_prefill(args, torch, np, pp)
     if not args.no_stack:
         out["stack"] = bench_stack(args, torch, np, pp)
+    if not args.no_mlp:
+        out["gpt2m_mlp"] = bench_mlp(args, torch, np, pp)
     if not args.no_loss:
         out["router_loss"] = bench_loss(args, torch, np, pp)
     if args.calibrate_copy_mib > 0:
@@ -471,6 +475,68 @@ def bench_stack(args, torch, np, pp):
             "k_mean_per_layer": [float(v) for v in cnt.mean(axis=1)],
             "union_per_layer": union,
             "k_histogram": {str(k): int(v) for k, v in enumerate(hist) if v}}
+
+
+def bench_mlp(args, torch, np, pp):
+    """The paper's GPT-2 Medium target: one non-gated GELU MLP layer with
+    biases (d 1024, d_ff 4096, E 32 experts of 128), decode T in {1, 32},
+    tau in {0.7, 0.9, 1.0}.  Calls rotate over 24 layer copies (384 MB of
+    weights, the whole model's MLPs, more than the Infinity Cache holds).
+    Algorithmic bytes: router E d 2 + union experts x (W_fc + W_proj 4 x 128 d,
+    b_fc 512) + b_proj 4 d + tokens 2 T d + y 4 T d."""
+    from paper_2605_28283_amd.workloads import WORKLOADS, make_mlp_layer, workload_tokens
+    w = WORKLOADS["gpt2m_decode"]
+    d, d_ff, E, ncp = w.d, w.d_ff, w.E, 24
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    hs = []
+    for c in range(ncp):
+        L = make_mlp_layer(d, d_ff, E, 4000 + c)
+        hs.append(pp.prunepath_create_mlp(d, d_ff, E, 64, dev(L.W_r.view(np.int16)),
+                                          dev(L.W_fc.view(np.int16)), dev(L.b_fc),
+                                          dev(L.W_proj.view(np.int16)), dev(L.b_proj)))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    res = []
+    for T in (1, 32):
+        xb, _ = workload_tokens(w, T)
+        x = dev(xb.view(np.int16))
+        y = torch.empty((T, d), dtype=torch.float32, device="cuda")
+        idx = torch.empty((T, E), dtype=torch.int32, device="cuda")
+        cnt = torch.empty((T,), dtype=torch.int32, device="cuda")
+        for tau in (0.7, 0.9, 1.0):
+            for i in range(args.warmup):
+                pp.prunepath_ffn_decode(hs[i % ncp], x, T, tau, None, y, idx, cnt, stream=stream)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for i in range(args.steps):
+                pp.prunepath_ffn_decode(hs[i % ncp], x, T, tau, None, y, idx, cnt, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / args.steps
+            us, ks = [], []
+            for h in hs:
+                pp.prunepath_route(h, x, T, tau, None, idx, cnt, stream=stream)
+                torch.cuda.synchronize()
+                ii = idx.cpu().numpy()
+                us.append(len(np.unique(ii[ii >= 0])))
+                ks.append(float(cnt.float().mean().item()))
+            U = float(np.mean(us))
+            nbytes = E * d * 2 + U * (4 * 128 * d + 512) + 4 * d + 6 * T * d
+            gbps = nbytes / (ms * 1e-3) / 1e9
+            r = {"T": T, "tau": tau, "ms_per_step": ms, "tokens_per_s_layer": T / (ms * 1e-3),
+                 "k_mean": float(np.mean(ks)), "union_experts": U,
+                 "algorithmic_bytes": nbytes, "effective_GBps": gbps,
+                 "frac_hbm_peak": gbps / HBM_PEAK_GBPS}
+            res.append(r)
+            print("# gpt2m MLP T=%-2d tau=%.2f  %7.1f us/step  %9.0f tok/s/layer  k %.2f  |U| %.1f"
+                  "  %6.0f GB/s" % (T, tau, ms * 1e3, r["tokens_per_s_layer"], r["k_mean"], U,
+                                     gbps), file=sys.stderr, flush=True)
+    for h in hs:
+        pp.prunepath_destroy(h)
+    torch.cuda.empty_cache()
+    return {"workload": "gpt2m_mlp_decode", "d": d, "d_ff": d_ff, "experts": E,
+            "layer_copies": ncp, "points": res}
 
 
 def bench_loss(args, torch, np, pp):

@@ -101,6 +101,29 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
                            const uint16_t *W_up, const uint16_t *W_down, const int32_t *perm,
                            const float *router_bias, uint32_t flags, void *hip_stream);
 
+/* prunepath_create_mlp -- a layer whose FFN is the non-gated GELU MLP of
+ * GPT-2 (the paper's GPT-2 Medium target, Sec. 4.2.2 and Sec. 4.5; Sec. 2.1
+ * notes that the expert decomposition holds for any FFN whose intermediate
+ * neurons are separable):
+ *   FFN(x) = GELU(x W_fc + b_fc) W_proj + b_proj,
+ * GELU in GPT-2's tanh form 0.5 a (1 + tanh(sqrt(2/pi) (a + 0.044715 a^3))).
+ * Expert e owns neurons perm[128e .. 128e+127] of W_fc, b_fc and W_proj; a
+ * kept expert contributes GELU(x W_fc^(e) + b_fc^(e)) W_proj^(e) [* sigmoid(g_e)]
+ * and b_proj is added once per token whatever is kept (a token that keeps no
+ * expert gets y = b_proj).
+ *   W_fc   : [d_ff, d] bf16, row n = intermediate neuron n (GPT-2's c_fc
+ *            weight transposed).
+ *   b_fc   : [d_ff] fp32 or NULL (zero).
+ *   W_proj : [d, d_ff] bf16, column n = intermediate neuron n.
+ *   b_proj : [d] fp32 or NULL (zero).
+ * Every other argument, the limits and the error behaviour are those of
+ * prunepath_create; the handle works with every call below. */
+pp_status prunepath_create_mlp(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
+                               int32_t max_tokens, const uint16_t *W_r, const uint16_t *W_fc,
+                               const float *b_fc, const uint16_t *W_proj, const float *b_proj,
+                               const int32_t *perm, const float *router_bias, uint32_t flags,
+                               void *hip_stream);
+
 /* prunepath_route -- routing only (Eqs. routing_logits, softmax_prob,
  * tau_thresh_activate).
  *   x          : [T, d] bf16 tokens, 1 <= T <= max_tokens.

@@ -8,6 +8,7 @@ from ._lib import (EXPORTED, PP_AGG_SIGMOID, PP_AGG_SUM, PP_EHIP, PP_EINVAL, PP_
                    PP_EUNSUPPORTED, PP_KERNEL_COUNT, PP_KERNEL_DISPATCH, PP_KERNEL_DOWN,
                    PP_KERNEL_GATEUP, PP_KERNEL_ROUTE, PP_OK, PP_SELECT_LTE, PP_SELECT_NUCLEUS,
                    PP_SELECT_STRICT, PP_SELECT_TOPK, PrunePathError, load, prunepath_create,
+                   prunepath_create_mlp,
                    prunepath_destroy, prunepath_ffn_decode, prunepath_ffn_prefill,
                    prunepath_profile_begin, prunepath_profile_end, prunepath_residual_rmsnorm,
                    prunepath_route, prunepath_router_loss, prunepath_router_loss_workspace,

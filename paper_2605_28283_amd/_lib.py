@@ -32,7 +32,7 @@ PP_KERNEL_GATEUP = 2
 PP_KERNEL_DOWN = 3
 PP_KERNEL_COUNT = 4
 
-EXPORTED = ("prunepath_create", "prunepath_route", "prunepath_ffn_decode",
+EXPORTED = ("prunepath_create", "prunepath_create_mlp", "prunepath_route", "prunepath_ffn_decode",
             "prunepath_ffn_prefill", "prunepath_destroy", "prunepath_status_string",
             "prunepath_profile_begin", "prunepath_profile_end", "prunepath_residual_rmsnorm",
             "prunepath_router_loss_workspace", "prunepath_router_loss")
@@ -59,6 +59,9 @@ def load():
         lib.prunepath_create.argtypes = [ctypes.POINTER(ctypes.c_void_p), I32, I32, I32, I32,
                                          P, P, P, P, P, P, U32, P]
         lib.prunepath_create.restype = ctypes.c_int
+        lib.prunepath_create_mlp.argtypes = [ctypes.POINTER(ctypes.c_void_p), I32, I32, I32, I32,
+                                             P, P, P, P, P, P, P, U32, P]
+        lib.prunepath_create_mlp.restype = ctypes.c_int
         lib.prunepath_route.argtypes = [P, P, I32, F32, P, P, P, P, P]
         lib.prunepath_route.restype = ctypes.c_int
         for f in (lib.prunepath_ffn_decode, lib.prunepath_ffn_prefill):
@@ -140,6 +143,18 @@ def prunepath_create(d, d_ff, E, max_tokens, W_r, W_gate, W_up, W_down, perm=Non
                                  _ptr(W_down, "bf16"), _ptr(perm, "i32"),
                                  _ptr(router_bias, "f32"), flags, _stream(stream))
     _check(st, "prunepath_create")
+    return out.value
+
+
+def prunepath_create_mlp(d, d_ff, E, max_tokens, W_r, W_fc, b_fc, W_proj, b_proj, perm=None,
+                         router_bias=None, flags=0, stream=None):
+    """Non-gated GELU MLP layer (b_fc / b_proj may be None).  Returns a handle."""
+    out = ctypes.c_void_p()
+    st = load().prunepath_create_mlp(ctypes.byref(out), d, d_ff, E, max_tokens,
+                                     _ptr(W_r, "bf16"), _ptr(W_fc, "bf16"), _ptr(b_fc, "f32"),
+                                     _ptr(W_proj, "bf16"), _ptr(b_proj, "f32"), _ptr(perm, "i32"),
+                                     _ptr(router_bias, "f32"), flags, _stream(stream))
+    _check(st, "prunepath_create_mlp")
     return out.value
 
 

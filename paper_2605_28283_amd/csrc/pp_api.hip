@@ -53,7 +53,7 @@ hipError_t dev_alloc(T **p, size_t elems) {
 
 void free_layer(pp_layer *L) {
     if (!L) return;
-    void *bufs[] = {L->Wr,     L->bias,  L->Wgu,     L->Wd,    L->gpart, L->counters,
+    void *bufs[] = {L->Wr,     L->bias,  L->Wgu,     L->Wd,    L->bfc,   L->bproj, L->gpart, L->counters,
                     L->selmask, L->gsig, L->idx_tmp, L->cnt_tmp, L->abpart, L->h_hi,
                     L->h_lo,   L->ypart, L->ecount,  L->tokl,  L->plan,  L->dec_tok,
                     L->emask};
@@ -103,15 +103,16 @@ pp_status run_ffn(pp_layer *L, const uint16_t *x, int32_t T, float tau, const fl
 
 }  // namespace
 
-extern "C" {
+namespace {
 
-pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
-                           int32_t max_tokens, const uint16_t *W_r, const uint16_t *W_gate,
-                           const uint16_t *W_up, const uint16_t *W_down, const int32_t *perm,
-                           const float *router_bias, uint32_t flags, void *hip_stream) {
-    if (!out) return PP_EINVAL;
-    *out = nullptr;
-    if (!W_r || !W_gate || !W_up || !W_down) return PP_EINVAL;
+// Both layer kinds: W_up NULL makes a non-gated layer (W_gate = W_fc,
+// W_down = W_proj, optional biases b_fc and b_proj).
+pp_status create_layer(pp_layer **out, int32_t d, int32_t d_ff, int32_t E, int32_t max_tokens,
+                       const uint16_t *W_r, const uint16_t *W_gate, const uint16_t *W_up,
+                       const uint16_t *W_down, const float *b_fc, const float *b_proj,
+                       const int32_t *perm, const float *router_bias, uint32_t flags,
+                       void *hip_stream) {
+    const bool gated = W_up != nullptr;
     if (d < 1 || d_ff < 1 || E < 1 || max_tokens < 1 || max_tokens > kMaxTokensLimit)
         return PP_EINVAL;
     if (flags & ~(PP_SELECT_STRICT | PP_SELECT_TOPK | PP_SELECT_LTE | PP_AGG_SIGMOID))
@@ -147,6 +148,7 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     L->dm.NS = d / kKStep;
     L->max_tokens = max_tokens;
     L->flags = flags;
+    L->gated = gated;
     hipError_t e = hipGetDevice(&L->device);
     if (e == hipSuccess)
         e = hipDeviceGetAttribute(&L->num_cu, hipDeviceAttributeMultiprocessorCount, L->device);
@@ -167,8 +169,12 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     };
     chk(dev_alloc(&L->Wr, dE));
     chk(dev_alloc(&L->bias, (size_t)E));
-    chk(dev_alloc(&L->Wgu, (size_t)2 * d_ff * d));
+    chk(dev_alloc(&L->Wgu, (size_t)(gated ? 2 : 1) * d_ff * d));
     chk(dev_alloc(&L->Wd, (size_t)d_ff * d));
+    if (!gated) {
+        chk(dev_alloc(&L->bfc, (size_t)d_ff));
+        if (b_proj) chk(dev_alloc(&L->bproj, (size_t)d));
+    }
     chk(dev_alloc(&L->gpart, L->gpart_elems));
     chk(dev_alloc(&L->counters, L->n_counters));
     chk(dev_alloc(&L->selmask, (size_t)max_tokens * 8));
@@ -195,7 +201,10 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
         chk(hipMemsetAsync(L->bias, 0, sizeof(float) * E, s));
     chk(hipMemsetAsync(L->counters, 0, sizeof(uint32_t) * L->n_counters, s));
     chk(hipMemsetAsync(L->emask, 0, sizeof(unsigned long long) * E, s));
-    if (a == hipSuccess) a = launch_repack(L, W_gate, W_up, W_down, perm, s);
+    if (!gated && !b_fc) chk(hipMemsetAsync(L->bfc, 0, sizeof(float) * d_ff, s));
+    if (L->bproj)
+        chk(hipMemcpyAsync(L->bproj, b_proj, sizeof(float) * d, hipMemcpyDeviceToDevice, s));
+    if (a == hipSuccess) a = launch_repack(L, W_gate, W_up, W_down, perm, gated ? nullptr : b_fc, s);
     chk(hipStreamSynchronize(s));
     if (a != hipSuccess) {
         free_layer(L);
@@ -203,6 +212,33 @@ pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
     }
     *out = L;
     return PP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pp_status prunepath_create(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
+                           int32_t max_tokens, const uint16_t *W_r, const uint16_t *W_gate,
+                           const uint16_t *W_up, const uint16_t *W_down, const int32_t *perm,
+                           const float *router_bias, uint32_t flags, void *hip_stream) {
+    if (!out) return PP_EINVAL;
+    *out = nullptr;
+    if (!W_r || !W_gate || !W_up || !W_down) return PP_EINVAL;
+    return create_layer(out, d, d_ff, E, max_tokens, W_r, W_gate, W_up, W_down, nullptr, nullptr,
+                        perm, router_bias, flags, hip_stream);
+}
+
+pp_status prunepath_create_mlp(pp_layer **out, int32_t d, int32_t d_ff, int32_t E,
+                               int32_t max_tokens, const uint16_t *W_r, const uint16_t *W_fc,
+                               const float *b_fc, const uint16_t *W_proj, const float *b_proj,
+                               const int32_t *perm, const float *router_bias, uint32_t flags,
+                               void *hip_stream) {
+    if (!out) return PP_EINVAL;
+    *out = nullptr;
+    if (!W_r || !W_fc || !W_proj) return PP_EINVAL;
+    return create_layer(out, d, d_ff, E, max_tokens, W_r, W_fc, nullptr, W_proj, b_fc, b_proj,
+                        perm, router_bias, flags, hip_stream);
 }
 
 pp_status prunepath_route(pp_layer *L, const uint16_t *x, int32_t T, float tau,

@@ -6,7 +6,8 @@
 // and workgroup 0 stores it for the down projection.
 //
 //   gateup_dec_k: unit = (group, K-slice), the gate/up projections and the
-//                 SiLU product of one group (code shared with prefill); the
+//                 SiLU product of one group (or the non-gated layer's input
+//                 projection, bias and GELU; code shared with prefill); the
 //                 K-split (one slice more for some groups) makes the units
 //                 fill the resident workgroups exactly, one round.
 //   down_dec_k  : sparse groups (<= 8 tokens per group on average): unit = one
@@ -37,6 +38,7 @@ struct DNParams {
     const uint16_t *h_hi;
     const uint16_t *h_lo;
     float *y;
+    const float *bproj;  // [d] output bias added once per token, or NULL
     float *ypart;      // [kDecodeChunks][T][d] chunk partials (dense groups)
     uint32_t *dn_cnt;  // [ceil(d / 128)] chunk arrivals per row block
     PlanView plan;
@@ -44,6 +46,7 @@ struct DNParams {
 
 // ------------------------------------------------------------------ gate/up
 
+template <bool GATED>
 __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     __shared__ uint4 xf[kXBufBytes / 16];
     __shared__ int stok[kGroupTokens];
@@ -79,7 +82,8 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         const unsigned long long m = D.mask[g];
         if (tid < 64 && ((m >> tid) & 1ull)) stok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
         __syncthreads();
-        gateup_group(P, D.e[g], __popcll(m), D.pair[g], g, ks, ksg, npairs, stok, xf, &s_flag);
+        gateup_group<GATED>(P, D.e[g], __popcll(m), D.pair[g], g, ks, ksg, npairs, stok, xf,
+                            &s_flag);
         __syncthreads();
     }
 }
@@ -278,9 +282,16 @@ __device__ void sh_unit(const DNParams &P, DnShared &S, int c, int rb, int Uc, i
     const int nq = nrows / 4;
     for (int i = tid; i < T * nq; i += blockDim.x) {
         const int t = i / nq, r = 4 * (i - t * nq);
-        const float4 v = *reinterpret_cast<const float4 *>(&S.yacc[t][r]);
+        float4 v = *reinterpret_cast<const float4 *>(&S.yacc[t][r]);
         const size_t col = (size_t)rb * kShRows + r;
         if (ES == 1) {
+            if (P.bproj) {
+                const float4 b = *reinterpret_cast<const float4 *>(P.bproj + col);
+                v.x += b.x;
+                v.y += b.y;
+                v.z += b.z;
+                v.w += b.w;
+            }
             *reinterpret_cast<float4 *>(P.y + (size_t)t * d + col) = v;
         } else {
             float *dst = P.ypart + ((size_t)c * T + t) * d + col;
@@ -322,8 +333,16 @@ __device__ void sh_unit(const DNParams &P, DnShared &S, int c, int rb, int Uc, i
                 }
     }
 #pragma unroll
-    for (int q = 0; q < kRedPer; ++q)
-        if (q < nown) *reinterpret_cast<float2 *>(P.y + off[q]) = acc[q];
+    for (int q = 0; q < kRedPer; ++q) {
+        if (q < nown) {
+            if (P.bproj) {
+                const float2 b = *reinterpret_cast<const float2 *>(P.bproj + off[q] % d);
+                acc[q].x += b.x;
+                acc[q].y += b.y;
+            }
+            *reinterpret_cast<float2 *>(P.y + off[q]) = acc[q];
+        }
+    }
 }
 
 template <int TB, int R>
@@ -386,6 +405,7 @@ __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
             float v = S.rw.yacc[0][t][r];
 #pragma unroll
             for (int w = 1; w < NW; ++w) v += S.rw.yacc[w][t][r];
+            if (P.bproj) v += P.bproj[rt * 16 + r];
             P.y[(size_t)t * P.d + rt * 16 + r] = v;
         }
         __syncthreads();
@@ -406,10 +426,14 @@ void launch_down_dec_tb(const DNParams &P, int num_cu, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s) {
-    static const int occ = resident(gateup_dec_k, kGuThreads);
+    static const int occ_g = resident(gateup_dec_k<true>, kGuThreads);
+    static const int occ_p = resident(gateup_dec_k<false>, kGuThreads);
     const GUParams gp = gu_params(L, x, T, false);
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
-    hipLaunchKernelGGL(gateup_dec_k, dim3(occ * L->num_cu), dim3(kGuThreads), 0, s, gp);
+    if (L->gated)
+        hipLaunchKernelGGL(gateup_dec_k<true>, dim3(occ_g * L->num_cu), dim3(kGuThreads), 0, s, gp);
+    else
+        hipLaunchKernelGGL(gateup_dec_k<false>, dim3(occ_p * L->num_cu), dim3(kGuThreads), 0, s, gp);
     prof_mark(L, PP_KERNEL_GATEUP, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
@@ -421,6 +445,7 @@ hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hi
     dp.h_hi = L->h_hi;
     dp.h_lo = L->h_lo;
     dp.y = y;
+    dp.bproj = L->bproj;
     dp.ypart = L->ypart;
     dp.dn_cnt = L->counters + counters_for(L->dm, L->max_tokens).down_base();
     dp.plan = plan_view(L, false);

@@ -9,7 +9,8 @@
 //
 //   dispatch_k  : per expert, the ascending list of tokens that kept it (block
 //                 scan + scatter) and the plan, written by the last expert to
-//                 finish; further workgroups clear y.
+//                 finish; further workgroups set y to the output bias (0 for
+//                 SwiGLU layers).
 //   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
 //                 SiLU product of one group (shared with the decode kernel).
 //   down_pf_k   : unit = (expert, 256 rows); the expert's down block stays in
@@ -31,6 +32,7 @@ struct DNParams {
     PlanView plan;
 };
 
+template <bool GATED>
 __global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
     __shared__ uint4 xf[kXBufBytes / 16];
     __shared__ int stok[kGroupTokens];
@@ -52,7 +54,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
         const int p0 = P.plan.grp_pair[g];
         if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
         __syncthreads();
-        gateup_group(P, e, n, p0, g, ks, KS, npairs, stok, xf, &s_flag);
+        gateup_group<GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, &s_flag);
         __syncthreads();
     }
 }
@@ -63,15 +65,17 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
                                                   int E, int32_t *__restrict__ ecount,
                                                   int32_t *__restrict__ tokl, int stride,
                                                   float *__restrict__ y, size_t ny4,
+                                                  const float *__restrict__ bproj, int d4,
                                                   uint32_t *cnt, PlanView plan) {
     __shared__ int scan[8];
     __shared__ int s_flag;
     const int e = blockIdx.x, tid = threadIdx.x;
-    if (e >= E) {  // workgroups past the experts clear y
+    if (e >= E) {  // workgroups past the experts set y to the output bias (or 0)
         float4 *y4 = reinterpret_cast<float4 *>(y);
+        const float4 *b4 = reinterpret_cast<const float4 *>(bproj);
         const size_t nz = (size_t)(gridDim.x - E) * blockDim.x;
         for (size_t i = (size_t)(e - E) * blockDim.x + tid; i < ny4; i += nz)
-            y4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            y4[i] = b4 ? b4[i % d4] : make_float4(0.f, 0.f, 0.f, 0.f);
         return;
     }
     const int w = e >> 5, b = e & 31;
@@ -252,15 +256,19 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     prof_mark(L, PP_KERNEL_DISPATCH, s, true);
     hipLaunchKernelGGL(dispatch_k, dim3(dm.E + L->num_cu), dim3(256), 0, s, L->selmask, T, dm.E,
                        L->ecount,
-                       L->tokl, L->max_tokens, y, (size_t)T * dm.d / 4,
+                       L->tokl, L->max_tokens, y, (size_t)T * dm.d / 4, L->bproj, dm.d / 4,
                        L->counters + cl.dispatch_base(), plan_view(L, true));
     prof_mark(L, PP_KERNEL_DISPATCH, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    static const int occ_gu = resident(gateup_pf_k, kGuThreads);
+    static const int occ_g = resident(gateup_pf_k<true>, kGuThreads);
+    static const int occ_p = resident(gateup_pf_k<false>, kGuThreads);
     const GUParams gp = gu_params(L, x, T, true);
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
-    hipLaunchKernelGGL(gateup_pf_k, dim3(occ_gu * L->num_cu), dim3(kGuThreads), 0, s, gp);
+    if (L->gated)
+        hipLaunchKernelGGL(gateup_pf_k<true>, dim3(occ_g * L->num_cu), dim3(kGuThreads), 0, s, gp);
+    else
+        hipLaunchKernelGGL(gateup_pf_k<false>, dim3(occ_p * L->num_cu), dim3(kGuThreads), 0, s, gp);
     prof_mark(L, PP_KERNEL_GATEUP, s, false);
     err = hipGetLastError();
     if (err != hipSuccess) return err;

@@ -1,6 +1,9 @@
 // Gate/up projections of one group (one expert with up to 64 of its tokens)
 // over one K-slice, shared by the decode and prefill kernels: Eq. (ffn)'s
-// x W_gate and x W_up for the kept expert, Eq. (moefication_decomp).
+// x W_gate and x W_up for the kept expert, Eq. (moefication_decomp).  With
+// GATED false the layer is the non-gated GELU MLP (one input projection with
+// a per-neuron bias, h = GELU(x W_fc + b_fc)), which Sec. 2.1's decomposition
+// covers as well.
 //
 // The group's token rows are staged in LDS in MFMA B-operand order; gate and
 // up fragments stream from HBM as contiguous 1 KiB wavefront loads
@@ -24,6 +27,7 @@ struct GUParams {
     const uint16_t *x;
     int T, d, E, NS;
     const uint16_t *Wgu;
+    const float *bfc;   // non-gated layers: [E][128] input bias in expert order
     const float *gsig;
     uint32_t flags;
     PlanView plan;
@@ -78,17 +82,23 @@ __device__ __forceinline__ void stage_x(const GUParams &P, const int *stok, int 
     }
 }
 
+// bf16 elements of one wavefront's weight block per K-step: gate and up
+// fragments (1024), or the single input projection of a non-gated layer (512).
+template <bool GATED>
+constexpr int kStepElems = GATED ? 1024 : 512;
+
+template <bool GATED>
 __device__ __forceinline__ void load_wgu(const uint16_t *wb, int step, int last, uint4 (&G)[kPF],
                                          uint4 (&U)[kPF]) {
 #pragma unroll
     for (int i = 0; i < kPF; ++i) {
-        const uint16_t *p = wb + (size_t)min(step + i, last) * 1024;
+        const uint16_t *p = wb + (size_t)min(step + i, last) * kStepElems<GATED>;
         G[i] = ldg16(p);
-        U[i] = ldg16(p + 512);
+        if (GATED) U[i] = ldg16(p + 512);
     }
 }
 
-template <int NT>
+template <int NT, bool GATED>
 __device__ __forceinline__ void mfma_wgu(const uint4 *xf, int nsc, int sl0, int nvalid,
                                          const uint4 (&G)[kPF], const uint4 (&U)[kPF],
                                          f32x4 (&ag)[NT], f32x4 (&au)[NT], int lane) {
@@ -99,13 +109,26 @@ __device__ __forceinline__ void mfma_wgu(const uint4 *xf, int nsc, int sl0, int 
             for (int j = 0; j < NT; ++j) {
                 const uint4 b = xf[(j * nsc + sl0 + i) * 64 + lane];
                 ag[j] = mfma16(G[i], b, ag[j]);
-                au[j] = mfma16(U[i], b, au[j]);
+                if (GATED) au[j] = mfma16(U[i], b, au[j]);
             }
         }
     }
 }
 
-template <int NT>
+// GPT-2's GELU, tanh form: 0.5 a (1 + tanh(sqrt(2/pi) (a + 0.044715 a^3))).
+__device__ __forceinline__ float gelu_tanh(float a) {
+    const float u = 0.7978845608028654f * (a + 0.044715f * a * a * a);
+    return 0.5f * a * (1.0f + tanhf(u));
+}
+
+// h of neuron r (0..127 inside expert e) from the projections' sums.
+template <bool GATED>
+__device__ __forceinline__ float act(const GUParams &P, int e, int r, float a, float b) {
+    if (GATED) return silu(a) * b;
+    return gelu_tanh(a + P.bfc[e * kExpertWidth + r]);
+}
+
+template <int NT, bool GATED>
 __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int ks, int KS,
                             int npairs, const int *stok, uint4 *xf, int *flag) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -117,18 +140,19 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
         ag[j] = f32x4{0.f, 0.f, 0.f, 0.f};
         au[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const uint16_t *wb = P.Wgu + (size_t)(e * 8 + wv) * P.NS * 1024 + lane * 8;
+    const uint16_t *wb = P.Wgu + (size_t)(e * 8 + wv) * P.NS * kStepElems<GATED> + lane * 8;
     for (int sc = s0; sc < s1; sc += nsc_max) {
         const int nsc = min(nsc_max, s1 - sc), last = sc + nsc - 1;
         uint4 G0[kPF], U0[kPF], G1[kPF], U1[kPF];
-        load_wgu(wb, sc, last, G0, U0);  // weights do not wait for the token staging
+        load_wgu<GATED>(wb, sc, last, G0, U0);  // weights do not wait for the token staging
         stage_x<NT>(P, stok, n, sc, nsc, xf);
         __syncthreads();
         for (int b = 0; b < nsc; b += 2 * kPF) {
-            if (b + kPF < nsc) load_wgu(wb, sc + b + kPF, last, G1, U1);
-            mfma_wgu<NT>(xf, nsc, b, min(kPF, nsc - b), G0, U0, ag, au, lane);
-            if (b + 2 * kPF < nsc) load_wgu(wb, sc + b + 2 * kPF, last, G0, U0);
-            if (b + kPF < nsc) mfma_wgu<NT>(xf, nsc, b + kPF, min(kPF, nsc - b - kPF), G1, U1, ag, au, lane);
+            if (b + kPF < nsc) load_wgu<GATED>(wb, sc + b + kPF, last, G1, U1);
+            mfma_wgu<NT, GATED>(xf, nsc, b, min(kPF, nsc - b), G0, U0, ag, au, lane);
+            if (b + 2 * kPF < nsc) load_wgu<GATED>(wb, sc + b + 2 * kPF, last, G0, U0);
+            if (b + kPF < nsc)
+                mfma_wgu<NT, GATED>(xf, nsc, b + kPF, min(kPF, nsc - b - kPF), G1, U1, ag, au, lane);
         }
         __syncthreads();
     }
@@ -143,7 +167,8 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
                 const float scl = sig ? P.gsig[(size_t)stok[q] * P.E + e] : 1.0f;
                 uint16_t hi[4], lo[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) split_bf16(silu(ag[j][i]) * au[j][i] * scl, hi[i], lo[i]);
+                for (int i = 0; i < 4; ++i)
+                    split_bf16(act<GATED>(P, e, r0 + i, ag[j][i], au[j][i]) * scl, hi[i], lo[i]);
                 const size_t row = (size_t)(p0 + q) * kExpertWidth + r0;
                 *reinterpret_cast<uint2 *>(P.h_hi + row) =
                     make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
@@ -160,8 +185,10 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
             float *row = P.abpart + ((size_t)ks * npairs + p0 + q) * 256 + r0;
             st_dev2(row, ag[j][0], ag[j][1]);
             st_dev2(row + 2, ag[j][2], ag[j][3]);
-            st_dev2(row + 128, au[j][0], au[j][1]);
-            st_dev2(row + 130, au[j][2], au[j][3]);
+            if (GATED) {
+                st_dev2(row + 128, au[j][0], au[j][1]);
+                st_dev2(row + 130, au[j][2], au[j][3]);
+            }
         }
     }
     if (!arrive_last(&P.cnt[g], (unsigned)KS, flag)) return;
@@ -190,7 +217,8 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
 #pragma unroll
                 for (int q = 0; q < kRedPer; ++q) {
                     u[k][q] = q < nq ? ld_dev2(base + off[q]) : make_float2(0.f, 0.f);
-                    v[k][q] = q < nq ? ld_dev2(base + off[q] + 128) : make_float2(0.f, 0.f);
+                    v[k][q] = (GATED && q < nq) ? ld_dev2(base + off[q] + 128)
+                                                : make_float2(0.f, 0.f);
                 }
             }
 #pragma unroll
@@ -211,8 +239,8 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
                 const int qq = i >> 6, r = 2 * (i & 63);
                 const float scl = sig ? P.gsig[(size_t)stok[qq] * P.E + e] : 1.0f;
                 uint16_t h0, l0, h1, l1;
-                split_bf16(silu(a[q].x) * b[q].x * scl, h0, l0);
-                split_bf16(silu(a[q].y) * b[q].y * scl, h1, l1);
+                split_bf16(act<GATED>(P, e, r, a[q].x, b[q].x) * scl, h0, l0);
+                split_bf16(act<GATED>(P, e, r + 1, a[q].y, b[q].y) * scl, h1, l1);
                 const size_t o = (size_t)(p0 + qq) * kExpertWidth + r;
                 *reinterpret_cast<uint32_t *>(P.h_hi + o) = h0 | ((uint32_t)h1 << 16);
                 *reinterpret_cast<uint32_t *>(P.h_lo + o) = l0 | ((uint32_t)l1 << 16);
@@ -266,14 +294,15 @@ __device__ void decode_plan(const GUParams &P, DecodePlan &D) {
 }
 
 // One group's gate/up unit, dispatched on its number of 16-token tiles.
+template <bool GATED>
 __device__ __forceinline__ void gateup_group(const GUParams &P, int e, int n, int p0, int g,
                                              int ks, int KS, int npairs, const int *stok,
                                              uint4 *xf, int *flag) {
     switch ((n + 15) >> 4) {
-    case 1: gateup_unit<1>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
-    case 2: gateup_unit<2>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
-    case 3: gateup_unit<3>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
-    default: gateup_unit<4>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
+    case 1: gateup_unit<1, GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
+    case 2: gateup_unit<2, GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
+    case 3: gateup_unit<3, GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
+    default: gateup_unit<4, GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
     }
 }
 
@@ -307,6 +336,7 @@ inline GUParams gu_params(pp_layer *L, const uint16_t *x, int T, bool prefill) {
     P.E = dm.E;
     P.NS = dm.NS;
     P.Wgu = L->Wgu;
+    P.bfc = L->bfc;
     P.gsig = L->gsig;
     P.flags = L->flags;
     P.plan = plan_view(L, prefill);

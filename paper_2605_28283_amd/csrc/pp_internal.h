@@ -67,13 +67,16 @@ struct pp_layer {
     pp::pp_dims dm;
     int max_tokens;
     uint32_t flags;
+    bool gated;        // SwiGLU (true) or the non-gated GELU MLP with biases
     int device;
     int num_cu;
     // library-owned weights
     uint16_t *Wr;      // [E][d] bf16
     float *bias;       // [E] fp32 (zeros when the caller gave none)
-    uint16_t *Wgu;     // expert-major gate/up MFMA fragments
-    uint16_t *Wd;      // expert-major down MFMA fragments
+    uint16_t *Wgu;     // expert-major gate/up (or W_fc) MFMA fragments
+    uint16_t *Wd;      // expert-major down (or W_proj) MFMA fragments
+    float *bfc;        // non-gated: [d_ff] input bias in expert order (Pi applied)
+    float *bproj;      // non-gated: [d] output bias, or NULL
     // scratch
     float *gpart;       // router K-slice partial logits [d/512][max_tokens][E]
     size_t gpart_elems;
@@ -115,8 +118,11 @@ counter_layout counters_for(const pp_dims &dm, int max_tokens);
 inline PlanView plan_view(pp_layer *L, bool prefill);
 
 
+// W_up NULL: non-gated layer (one input projection per expert); b_fc, if
+// given, is copied into expert order.
 hipError_t launch_repack(pp_layer *L, const uint16_t *W_gate, const uint16_t *W_up,
-                         const uint16_t *W_down, const int32_t *perm, hipStream_t s);
+                         const uint16_t *W_down, const int32_t *perm, const float *b_fc,
+                         hipStream_t s);
 hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const float *inv_temp,
                         int32_t *idx, int32_t *count, float *gate_w, bool build_plan,
                         hipStream_t s);

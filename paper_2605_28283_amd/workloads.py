@@ -163,6 +163,7 @@ class MlpLayer:
     W_proj: np.ndarray   # [d, d_ff] bf16 bits
     b_proj: np.ndarray   # [d]       fp32
     perm: Optional[np.ndarray] = None
+    bias: Optional[np.ndarray] = None   # [E] fp32 router bias (none in these workloads)
 
 
 def make_mlp_layer(d: int, d_ff: int, E: int, seed, *, weight_std: float = 0.02,

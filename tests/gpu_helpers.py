@@ -20,16 +20,29 @@ def to_dev(bits):
 
 
 class DevLayer:
-    def __init__(self, L, max_tokens, flags=0):
+    """A SwiGLU layer (workloads.Layer) or a non-gated GELU MLP layer
+    (workloads.MlpLayer) uploaded and created through the C ABI."""
+
+    def __init__(self, L, max_tokens, flags=0, biases=True):
         t = torch()
         self.L = L
         self.flags = flags
         self.E, self.d = L.E, L.d
-        self.W = [to_dev(a) for a in (L.W_r, L.W_gate, L.W_up, L.W_down)]
+        self.mlp = hasattr(L, "W_fc")
         self.perm = None if L.perm is None else t.from_numpy(L.perm).cuda()
         self.bias = None if L.bias is None else t.from_numpy(L.bias).cuda()
-        self.h = pp.prunepath_create(L.d, L.d_ff, L.E, max_tokens, *self.W, perm=self.perm,
-                                     router_bias=self.bias, flags=flags)
+        if self.mlp:
+            self.W = [to_dev(a) for a in (L.W_r, L.W_fc, L.W_proj)]
+            self.b_fc = t.from_numpy(L.b_fc).cuda() if biases else None
+            self.b_proj = t.from_numpy(L.b_proj).cuda() if biases else None
+            self.h = pp.prunepath_create_mlp(L.d, L.d_ff, L.E, max_tokens, self.W[0], self.W[1],
+                                             self.b_fc, self.W[2], self.b_proj, perm=self.perm,
+                                             router_bias=self.bias, flags=flags)
+        else:
+            self.W = [to_dev(a) for a in (L.W_r, L.W_gate, L.W_up, L.W_down)]
+            self.h = pp.prunepath_create(L.d, L.d_ff, L.E, max_tokens, *self.W, perm=self.perm,
+                                         router_bias=self.bias, flags=flags)
+        self.biases = biases
 
     def close(self):
         if self.h:
@@ -134,16 +147,21 @@ def check_selection(oracle, L, x, tau, flags, idx_g, cnt_g, inv_temp=None):
     return r, exempt
 
 
-def check_output(oracle, L, x, flags, idx_g, cnt_g, y_g, g_ref, rows=None):
+def check_output(oracle, L, x, flags, idx_g, cnt_g, y_g, g_ref, rows=None, biases=True):
     """y against the oracle evaluated on the GPU's own selection."""
     if rows is None:
         rows = np.arange(x.shape[0])
-    y_ref = oracle.ffn(x[rows], L.W_gate, L.W_up, L.W_down, idx_g[rows], cnt_g[rows],
-                       flags=flags, g=g_ref[rows], perm=L.perm)
+    if hasattr(L, "W_fc"):
+        y_ref = oracle.mlp(x[rows], L.W_fc, L.b_fc if biases else None, L.W_proj,
+                           L.b_proj if biases else None, idx_g[rows], cnt_g[rows], flags=flags,
+                           g=g_ref[rows], perm=L.perm)
+    else:
+        y_ref = oracle.ffn(x[rows], L.W_gate, L.W_up, L.W_down, idx_g[rows], cnt_g[rows],
+                           flags=flags, g=g_ref[rows], perm=L.perm)
     err = np.abs(y_g[rows].astype(np.float64) - y_ref)
     rms = float(np.sqrt(np.mean(y_ref ** 2)))
     assert np.isfinite(y_g[rows]).all()
-    if rms == 0.0:  # no token kept an expert (LTE): y must be exactly zero
+    if rms == 0.0:  # no token kept an expert (LTE) and no output bias: y must be 0
         assert (y_g[rows] == 0).all()
         return 0.0
     worst = float(err.max()) / rms
@@ -154,5 +172,6 @@ def check_output(oracle, L, x, flags, idx_g, cnt_g, y_g, g_ref, rows=None):
 def parity(oracle, dl, mode, x, tau, inv_temp=None, rows=None):
     idx, cnt, y = dl.run(mode, x, tau, inv_temp)
     r, exempt = check_selection(oracle, dl.L, x, tau, dl.flags, idx, cnt, inv_temp)
-    worst = check_output(oracle, dl.L, x, dl.flags, idx, cnt, y, r["g"], rows)
+    worst = check_output(oracle, dl.L, x, dl.flags, idx, cnt, y, r["g"], rows,
+                         biases=getattr(dl, "biases", True))
     return dict(idx=idx, cnt=cnt, y=y, exempt=int(exempt.sum()), worst=worst)

@@ -149,3 +149,31 @@ def test_router_loss_rejects_bad_arguments(args):
     g, B, E, eps, eta, lam, gam, losses, dg, ws = args
     assert lib.prunepath_router_loss(g, B, E, eps, eta, lam, gam, losses, dg, ws,
                                      None) == pp.PP_EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (None, 8, 8),      # W_r NULL
+    (8, None, 8),      # W_fc NULL
+    (8, 8, None),      # W_proj NULL
+])
+def test_create_mlp_rejects_null_weights(args):
+    import ctypes
+    lib = pp.load()
+    W_r, W_fc, W_proj = args
+    out = ctypes.c_void_p(123)
+    assert lib.prunepath_create_mlp(ctypes.byref(out), 64, 128, 1, 4, W_r, W_fc, None, W_proj,
+                                    None, None, None, 0, None) == pp.PP_EINVAL
+    assert out.value is None
+
+
+def test_create_mlp_rejects_bad_shapes():
+    import ctypes
+    lib = pp.load()
+    out = ctypes.c_void_p()
+    for d, d_ff, E, mt, flags, want in ((0, 128, 1, 4, 0, pp.PP_EINVAL),
+                                        (64, 128, 1, 0, 0, pp.PP_EINVAL),
+                                        (64, 256, 1, 4, 0, pp.PP_EUNSUPPORTED),
+                                        (96, 128, 1, 4, 0, pp.PP_EUNSUPPORTED),
+                                        (64, 128, 1, 4, 16, pp.PP_EINVAL)):
+        assert lib.prunepath_create_mlp(ctypes.byref(out), d, d_ff, E, mt, 8, 8, None, 8, None,
+                                        None, None, flags, None) == want
