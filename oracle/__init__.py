@@ -8,6 +8,9 @@ The arithmetic lives in ``prunepath_oracle.c`` (fp64, per token, following the
 paper's Sec. 3.1 equations in order, and the Sec. 3.2 / Sec. 4.2.3 routing
 regularisers with their gradient); this module only marshals numpy arrays.
 
+The balanced k-means of MoEfication's clustering step (Sec. 2.2) is the
+module ``oracle.kmeans`` (numpy / scipy, fp64).
+
 Readings taken where the paper is open are stated in the C file's header.
 Every function here is pinned by ``tests/test_oracle_pins.py`` against closed
 forms, library routines, brute force and the paper's all-expert identity

@@ -101,6 +101,22 @@ def make_tokens(T: int, d: int, seed, *, row_lognormal_sigma: float = 0.0,
 ROUTER_LOSS_B, ROUTER_LOSS_E = 16384, 112
 
 
+def make_clustered_features(n: int, D: int, k: int, seed, *, centre_std: float = 0.02,
+                            noise_std: float = 0.02):
+    """Neuron feature rows for the clustering step: n rows of D bf16 values
+    around k planted centres (n / k rows each), centre ~ N(0, centre_std^2),
+    row = centre + N(0, noise_std^2), rows shuffled; plus k distinct row
+    indices for the initial centroids.  Returns (F bits [n, D], planted group
+    [n], init rows [k])."""
+    rng = np.random.default_rng(seed)
+    centres = rng.standard_normal((k, D), dtype=np.float32) * np.float32(centre_std)
+    group = np.repeat(np.arange(k), n // k)
+    rng.shuffle(group)
+    F = centres[group] + rng.standard_normal((n, D), dtype=np.float32) * np.float32(noise_std)
+    init = rng.choice(n, size=k, replace=False).astype(np.int32)
+    return bf16_bits(F), group.astype(np.int32), init
+
+
 def make_router_logits(B: int, E: int, seed, *, std: float = 3.0,
                        row_lognormal_sigma: float = 0.5, expert_gumbel: float = 1.0) -> np.ndarray:
     """Router logits [B, E] fp32 for the routing-regulariser kernels."""

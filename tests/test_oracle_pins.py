@@ -679,3 +679,97 @@ def test_mlp_scalar_closed_form(oracle_mod):
     want[3] = 0.5
     want[11] = -0.75 * gelu_a
     np.testing.assert_allclose(y[0], want, rtol=1e-14, atol=1e-15)
+
+
+# ----------------------------------------- balanced k-means (MoEfication, Sec. 2.2)
+def _balanced_splits(n, k):
+    """Every assignment of n labelled rows to k labelled clusters of n/k rows."""
+    m = n // k
+
+    def rec(rest, j):
+        if j == k - 1:
+            yield {j: rest}
+            return
+        for c in itertools.combinations(rest, m):
+            left = tuple(r for r in rest if r not in c)
+            for tail in rec(left, j + 1):
+                tail = dict(tail)
+                tail[j] = c
+                yield tail
+    for split in rec(tuple(range(n)), 0):
+        a = np.empty(n, np.int64)
+        for j, rows in split.items():
+            a[list(rows)] = j
+        yield a
+
+
+@pytest.mark.parametrize("n,k,seed", [(8, 2, 0), (9, 3, 1), (8, 4, 2), (12, 3, 3)])
+def test_kmeans_assignment_brute_force(n, k, seed):
+    """The balanced assignment's cost is the minimum over every balanced
+    assignment (enumerated), and the assignment is balanced."""
+    from oracle import kmeans
+    rng = np.random.default_rng(seed)
+    X = rng.normal(0, 1, (n, 3))
+    mu = rng.normal(0, 1, (k, 3))
+    a, cost = kmeans.balanced_assign(X, mu)
+    assert (np.bincount(a, minlength=k) == n // k).all()
+    S = ((X[:, None, :] - mu[None]) ** 2).sum(-1)
+    best = min(S[np.arange(n), b].sum() for b in _balanced_splits(n, k))
+    assert cost == pytest.approx(best, rel=1e-12)
+
+
+def test_kmeans_planted_clusters_recovered():
+    """Rows scattered tightly around k far-apart centres, m per centre, in a
+    shuffled order: one iteration from one row of each group returns the
+    planted groups, their means as centroids and Pi listing them."""
+    from oracle import kmeans
+    rng = np.random.default_rng(4)
+    k, m, D = 6, 8, 5
+    centres = rng.normal(0, 10, (k, D))
+    X = np.repeat(centres, m, axis=0) + rng.normal(0, 0.01, (k * m, D))
+    order = rng.permutation(k * m)
+    X = X[order]
+    group = np.repeat(np.arange(k), m)[order]
+    init = np.stack([X[np.nonzero(group == j)[0][0]] for j in range(k)])
+    r = kmeans.balanced_kmeans(X, init, 1)
+    np.testing.assert_array_equal(r["assign"], group)
+    for j in range(k):
+        np.testing.assert_allclose(r["centroids"][j], X[group == j].mean(0), rtol=1e-12)
+        np.testing.assert_array_equal(r["perm"][j * m:(j + 1) * m], np.nonzero(group == j)[0])
+
+
+def test_kmeans_unconstrained_when_already_balanced():
+    """If every row's nearest centroid already gives m rows per cluster, the
+    balanced assignment is the nearest-centroid assignment."""
+    from oracle import kmeans
+    rng = np.random.default_rng(5)
+    k, m = 4, 6
+    mu = np.eye(k, 4) * 20
+    X = np.repeat(mu, m, axis=0) + rng.normal(0, 1, (k * m, 4))
+    a, _ = kmeans.balanced_assign(X, mu)
+    near = np.argmin(((X[:, None] - mu[None]) ** 2).sum(-1), axis=1)
+    assert (np.bincount(near, minlength=k) == m).all()
+    np.testing.assert_array_equal(a, near)
+
+
+def test_kmeans_objective_monotone_and_perm_valid():
+    """Lloyd's steps never increase the objective (the assignment is optimal
+    for fixed centroids, the means for a fixed assignment); Pi is a
+    permutation whose blocks are the clusters, ascending."""
+    from oracle import kmeans
+    rng = np.random.default_rng(6)
+    n, k, D = 96, 8, 7
+    X = rng.normal(0, 1, (n, D))
+    init = X[rng.choice(n, k, replace=False)]
+    r = kmeans.balanced_kmeans(X, init, 6)
+    assert (np.diff(r["objective"]) <= 1e-9 * r["objective"][0]).all()
+    p = r["perm"]
+    assert sorted(p.tolist()) == list(range(n))
+    m = n // k
+    for j in range(k):
+        blk = p[j * m:(j + 1) * m]
+        assert (r["assign"][blk] == j).all() and (np.diff(blk) > 0).all()
+    # the objective after the last update is the cost of the last assignment
+    # evaluated at the updated centroids, which is no larger
+    last = ((X - r["centroids"][r["assign"]]) ** 2).sum()
+    assert last <= r["objective"][-1] + 1e-9
