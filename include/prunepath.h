@@ -25,8 +25,9 @@
  *    calls that can run concurrently (for example on two streams).
  *  - Errors: a call that returns anything but PP_OK has enqueued no work and
  *    left every output untouched, except PP_EHIP, which reports a failure of
- *    the HIP runtime (outputs then undefined).  No exception or abort crosses
- *    this interface.
+ *    the HIP runtime (outputs then undefined), and PP_ENOTCONVERGED (see
+ *    prunepath_balanced_kmeans).  No exception or abort crosses this
+ *    interface.
  */
 #ifndef PRUNEPATH_H
 #define PRUNEPATH_H
@@ -46,7 +47,8 @@ typedef enum {
     PP_EINVAL = 1,        /* bad argument (NULL pointer, size, tau, permutation) */
     PP_ENOMEM = 2,        /* device allocation failed */
     PP_EHIP = 3,          /* HIP runtime error */
-    PP_EUNSUPPORTED = 4   /* valid but unsupported shape (see create) */
+    PP_EUNSUPPORTED = 4,  /* valid but unsupported shape (see create) */
+    PP_ENOTCONVERGED = 5  /* iteration limit reached (balanced k-means assignment) */
 } pp_status;
 
 /* Selection rule (Eq. tau_thresh_activate; pi = experts by descending p,
@@ -201,6 +203,45 @@ size_t prunepath_router_loss_workspace(int32_t B, int32_t E); /* 0 for bad sizes
 pp_status prunepath_router_loss(const float *g, int32_t B, int32_t E, float eps, float eta,
                                 float lambda, float gamma, float *losses, float *dg,
                                 void *workspace, void *hip_stream);
+
+/* prunepath_balanced_kmeans -- MoEfication's neuron clustering (Sec. 2.2):
+ * balanced k-means of the n rows of F into k clusters of exactly m = n / k
+ * rows (the constrained k-means the paper cites), which gives the
+ * permutation Pi of Eq. (permuted_weights) that prunepath_create takes as
+ * `perm` (n = d_ff, k = E, F = one feature row per intermediate neuron, e.g.
+ * the rows of W_gate or of W_fc).  Each of `iters` Lloyd iterations:
+ *   assignment  minimise sum_i ||F_i - mu_a(i)||^2 subject to the balance,
+ *               exactly (an auction on k cluster prices whose final argmax
+ *               assignment is balanced, hence optimal by LP duality);
+ *   update      mu_j = mean of cluster j's rows.
+ *   F              : [n, D] bf16, 16-byte aligned (device)
+ *   init_centroids : [k, D] fp32 (device); may equal `centroids`
+ *   iters          : 1 .. 1000
+ *   assign         : [n] int32 out (device): cluster of each row, last iteration
+ *   perm           : [n] int32 out (device): Pi, cluster 0's rows ascending,
+ *                    then cluster 1's, ...
+ *   centroids      : [k, D] fp32 out (device): the means of the last assignment
+ *   objective      : [iters] fp32 out (device) or NULL: the assignment cost of
+ *                    each iteration with the centroids it used
+ *   prices         : [k] fp32 out (device) or NULL: the last step's prices
+ *                    (row i's cluster maximises -||mu_j||^2 + 2 F_i.mu_j -
+ *                    price_j over j, in the kernels' fp32 arithmetic)
+ *   rounds         : [iters] int32 out (HOST memory) or NULL: auction rounds
+ *                    each assignment took (-1: did not converge)
+ *   workspace      : prunepath_kmeans_workspace(n, D, k) bytes (device),
+ *                    16-byte aligned, no initial contents required
+ * Limits: 1 <= k <= 256, k <= n <= 65536, n % k == 0, 64 <= D <= 16384,
+ * D % 64 == 0 (PP_EINVAL otherwise; the workspace query returns 0).  The
+ * call blocks: it synchronises hip_stream to follow the auction.
+ * PP_ENOTCONVERGED when an assignment needs more than 32768 auction rounds
+ * (possible when rows are exact duplicates of each other); outputs then hold
+ * the last unbalanced state. */
+size_t prunepath_kmeans_workspace(int32_t n, int32_t D, int32_t k); /* 0 for bad sizes */
+pp_status prunepath_balanced_kmeans(const uint16_t *F, int32_t n, int32_t D, int32_t k,
+                                    const float *init_centroids, int32_t iters, int32_t *assign,
+                                    int32_t *perm, float *centroids, float *objective,
+                                    float *prices, int32_t *rounds, void *workspace,
+                                    void *hip_stream);
 
 /* Kernel kinds reported by prunepath_profile_end. */
 #define PP_KERNEL_ROUTE 0     /* router: logits, softmax, sort, cut */

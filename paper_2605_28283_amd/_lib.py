@@ -18,6 +18,7 @@ PP_EINVAL = 1
 PP_ENOMEM = 2
 PP_EHIP = 3
 PP_EUNSUPPORTED = 4
+PP_ENOTCONVERGED = 5
 
 PP_SELECT_NUCLEUS = 0
 PP_SELECT_STRICT = 1
@@ -35,7 +36,8 @@ PP_KERNEL_COUNT = 4
 EXPORTED = ("prunepath_create", "prunepath_create_mlp", "prunepath_route", "prunepath_ffn_decode",
             "prunepath_ffn_prefill", "prunepath_destroy", "prunepath_status_string",
             "prunepath_profile_begin", "prunepath_profile_end", "prunepath_residual_rmsnorm",
-            "prunepath_router_loss_workspace", "prunepath_router_loss")
+            "prunepath_router_loss_workspace", "prunepath_router_loss",
+            "prunepath_kmeans_workspace", "prunepath_balanced_kmeans")
 
 
 class PrunePathError(RuntimeError):
@@ -80,6 +82,11 @@ def load():
         lib.prunepath_router_loss_workspace.restype = ctypes.c_size_t
         lib.prunepath_router_loss.argtypes = [P, I32, I32, F32, F32, F32, F32, P, P, P, P]
         lib.prunepath_router_loss.restype = ctypes.c_int
+        lib.prunepath_kmeans_workspace.argtypes = [I32, I32, I32]
+        lib.prunepath_kmeans_workspace.restype = ctypes.c_size_t
+        lib.prunepath_balanced_kmeans.argtypes = [P, I32, I32, I32, P, I32, P, P, P, P, P, P, P,
+                                                  P]
+        lib.prunepath_balanced_kmeans.restype = ctypes.c_int
         lib.prunepath_status_string.argtypes = [ctypes.c_int]
         lib.prunepath_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -198,6 +205,24 @@ def prunepath_router_loss(g, B, E, eps, eta, lam, gamma, losses, dg, workspace, 
                                       _ptr(losses, "f32"), _ptr(dg, "f32"), _ptr(workspace),
                                       _stream(stream))
     _check(st, "prunepath_router_loss")
+
+
+def prunepath_kmeans_workspace(n, D, k):
+    """Workspace bytes prunepath_balanced_kmeans needs (0 for bad sizes)."""
+    return int(load().prunepath_kmeans_workspace(n, D, k))
+
+
+def prunepath_balanced_kmeans(F, n, D, k, init_centroids, iters, assign, perm, centroids,
+                              workspace, objective=None, prices=None, stream=None):
+    """Balanced k-means of F's rows (blocks until done).  Returns the auction
+    rounds of each iteration as a list."""
+    rounds = (ctypes.c_int32 * iters)()
+    st = load().prunepath_balanced_kmeans(
+        _ptr(F, "bf16"), n, D, k, _ptr(init_centroids, "f32"), iters, _ptr(assign, "i32"),
+        _ptr(perm, "i32"), _ptr(centroids, "f32"), _ptr(objective, "f32"), _ptr(prices, "f32"),
+        ctypes.cast(rounds, ctypes.c_void_p), _ptr(workspace), _stream(stream))
+    _check(st, "prunepath_balanced_kmeans")
+    return list(rounds)
 
 
 def prunepath_profile_begin(handle, capacity):

@@ -315,6 +315,7 @@ const char *prunepath_status_string(pp_status s) {
     case PP_ENOMEM: return "out of device memory";
     case PP_EHIP: return "HIP runtime error";
     case PP_EUNSUPPORTED: return "unsupported shape";
+    case PP_ENOTCONVERGED: return "did not converge";
     }
     return "unknown status";
 }

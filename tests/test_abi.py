@@ -177,3 +177,22 @@ def test_create_mlp_rejects_bad_shapes():
                                         (64, 128, 1, 4, 16, pp.PP_EINVAL)):
         assert lib.prunepath_create_mlp(ctypes.byref(out), d, d_ff, E, mt, 8, 8, None, 8, None,
                                         None, None, flags, None) == want
+
+
+def test_kmeans_workspace_and_rejections():
+    lib = pp.load()
+    assert lib.prunepath_kmeans_workspace(14336, 4096, 112) > 0
+    for n, D, k in ((0, 64, 1), (64, 64, 0), (64, 64, 257), (100, 64, 8), (64, 96, 8),
+                    (64, 32, 8), (131072, 64, 8), (8, 64, 16)):
+        assert lib.prunepath_kmeans_workspace(n, D, k) == 0, (n, D, k)
+    args = dict(F=16, n=256, D=64, k=8, init=16, iters=1, assign=16, perm=16, cent=16, ws=256)
+    bad = [dict(F=None), dict(init=None), dict(assign=None), dict(perm=None), dict(cent=None),
+           dict(ws=None), dict(iters=0), dict(iters=1001), dict(n=100), dict(D=96), dict(k=0),
+           dict(F=8), dict(ws=264)]
+    for b in bad:
+        a = dict(args, **b)
+        st = lib.prunepath_balanced_kmeans(a["F"], a["n"], a["D"], a["k"], a["init"], a["iters"],
+                                           a["assign"], a["perm"], a["cent"], None, None, None,
+                                           a["ws"], None)
+        assert st == pp.PP_EINVAL, b
+    assert pp.prunepath_status_string(pp.PP_ENOTCONVERGED) == "did not converge"
