@@ -44,6 +44,8 @@ def parse_args():
                     help="skip the 2048-token prefill measurement")
     ap.add_argument("--no-mlp", action="store_true",
                     help="skip the GPT-2 Medium (non-gated GELU MLP) decode leg")
+    ap.add_argument("--no-kmeans", action="store_true",
+                    help="skip the balanced k-means (neuron clustering) leg")
     ap.add_argument("--no-loss", action="store_true",
                     help="skip the router-loss (training regularisers) leg")
     ap.add_argument("--no-rules", action="store_true",
@@ -275,6 +277,8 @@ def main():
         out["gpt2m_mlp"] = bench_mlp(args, torch, np, pp)
     if not args.no_loss:
         out["router_loss"] = bench_loss(args, torch, np, pp)
+    if not args.no_kmeans:
+        out["kmeans"] = bench_kmeans(args, torch, np, pp)
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -537,6 +541,40 @@ def bench_mlp(args, torch, np, pp):
     torch.cuda.empty_cache()
     return {"workload": "gpt2m_mlp_decode", "d": d, "d_ff": d_ff, "experts": E,
             "layer_copies": ncp, "points": res}
+
+
+def bench_kmeans(args, torch, np, pp):
+    """MoEfication's clustering at the LLaMA-3-8B split: the d_ff = 14336
+    neuron rows of D = 4096 (bf16, planted structure: centres N(0, 0.02^2)
+    plus N(0, 0.02^2) noise) into E = 112 balanced clusters of 128, 5 Lloyd
+    iterations from seeded initial rows, timed as one call (it blocks).
+    Reports ms per iteration, auction rounds per assignment, and the distance
+    GEMM's byte and flop rates (F read once, 3 bf16 MFMA passes)."""
+    import time
+    from paper_2605_28283_amd.workloads import bf16_to_f32, make_clustered_features
+    n, D, k, iters = 14336, 4096, 112, 5
+    F_bits, _, init_rows = make_clustered_features(n, D, k, 0)
+    F = torch.from_numpy(F_bits.view(np.int16)).cuda()
+    init = torch.from_numpy(bf16_to_f32(F_bits)[init_rows].copy()).cuda()
+    ws = torch.empty(pp.prunepath_kmeans_workspace(n, D, k), dtype=torch.uint8, device="cuda")
+    assign = torch.empty(n, dtype=torch.int32, device="cuda")
+    perm = torch.empty(n, dtype=torch.int32, device="cuda")
+    cent = torch.empty((k, D), dtype=torch.float32, device="cuda")
+    obj = torch.empty(iters, dtype=torch.float32, device="cuda")
+    pp.prunepath_balanced_kmeans(F, n, D, k, init, 1, assign, perm, cent, ws)  # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    rounds = pp.prunepath_balanced_kmeans(F, n, D, k, init, iters, assign, perm, cent, ws,
+                                          objective=obj)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3
+    o = obj.cpu().numpy().tolist()
+    print("# kmeans n=%d D=%d k=%d: %.2f ms for %d iterations (%.2f ms/iter), rounds %s, "
+          "objective %.4g -> %.4g" % (n, D, k, ms, iters, ms / iters, rounds, o[0], o[-1]),
+          file=sys.stderr, flush=True)
+    return {"workload": "kmeans_llama8b_dff14336_E112", "n": n, "D": D, "k": k, "iters": iters,
+            "ms_total": ms, "ms_per_iter": ms / iters, "rounds": rounds, "objective": o,
+            "dist_gemm_bytes": 2.0 * n * D, "dist_gemm_bf16_flops": 3 * 2.0 * n * k * D}
 
 
 def bench_loss(args, torch, np, pp):

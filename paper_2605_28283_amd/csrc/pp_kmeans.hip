@@ -48,7 +48,7 @@ constexpr int kKmCols = 64;            // columns of mu staged in LDS per chunk
 constexpr int kKmDistWaves = 8;        // km_dist_k: 8 wavefronts x 16 rows
 constexpr int kKmBidThreads = 256;
 constexpr int kKmPriceThreads = 256;
-constexpr int kKmAuctionRounds = 256;  // price rounds before the shortest-path finish
+constexpr int kKmAuctionRounds = 128;  // price rounds before the shortest-path finish
 constexpr int kKmBatch = 64;           // rounds enqueued between convergence checks
 constexpr int kKmSspThreads = 1024;
 
@@ -56,6 +56,7 @@ struct KmWork {
     float *S;            // [k][n] s_ij
     double *xnorm;       // [n]
     float *list;         // [k][n] margins (rounded up to fp32) of each cluster's rows
+    int32_t *memb;       // [k][n] the rows themselves (same order as list)
     double *lam;         // [k] cluster prices
     double *part;        // [bid workgroups] spread sums (eps scale)
     float *cn;           // [k] ||mu_j||^2
@@ -68,7 +69,7 @@ struct KmWork {
                          // [3] rounds the step took
 };
 
-inline int bid_blocks(int n) { return (n + kKmBidThreads - 1) / kKmBidThreads; }
+inline int bid_blocks(int n) { return (n + kKmBidThreads / 4 - 1) / (kKmBidThreads / 4); }
 
 size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
 
@@ -84,6 +85,7 @@ size_t km_layout(int n, int D, int k, KmWork *w, char *base) {
     t.S = reinterpret_cast<float *>(take(sizeof(float) * (size_t)k * n));
     t.xnorm = reinterpret_cast<double *>(take(sizeof(double) * n));
     t.list = reinterpret_cast<float *>(take(sizeof(float) * (size_t)k * n));
+    t.memb = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (size_t)k * n));
     t.lam = reinterpret_cast<double *>(take(sizeof(double) * k));
     t.part = reinterpret_cast<double *>(take(sizeof(double) * bid_blocks(n)));
     t.cn = reinterpret_cast<float *>(take(sizeof(float) * k));
@@ -227,20 +229,54 @@ __global__ void km_auction_init_k(int k, double *lam, int32_t *count, int32_t *f
     if (t < 4) flags[t] = 0;
 }
 
+// (best, its cluster, second best) of part of a row's clusters; merging two
+// parts gives the same result in any order: the better best wins (lower
+// cluster on equal values), the second is the larger of the kept second and
+// the other best.
+struct Best2 {
+    double w1, w2;
+    int j1;
+    float smin, smax;
+};
+__device__ __forceinline__ Best2 merge_best2(Best2 a, Best2 b) {
+    if (b.w1 > a.w1 || (b.w1 == a.w1 && b.j1 < a.j1)) {
+        const Best2 t = a;
+        a = b;
+        b = t;
+    }
+    a.w2 = fmax(a.w2, b.w1);
+    a.smin = fminf(a.smin, b.smin);
+    a.smax = fmaxf(a.smax, b.smax);
+    return a;
+}
+__device__ __forceinline__ Best2 shfl_best2(const Best2 &v, int st) {
+    Best2 o;
+    o.w1 = __shfl_xor(v.w1, st, 64);
+    o.w2 = __shfl_xor(v.w2, st, 64);
+    o.j1 = __shfl_xor(v.j1, st, 64);
+    o.smin = __shfl_xor(v.smin, st, 64);
+    o.smax = __shfl_xor(v.smax, st, 64);
+    return o;
+}
+
 // Round r, bids: every row's argmax j1 of w_ij = -s_ij - lambda_j (first
 // index on ties) and its margin w1 - w2 (w2 the best over the other
-// clusters), rounded up to fp32 and appended to cluster j1's margin list;
-// counts per cluster.  A row's k costs are loaded 16 at a time, all in flight
-// together, and folded in without branches.  Exits at once when the previous
-// round left no cluster over-full (the assignment then stands).
+// clusters), rounded up to fp32 and appended, with the row, to cluster j1's
+// lists; counts per cluster.  kBidLanes adjacent lanes share a row, each
+// taking every kBidLanes-th cluster with its loads 8 at a time in flight, and
+// their partial results are merged.  Exits at once when the previous round
+// left no cluster over-full (the assignment then stands).
+constexpr int kBidLanes = 4;
+constexpr int kBidRows = kKmBidThreads / kBidLanes;  // rows per workgroup
+
 __global__ __launch_bounds__(kKmBidThreads) void km_bid_k(const float *__restrict__ S, int n, int k,
                                                           int r, KmWork W,
                                                           int32_t *__restrict__ assign) {
-    constexpr int kBatch = 16;
+    constexpr int kBatch = 8;
     __shared__ double lam[kKmMaxK];
     __shared__ int cnt[kKmMaxK];
     __shared__ int base[kKmMaxK];
-    __shared__ double spread[kKmBidThreads];
+    __shared__ double spread[kBidRows];
     const int tid = threadIdx.x;
     if (W.flags[2]) return;
     if (r > 0 && W.flags[(r - 1) & 1] == 0) {
@@ -256,43 +292,50 @@ __global__ __launch_bounds__(kKmBidThreads) void km_bid_k(const float *__restric
         cnt[j] = 0;
     }
     __syncthreads();
-    const int i = blockIdx.x * kKmBidThreads + tid;
+    const int q = tid % kBidLanes, row = tid / kBidLanes;
+    const int i = blockIdx.x * kBidRows + row;
     const bool valid = i < n;
     const int ii = min(i, n - 1);
-    double w1 = -INFINITY, w2 = -INFINITY;
-    float smin = INFINITY, smax = -INFINITY;
-    int j1 = 0;
-    for (int j0 = 0; j0 < k; j0 += kBatch) {
+    Best2 v{-INFINITY, -INFINITY, 0x7FFFFFFF, INFINITY, -INFINITY};
+    for (int j0 = q; j0 < k; j0 += kBatch * kBidLanes) {
         float sv[kBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) sv[u] = S[(size_t)min(j0 + u, k - 1) * n + ii];
+        for (int u = 0; u < kBatch; ++u)
+            sv[u] = S[(size_t)min(j0 + u * kBidLanes, k - 1) * n + ii];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            if (j0 + u < k) {  // uniform across the workgroup
-                const double w = -(double)sv[u] - lam[j0 + u];
-                const bool b1 = w > w1;
-                w2 = b1 ? w1 : fmax(w2, w);
-                w1 = b1 ? w : w1;
-                j1 = b1 ? j0 + u : j1;
-                smin = fminf(smin, sv[u]);
-                smax = fmaxf(smax, sv[u]);
+            const int j = j0 + u * kBidLanes;
+            if (j < k) {
+                const double w = -(double)sv[u] - lam[j];
+                const bool b1 = w > v.w1;  // ascending j within a lane: first wins ties
+                v.w2 = b1 ? v.w1 : fmax(v.w2, w);
+                v.w1 = b1 ? w : v.w1;
+                v.j1 = b1 ? j : v.j1;
+                v.smin = fminf(v.smin, sv[u]);
+                v.smax = fmaxf(v.smax, sv[u]);
             }
         }
     }
+#pragma unroll
+    for (int st = 1; st < kBidLanes; st <<= 1) v = merge_best2(v, shfl_best2(v, st));
+    const bool lead = q == 0 && valid;
     int slot = 0;
-    if (valid) slot = atomicAdd(&cnt[j1], 1);
+    if (lead) slot = atomicAdd(&cnt[v.j1], 1);
     __syncthreads();
     for (int j = tid; j < k; j += kKmBidThreads) base[j] = cnt[j] ? atomicAdd(&W.count[j], cnt[j]) : 0;
     __syncthreads();
-    if (valid) {
-        const double mg = w1 - w2;  // +inf when k == 1
-        assign[i] = j1;
-        W.list[(size_t)j1 * n + base[j1] + slot] = isinf(mg) ? 3.0e38f : __double2float_ru(mg);
+    if (lead) {
+        const double mg = v.w1 - v.w2;  // +inf when k == 1
+        const int at = base[v.j1] + slot;
+        assign[i] = v.j1;
+        W.list[(size_t)v.j1 * n + at] = isinf(mg) ? 3.0e38f : __double2float_ru(mg);
+        W.memb[(size_t)v.j1 * n + at] = i;
+        W.pos[i] = at;
     }
     if (r == 0) {  // eps scale: sum of per-row spreads, fixed order
-        spread[tid] = valid ? (double)smax - (double)smin : 0.0;
+        if (q == 0) spread[row] = valid ? (double)v.smax - (double)v.smin : 0.0;
         __syncthreads();
-        for (int st = kKmBidThreads / 2; st >= 1; st >>= 1) {
+        for (int st = kBidRows / 2; st >= 1; st >>= 1) {
             if (tid < st) spread[tid] += spread[tid + st];
             __syncthreads();
         }
@@ -309,7 +352,9 @@ __global__ __launch_bounds__(kKmBidThreads) void km_bid_k(const float *__restric
 __global__ __launch_bounds__(kKmPriceThreads) void km_price_k(int n, int k, int m, int r,
                                                               int nbid, KmWork W) {
     constexpr int kBatch = 4;
+    static_assert(kKmPriceThreads == 256, "one thread per radix digit");
     __shared__ int hist[256];
+    __shared__ int scan[8];
     __shared__ uint32_t s_pref;
     __shared__ int s_rank;
     const int j = blockIdx.x, tid = threadIdx.x;
@@ -323,37 +368,38 @@ __global__ __launch_bounds__(kKmPriceThreads) void km_price_k(int n, int k, int 
         s_rank = m;  // 0-based rank from the top
     }
     const float *lst = W.list + (size_t)j * n;
-    uint32_t mask = 0u;
-    for (int pass = 0; pass < 4; ++pass) {
-        const int shift = 24 - 8 * pass;
-        hist[tid] = 0;
-        __syncthreads();
-        const uint32_t pref = s_pref;
-        for (int i0 = 0; i0 < c; i0 += kBatch * kKmPriceThreads) {
-            uint32_t v[kBatch];
-#pragma unroll
-            for (int u = 0; u < kBatch; ++u)
-                v[u] = __float_as_uint(lst[min(i0 + u * kKmPriceThreads + tid, c - 1)]);
-#pragma unroll
-            for (int u = 0; u < kBatch; ++u)
-                if (i0 + u * kKmPriceThreads + tid < c && (v[u] & mask) == pref)
-                    atomicAdd(&hist[(v[u] >> shift) & 255], 1);
-        }
-        __syncthreads();
-        if (tid == 0) {
-            int rank = s_rank, cum = 0, dsel = 0;
-            for (int dgt = 255; dgt >= 0; --dgt) {
-                if (cum + hist[dgt] > rank) {
-                    dsel = dgt;
-                    break;
-                }
-                cum += hist[dgt];
+    {
+        uint32_t mask = 0u;
+        for (int pass = 0; pass < 4; ++pass) {
+            const int shift = 24 - 8 * pass;
+            hist[tid] = 0;
+            __syncthreads();
+            const uint32_t pref = s_pref;
+            for (int i0 = 0; i0 < c; i0 += kBatch * kKmPriceThreads) {
+                uint32_t v[kBatch];
+    #pragma unroll
+                for (int u = 0; u < kBatch; ++u)
+                    v[u] = __float_as_uint(lst[min(i0 + u * kKmPriceThreads + tid, c - 1)]);
+    #pragma unroll
+                for (int u = 0; u < kBatch; ++u)
+                    if (i0 + u * kKmPriceThreads + tid < c && (v[u] & mask) == pref)
+                        atomicAdd(&hist[(v[u] >> shift) & 255], 1);
             }
-            s_rank = rank - cum;
-            s_pref = pref | ((uint32_t)dsel << shift);
+            __syncthreads();
+            {  // digits from the top: thread t takes digit 255 - t; the selected
+               // digit is where the running count first exceeds the rank
+                const int h = hist[255 - tid], rank = s_rank;
+                int ex, ex1, tot, tot1;
+                block_excl_scan2(h, 0, &ex, &ex1, &tot, &tot1, scan);
+                __syncthreads();
+                if (ex <= rank && rank < ex + h) {
+                    s_rank = rank - ex;
+                    s_pref = pref | ((uint32_t)(255 - tid) << shift);
+                }
+            }
+            mask |= 255u << shift;
+            __syncthreads();
         }
-        mask |= 255u << shift;
-        __syncthreads();
     }
     if (tid == 0) {
         double scale = 0.0;
@@ -402,52 +448,34 @@ __device__ void ssp_row(const float *__restrict__ S, int n, int k, int a, int na
     }
 }
 
+// All edge rows at once, one workgroup per cluster, from the member lists of
+// the bid round that precedes the finish (its argmax matches the prices).
+__global__ __launch_bounds__(kKmSspThreads) void km_ssp_rows_k(const float *__restrict__ S, int n,
+                                                               int k, KmWork W) {
+    ssp_row(S, n, k, blockIdx.x, W.count[blockIdx.x], W.memb, W.base, W.bidx);
+}
+
 // Shortest-path finish of an assignment step (one workgroup; every loop is
-// bounded by n, the largest possible excess).  Starts from the argmax
-// assignment of the current prices, then per augmentation: multi-source
-// Dijkstra from the over-full clusters over reduced costs
+// bounded by n, the largest possible excess).  Starts from the bid round's
+// argmax assignment, counts and member lists, then per augmentation:
+// multi-source Dijkstra from the over-full clusters over reduced costs
 // max(0, base[u][v] + lambda_v - lambda_u) until the first under-full
 // cluster t is settled; the path's rows move one edge each; lambda_v -=
 // min(dist_v, dist_t); the edge rows of the clusters on the path are
-// recomputed.  Sets flags[2] when balanced, flags[3] = augmentations.
+// recomputed.  Sets flags[2] when balanced, flags[3] = augmentations, and
+// clears the counts.
 __global__ __launch_bounds__(kKmSspThreads) void km_ssp_k(const float *__restrict__ S, int n, int k,
                                                           int m, KmWork W,
                                                           int32_t *__restrict__ assign) {
     __shared__ double lam[kKmMaxK], dist[kKmMaxK];
     __shared__ int cnt[kKmMaxK], pred[kKmMaxK], settled[kKmMaxK], chg[kKmMaxK];
     __shared__ int s_u, s_t, s_excess;
-    int32_t *memb = reinterpret_cast<int32_t *>(W.list);  // [k][n] member lists
+    int32_t *memb = W.memb;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     for (int j = tid; j < k; j += kKmSspThreads) {
         lam[j] = W.lam[j];
-        cnt[j] = 0;
+        cnt[j] = W.count[j];
     }
-    __syncthreads();
-    // argmax assignment for the current prices, member lists
-    for (int i = tid; i < n; i += kKmSspThreads) {
-        double w1 = -INFINITY;
-        int j1 = 0;
-        for (int j0 = 0; j0 < k; j0 += 16) {
-            float sv[16];
-#pragma unroll
-            for (int u = 0; u < 16; ++u) sv[u] = S[(size_t)min(j0 + u, k - 1) * n + i];
-#pragma unroll
-            for (int u = 0; u < 16; ++u) {
-                if (j0 + u < k) {
-                    const double w = -(double)sv[u] - lam[j0 + u];
-                    const bool b1 = w > w1;
-                    w1 = b1 ? w : w1;
-                    j1 = b1 ? j0 + u : j1;
-                }
-            }
-        }
-        assign[i] = j1;
-        const int t = atomicAdd(&cnt[j1], 1);
-        memb[(size_t)j1 * n + t] = i;
-        W.pos[i] = t;
-    }
-    __syncthreads();
-    for (int a = 0; a < k; ++a) ssp_row(S, n, k, a, cnt[a], memb, W.base, W.bidx);
     __syncthreads();
     int aug = 0;
     for (; aug <= n; ++aug) {
@@ -531,7 +559,10 @@ __global__ __launch_bounds__(kKmSspThreads) void km_ssp_k(const float *__restric
             if (chg[a]) ssp_row(S, n, k, a, cnt[a], memb, W.base, W.bidx);
         __syncthreads();
     }
-    for (int j = tid; j < k; j += kKmSspThreads) W.lam[j] = lam[j];
+    for (int j = tid; j < k; j += kKmSspThreads) {
+        W.lam[j] = lam[j];
+        W.count[j] = 0;
+    }
     if (tid == 0) {
         W.flags[2] = s_excess == 0 ? 1 : 0;
         W.flags[3] = aug;
@@ -656,6 +687,11 @@ extern "C" pp_status prunepath_balanced_kmeans(const uint16_t *F, int32_t n, int
             used = fl[2] != 0 ? fl[3] : r;
         }
         if (!done) {  // route the remaining excess by shortest paths
+            // one more bid round: the argmax, counts and member lists of the
+            // current prices (no price round follows it)
+            hipLaunchKernelGGL(km_bid_k, dim3(nbid), dim3(kKmBidThreads), 0, s, W.S, n, k, r, W,
+                               assign);
+            hipLaunchKernelGGL(km_ssp_rows_k, dim3(k), dim3(kKmSspThreads), 0, s, W.S, n, k, W);
             hipLaunchKernelGGL(km_ssp_k, dim3(1), dim3(kKmSspThreads), 0, s, W.S, n, k, m, W,
                                assign);
             int32_t fl[4];
