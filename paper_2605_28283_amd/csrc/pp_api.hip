@@ -56,6 +56,7 @@ void free_layer(pp_layer *L) {
     void *bufs[] = {L->Wr,     L->bias,  L->Wgu,     L->Wd,    L->bfc,   L->bproj, L->gpart, L->counters,
                     L->selmask, L->gsig, L->idx_tmp, L->cnt_tmp, L->abpart, L->h_hi,
                     L->h_lo,   L->ypart, L->ecount,  L->tokl,  L->plan,  L->dec_tok,
+                    L->pf_part, L->pf_ebase, L->pf_posq,
                     L->emask};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
@@ -187,6 +188,11 @@ pp_status create_layer(pp_layer **out, int32_t d, int32_t d_ff, int32_t E, int32
     chk(dev_alloc(&L->ypart, (size_t)kDecodeChunks * kDecodeTile * d));
     chk(dev_alloc(&L->ecount, (size_t)E));
     chk(dev_alloc(&L->tokl, (size_t)E * max_tokens));
+    L->pf_cap = kPfPartBytes / (sizeof(float) * (size_t)d);
+    if (L->pf_cap > (size_t)max_tokens * E) L->pf_cap = (size_t)max_tokens * E;
+    chk(dev_alloc(&L->pf_part, L->pf_cap * d));
+    chk(dev_alloc(&L->pf_ebase, (size_t)E));
+    chk(dev_alloc(&L->pf_posq, (size_t)max_tokens * E));
     chk(dev_alloc(&L->plan, (size_t)4 + 4 * (size_t)plan_max_groups(L->dm, max_tokens) + E + 1));
     chk(dev_alloc(&L->dec_tok, (size_t)kDecodeTile * E));
     chk(dev_alloc(&L->emask, (size_t)E));

@@ -14,9 +14,12 @@
 //   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
 //                 SiLU product of one group (shared with the decode kernel).
 //   down_pf_k   : unit = (expert, 256 rows); the expert's down block stays in
-//                 registers across its token groups; outputs are added into y
-//                 with fp32 atomics, 64 consecutive floats of one token row per
-//                 instruction.
+//                 registers across its token groups; each (token, expert)
+//                 pair's rows go to a pair-row buffer (pairs past its 1 GiB
+//                 capacity add into y with fp32 atomics).
+//   combine_pf_k: y[t] += t's pair rows, kept experts in ascending order --
+//                 no float atomics while the buffer holds every pair, so the
+//                 result is deterministic.
 // Units of one expert are placed on one XCD (shared weights or h in L2).
 #include "pp_gateup.h"
 
@@ -29,6 +32,8 @@ struct DNParams {
     const uint16_t *h_hi;
     const uint16_t *h_lo;
     float *y;
+    float *part;     // [cap][d] pair rows
+    size_t cap;
     PlanView plan;
 };
 
@@ -66,7 +71,9 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
                                                   int32_t *__restrict__ tokl, int stride,
                                                   float *__restrict__ y, size_t ny4,
                                                   const float *__restrict__ bproj, int d4,
-                                                  uint32_t *cnt, PlanView plan) {
+                                                  int32_t *__restrict__ posq,
+                                                  int32_t *__restrict__ ebase, uint32_t *cnt,
+                                                  PlanView plan) {
     __shared__ int scan[8];
     __shared__ int s_flag;
     const int e = blockIdx.x, tid = threadIdx.x;
@@ -85,7 +92,10 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
         const int f = (t < T && ((selmask[(size_t)t * 8 + w] >> b) & 1u)) ? 1 : 0;
         int ex, ex1, tot, tot1;
         block_excl_scan2(f, 0, &ex, &ex1, &tot, &tot1, scan);
-        if (f) tokl[(size_t)e * stride + base + ex] = t;
+        if (f) {
+            tokl[(size_t)e * stride + base + ex] = t;
+            posq[(size_t)t * E + e] = base + ex;
+        }
         base += tot;
     }
     if (tid == 0) st_dev_u32(reinterpret_cast<uint32_t *>(ecount + e), (uint32_t)base);
@@ -95,7 +105,10 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
     const int nch = (c + kGroupTokens - 1) / kGroupTokens;
     int cb, off, nG, npairs;
     block_excl_scan2(nch, c, &cb, &off, &nG, &npairs, scan);
-    if (tid < E) plan.egrp[tid] = cb;
+    if (tid < E) {
+        plan.egrp[tid] = cb;
+        ebase[tid] = off;
+    }
     if (tid == 0) plan.egrp[E] = nG;
     for (int ch = 0; ch < nch; ++ch) {
         const int g = cb + ch;
@@ -114,9 +127,11 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
 // 256 x 128 down block in registers (four 16-row tiles each, loaded once) and
 // run it over the expert's token groups of 64.  A group's h (hi and lo, MFMA B
 // order) is staged in LDS while the next group's is being loaded; the
-// 64 x 256 result is transposed through LDS so that each fp32 atomic add
-// instruction covers 64 consecutive floats of one token's row of y.  Units of
-// one expert share its h rows and go to the same XCD.
+// 64 x 256 result is transposed through LDS and stored as the pairs' rows
+// (each store instruction 64 consecutive floats of one pair's row), which
+// combine_pf_k sums per token.  Pairs past the buffer's capacity add into y
+// with fp32 atomics instead.  Units of one expert share its h rows and go to
+// the same XCD.
 constexpr int kPfRows = 256;
 __global__ __launch_bounds__(256, 2) void down_pf_k(DNParams P) {
     constexpr int MT = 4;
@@ -213,13 +228,76 @@ __global__ __launch_bounds__(256, 2) void down_pf_k(DNParams P) {
                             acc[mt][j][0], acc[mt][j][1], acc[mt][j][2], acc[mt][j][3]);
             }
             __syncthreads();
+            const int p0 = P.plan.grp_pair[g];
             for (int q = wv; q < n; q += 4) {
-                float *yr = P.y + (size_t)stok[q] * P.d + (size_t)rb * kPfRows;
+                const size_t pair = (size_t)(p0 + q);
+                if (pair < P.cap) {  // the pair's row, summed per token by combine_pf_k
+                    static_assert(kPfRows == 4 * 64, "one float4 per lane covers a row");
+                    float4 *pr = reinterpret_cast<float4 *>(P.part + pair * P.d + (size_t)rb * kPfRows);
+                    if (4 * lane < nrows) pr[lane] = *reinterpret_cast<const float4 *>(&S.y[q][4 * lane]);
+                } else {  // past the buffer: straight into y
+                    float *yr = P.y + (size_t)stok[q] * P.d + (size_t)rb * kPfRows;
 #pragma unroll
-                for (int c = 0; c < kPfRows / 64; ++c)
-                    if (64 * c + lane < nrows) atomicAdd(yr + 64 * c + lane, S.y[q][64 * c + lane]);
+                    for (int c = 0; c < kPfRows / 64; ++c)
+                        if (64 * c + lane < nrows) atomicAdd(yr + 64 * c + lane, S.y[q][64 * c + lane]);
+                }
             }
         }
+    }
+}
+
+// y[t] += the rows of t's pairs, kept experts in ascending order (a fixed
+// order: deterministic).  One workgroup per token: wavefront 0 lists the
+// token's pair rows in LDS (a ballot prefix over the expert bitmask), then
+// every thread sums its float4 columns with 8 rows in flight.  y holds the
+// output bias (or 0) and the atomic contributions of pairs past the buffer.
+__global__ __launch_bounds__(256) void combine_pf_k(const uint32_t *__restrict__ selmask, int T,
+                                                    int E, int d, const int32_t *__restrict__ posq,
+                                                    const int32_t *__restrict__ ebase,
+                                                    const float *__restrict__ part, size_t cap,
+                                                    float *__restrict__ y) {
+    constexpr int kBatch = 8;
+    __shared__ int plist[kMaxExperts];
+    __shared__ int s_k;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int t = blockIdx.x;
+    if (tid < 64) {
+        const uint32_t *sm = selmask + (size_t)t * 8;
+        int k = 0;
+        for (int e0 = 0; e0 < E; e0 += 64) {
+            const int e = e0 + lane;
+            const bool kept = e < E && ((sm[e >> 5] >> (e & 31)) & 1u);
+            const unsigned long long bal = __ballot(kept);
+            if (kept) {
+                const size_t pair = (size_t)ebase[e] + posq[(size_t)t * E + e];
+                plist[k + __popcll(bal & ((1ull << lane) - 1ull))] = pair < cap ? (int)pair : -1;
+            }
+            k += __popcll(bal);
+        }
+        if (lane == 0) s_k = k;
+    }
+    __syncthreads();
+    const int k = s_k;
+    for (int c4 = tid; c4 < d / 4; c4 += 256) {
+        float4 acc = reinterpret_cast<const float4 *>(y + (size_t)t * d)[c4];
+        for (int i0 = 0; i0 < k; i0 += kBatch) {
+            float4 v[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int p = plist[min(i0 + u, k - 1)];
+                v[u] = reinterpret_cast<const float4 *>(part + (size_t)max(p, 0) * d)[c4];
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                if (i0 + u < k && plist[i0 + u] >= 0) {
+                    acc.x += v[u].x;
+                    acc.y += v[u].y;
+                    acc.z += v[u].z;
+                    acc.w += v[u].w;
+                }
+            }
+        }
+        reinterpret_cast<float4 *>(y + (size_t)t * d)[c4] = acc;
     }
 }
 
@@ -234,6 +312,8 @@ DNParams dn_params(pp_layer *L, int T, float *y) {
     P.h_hi = L->h_hi;
     P.h_lo = L->h_lo;
     P.y = y;
+    P.part = L->pf_part;
+    P.cap = L->pf_cap;
     P.plan = plan_view(L, true);
     return P;
 }
@@ -257,7 +337,8 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     hipLaunchKernelGGL(dispatch_k, dim3(dm.E + L->num_cu), dim3(256), 0, s, L->selmask, T, dm.E,
                        L->ecount,
                        L->tokl, L->max_tokens, y, (size_t)T * dm.d / 4, L->bproj, dm.d / 4,
-                       L->counters + cl.dispatch_base(), plan_view(L, true));
+                       L->pf_posq, L->pf_ebase, L->counters + cl.dispatch_base(),
+                       plan_view(L, true));
     prof_mark(L, PP_KERNEL_DISPATCH, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
@@ -276,6 +357,8 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     static const int occ_dn = resident(down_pf_k, 256);
     prof_mark(L, PP_KERNEL_DOWN, s, true);
     hipLaunchKernelGGL(down_pf_k, dim3(occ_dn * L->num_cu), dim3(256), 0, s, dp);
+    hipLaunchKernelGGL(combine_pf_k, dim3(T), dim3(256), 0, s, L->selmask, T, dm.E, dm.d,
+                       L->pf_posq, L->pf_ebase, L->pf_part, L->pf_cap, y);
     prof_mark(L, PP_KERNEL_DOWN, s, false);
     return hipGetLastError();
 }

@@ -22,6 +22,7 @@ constexpr int kMinStepsPerSlice = 8;   // K-steps each gate/up K-slice covers at
 
 // Byte sizes of the scratch areas whose size does not follow from max_tokens.
 constexpr size_t kAbPartRows = 65536;  // K-split partial (a,b) rows of 256 floats
+constexpr size_t kPfPartBytes = (size_t)1 << 30;  // cap of the prefill pair-row buffer
 
 struct pp_dims {
     int d, d_ff, E, NS;      // NS = d / 32 K-steps
@@ -93,6 +94,10 @@ struct pp_layer {
     float *ypart;       // [kDecodeChunks][kDecodeTile][d] chunk partial outputs (decode, dense groups)
     int32_t *ecount;    // [E] tokens per expert (prefill)
     int32_t *tokl;      // [E][max_tokens] token ids per expert (prefill)
+    float *pf_part;     // prefill: [pf_cap][d] down-projection row of each (token, expert) pair
+    size_t pf_cap;      // pair rows pf_part holds (pairs past it add into y atomically)
+    int32_t *pf_ebase;  // prefill: [E] first pair row of each expert's bucket
+    int32_t *pf_posq;   // prefill: [max_tokens][E] a token's place in each kept expert's bucket
     int32_t *plan;      // PlanView storage: 4 + 4 * plan_max_groups + E + 1 ints
     int32_t *dec_tok;   // [64 * E] token ids of the decode plan, pair order
     unsigned long long *emask;  // [E] decode: tokens that kept each expert (zero between calls)

@@ -267,3 +267,15 @@ def test_qwen_skewed(oracle_mod):
         for tau in w.taus:
             res = parity(oracle_mod, dl, "decode", x, tau, it, rows=np.array([0, 21, 42, 63]))
             assert res["cnt"].min() >= 1
+
+
+def test_prefill_deterministic(oracle_mod, llama8b):
+    """Prefill sums each token's expert rows in a fixed order (no float
+    atomics while the pair-row buffer holds every pair): reruns give the same
+    bits."""
+    L, w, dl = llama8b
+    x, _ = make_tokens(300, w.d, 77, row_lognormal_sigma=0.5)
+    a = dl.run("prefill", x, 0.8)
+    b = dl.run("prefill", x, 0.8)
+    np.testing.assert_array_equal(a[2], b[2])
+    np.testing.assert_array_equal(a[0], b[0])
