@@ -46,7 +46,7 @@ struct DNParams {
 
 // ------------------------------------------------------------------ gate/up
 
-template <bool GATED>
+template <bool GATED, int NTMAX, int PF>
 __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     __shared__ uint4 xf[kXBufBytes / 16];
     __shared__ int stok[kGroupTokens];
@@ -82,8 +82,8 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         const unsigned long long m = D.mask[g];
         if (tid < 64 && ((m >> tid) & 1ull)) stok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
         __syncthreads();
-        gateup_group<GATED>(P, D.e[g], __popcll(m), D.pair[g], g, ks, ksg, npairs, stok, xf,
-                            &s_flag);
+        gateup_group<GATED, NTMAX, PF>(P, D.e[g], __popcll(m), D.pair[g], g, ks, ksg, npairs, stok,
+                                       xf, &s_flag);
         __syncthreads();
     }
 }
@@ -425,15 +425,33 @@ void launch_down_dec_tb(const DNParams &P, int num_cu, hipStream_t s) {
 
 }  // namespace
 
+// gate/up of a decode slice of T tokens: groups hold at most T tokens, so
+// the kernel is compiled for at most ceil(T / 16) token tiles, and the
+// registers the larger tiles would take go to a deeper weight prefetch.
+template <bool GATED, int NTMAX, int PF>
+void launch_gateup_dec(const GUParams &gp, int num_cu, hipStream_t s) {
+    static const int occ = resident(gateup_dec_k<GATED, NTMAX, PF>, kGuThreads);
+    hipLaunchKernelGGL((gateup_dec_k<GATED, NTMAX, PF>), dim3(occ * num_cu), dim3(kGuThreads), 0, s,
+                       gp);
+}
+
+template <bool GATED>
+void launch_gateup_dec_t(const GUParams &gp, int T, int num_cu, hipStream_t s) {
+    if (T <= 16)
+        launch_gateup_dec<GATED, 1, 3>(gp, num_cu, s);
+    else if (T <= 32)
+        launch_gateup_dec<GATED, 2, 3>(gp, num_cu, s);
+    else
+        launch_gateup_dec<GATED, 4, kPF>(gp, num_cu, s);
+}
+
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s) {
-    static const int occ_g = resident(gateup_dec_k<true>, kGuThreads);
-    static const int occ_p = resident(gateup_dec_k<false>, kGuThreads);
     const GUParams gp = gu_params(L, x, T, false);
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
     if (L->gated)
-        hipLaunchKernelGGL(gateup_dec_k<true>, dim3(occ_g * L->num_cu), dim3(kGuThreads), 0, s, gp);
+        launch_gateup_dec_t<true>(gp, T, L->num_cu, s);
     else
-        hipLaunchKernelGGL(gateup_dec_k<false>, dim3(occ_p * L->num_cu), dim3(kGuThreads), 0, s, gp);
+        launch_gateup_dec_t<false>(gp, T, L->num_cu, s);
     prof_mark(L, PP_KERNEL_GATEUP, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;

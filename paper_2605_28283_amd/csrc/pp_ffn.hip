@@ -59,7 +59,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
         const int p0 = P.plan.grp_pair[g];
         if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
         __syncthreads();
-        gateup_group<GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, &s_flag);
+        gateup_group<GATED, 4, kPF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, &s_flag);
         __syncthreads();
     }
 }

@@ -21,7 +21,7 @@ namespace {
 
 constexpr int kXBufBytes = 64 * 1024;
 constexpr int kGuThreads = 512;
-constexpr int kPF = 2;          // K-steps per register buffer in gateup_k (two buffers)
+constexpr int kPF = 2;          // K-steps per register buffer (two buffers) with up to 4 token tiles
 
 struct GUParams {
     const uint16_t *x;
@@ -87,23 +87,23 @@ __device__ __forceinline__ void stage_x(const GUParams &P, const int *stok, int 
 template <bool GATED>
 constexpr int kStepElems = GATED ? 1024 : 512;
 
-template <bool GATED>
-__device__ __forceinline__ void load_wgu(const uint16_t *wb, int step, int last, uint4 (&G)[kPF],
-                                         uint4 (&U)[kPF]) {
+template <bool GATED, int PF>
+__device__ __forceinline__ void load_wgu(const uint16_t *wb, int step, int last, uint4 (&G)[PF],
+                                         uint4 (&U)[PF]) {
 #pragma unroll
-    for (int i = 0; i < kPF; ++i) {
+    for (int i = 0; i < PF; ++i) {
         const uint16_t *p = wb + (size_t)min(step + i, last) * kStepElems<GATED>;
         G[i] = ldg16(p);
         if (GATED) U[i] = ldg16(p + 512);
     }
 }
 
-template <int NT, bool GATED>
+template <int NT, bool GATED, int PF>
 __device__ __forceinline__ void mfma_wgu(const uint4 *xf, int nsc, int sl0, int nvalid,
-                                         const uint4 (&G)[kPF], const uint4 (&U)[kPF],
+                                         const uint4 (&G)[PF], const uint4 (&U)[PF],
                                          f32x4 (&ag)[NT], f32x4 (&au)[NT], int lane) {
 #pragma unroll
-    for (int i = 0; i < kPF; ++i) {
+    for (int i = 0; i < PF; ++i) {
         if (i < nvalid) {
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
@@ -128,7 +128,9 @@ __device__ __forceinline__ float act(const GUParams &P, int e, int r, float a, f
     return gelu_tanh(a + P.bfc[e * kExpertWidth + r]);
 }
 
-template <int NT, bool GATED>
+// PF: K-steps per register buffer; two buffers alternate, so PF steps of
+// weights are in flight while the other PF are multiplied.
+template <int NT, bool GATED, int PF>
 __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int ks, int KS,
                             int npairs, const int *stok, uint4 *xf, int *flag) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -143,16 +145,17 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
     const uint16_t *wb = P.Wgu + (size_t)(e * 8 + wv) * P.NS * kStepElems<GATED> + lane * 8;
     for (int sc = s0; sc < s1; sc += nsc_max) {
         const int nsc = min(nsc_max, s1 - sc), last = sc + nsc - 1;
-        uint4 G0[kPF], U0[kPF], G1[kPF], U1[kPF];
-        load_wgu<GATED>(wb, sc, last, G0, U0);  // weights do not wait for the token staging
+        uint4 G0[PF], U0[PF], G1[PF], U1[PF];
+        load_wgu<GATED, PF>(wb, sc, last, G0, U0);  // weights do not wait for the token staging
         stage_x<NT>(P, stok, n, sc, nsc, xf);
         __syncthreads();
-        for (int b = 0; b < nsc; b += 2 * kPF) {
-            if (b + kPF < nsc) load_wgu<GATED>(wb, sc + b + kPF, last, G1, U1);
-            mfma_wgu<NT, GATED>(xf, nsc, b, min(kPF, nsc - b), G0, U0, ag, au, lane);
-            if (b + 2 * kPF < nsc) load_wgu<GATED>(wb, sc + b + 2 * kPF, last, G0, U0);
-            if (b + kPF < nsc)
-                mfma_wgu<NT, GATED>(xf, nsc, b + kPF, min(kPF, nsc - b - kPF), G1, U1, ag, au, lane);
+        for (int b = 0; b < nsc; b += 2 * PF) {
+            if (b + PF < nsc) load_wgu<GATED, PF>(wb, sc + b + PF, last, G1, U1);
+            mfma_wgu<NT, GATED, PF>(xf, nsc, b, min(PF, nsc - b), G0, U0, ag, au, lane);
+            if (b + 2 * PF < nsc) load_wgu<GATED, PF>(wb, sc + b + 2 * PF, last, G0, U0);
+            if (b + PF < nsc)
+                mfma_wgu<NT, GATED, PF>(xf, nsc, b + PF, min(PF, nsc - b - PF), G1, U1, ag, au,
+                                        lane);
         }
         __syncthreads();
     }
@@ -293,17 +296,22 @@ __device__ void decode_plan(const GUParams &P, DecodePlan &D) {
     __syncthreads();
 }
 
-// One group's gate/up unit, dispatched on its number of 16-token tiles.
-template <bool GATED>
+// One group's gate/up unit, dispatched on its number of 16-token tiles (at
+// most NTMAX: a kernel whose groups are known to be small is compiled without
+// the larger tiles' registers and spends them on a deeper weight prefetch PF).
+template <bool GATED, int NTMAX, int PF>
 __device__ __forceinline__ void gateup_group(const GUParams &P, int e, int n, int p0, int g,
                                              int ks, int KS, int npairs, const int *stok,
                                              uint4 *xf, int *flag) {
-    switch ((n + 15) >> 4) {
-    case 1: gateup_unit<1, GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
-    case 2: gateup_unit<2, GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
-    case 3: gateup_unit<3, GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
-    default: gateup_unit<4, GATED>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag); break;
-    }
+    const int nt = (n + 15) >> 4;
+    if (NTMAX >= 4 && nt >= 4)
+        gateup_unit<(NTMAX >= 4 ? 4 : 1), GATED, PF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+    else if (NTMAX >= 3 && nt == 3)
+        gateup_unit<(NTMAX >= 3 ? 3 : 1), GATED, PF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+    else if (NTMAX >= 2 && nt == 2)
+        gateup_unit<(NTMAX >= 2 ? 2 : 1), GATED, PF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+    else
+        gateup_unit<1, GATED, PF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
 }
 
 // K-slices per group: as many as keep all nG * KS units within `slots`
