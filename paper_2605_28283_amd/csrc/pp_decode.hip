@@ -9,7 +9,11 @@
 //                 SiLU product of one group (or the non-gated layer's input
 //                 projection, bias and GELU; code shared with prefill); the
 //                 K-split (one slice more for some groups) makes the units
-//                 fill the resident workgroups exactly, one round.
+//                 fill the resident workgroups exactly, one round.  Sparse
+//                 batches of up to 32 tokens with one to one and a half
+//                 16-neuron tiles per workgroup use neuron-tile units instead:
+//                 one tile over all of K per half workgroup, its K quarters
+//                 summed in LDS, so no partial sums pass between workgroups.
 //   down_dec_k  : sparse groups (<= 8 tokens per group on average): unit = one
 //                 16-row tile of d over all groups; each of the 8 wavefronts
 //                 takes every eighth group, tile by tile of 16 tokens (three
@@ -46,15 +50,175 @@ struct DNParams {
 
 // ------------------------------------------------------------------ gate/up
 
+// Neuron-tile units (sparse groups): unit = one 16-neuron tile of one group's
+// expert over all of K, taken by one half of the workgroup; wavefront q of
+// the half takes K quarter q, its token B fragments straight from x (a few
+// tokens, cache resident), the weights PF steps ahead in two register
+// buffers.  The four quarters' (a, b) are added in LDS in quarter order and
+// the half writes h for its 16 neurons: no partial sums leave the workgroup,
+// so no hand-off between workgroups.
+constexpr int kTileHalves = 2;      // units per workgroup at a time
+constexpr int kTileQuarters = 4;    // wavefronts per unit (K split)
+constexpr int kTilePF = 2;          // K-steps per register buffer (two buffers)
+constexpr int kTileMaxNT = 2;       // token tiles per unit (batches of up to 32 tokens)
+static_assert(kTileHalves * kTileQuarters * 64 == kGuThreads, "two halves of four wavefronts");
+static_assert(kTileHalves * kTileMaxNT * 2 * kTileQuarters * 64 * 16 <= kXBufBytes,
+              "the quarters' (a, b) of both halves fit in the token staging buffer");
+
+template <int NT, bool GATED, int PF>
+__device__ __forceinline__ void tile_load(const uint16_t *wb, const uint16_t *const (&xr)[NT],
+                                          int step, int last, uint4 (&G)[PF], uint4 (&U)[PF],
+                                          uint4 (&B)[PF][NT]) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+        const int s = min(step + i, last);
+        const uint16_t *p = wb + (size_t)s * kStepElems<GATED>;
+        G[i] = ldg16(p);
+        if (GATED) U[i] = ldg16(p + 512);
+#pragma unroll
+        for (int j = 0; j < NT; ++j) B[i][j] = ldg16(xr[j] + s * kKStep);
+    }
+}
+
+template <int NT, bool GATED, int PF>
+__device__ __forceinline__ void tile_mfma(int nvalid, const uint4 (&G)[PF], const uint4 (&U)[PF],
+                                          const uint4 (&B)[PF][NT], f32x4 (&ag)[NT],
+                                          f32x4 (&au)[NT]) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+        if (i < nvalid) {
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                ag[j] = mfma16(G[i], B[i][j], ag[j]);
+                if (GATED) au[j] = mfma16(U[i], B[i][j], au[j]);
+            }
+        }
+    }
+}
+
+// One wavefront's K quarter of a tile unit; leaves its (a, b) in red.
+template <int NT, bool GATED, int PF>
+__device__ __forceinline__ void tile_quarter(const GUParams &P, int e, int nt, int n,
+                                             const int *tok, int q, int lane, float4 *red) {
+    const int sA = q * P.NS / kTileQuarters, sB = (q + 1) * P.NS / kTileQuarters;
+    const uint16_t *wb = P.Wgu + (size_t)(e * 8 + nt) * P.NS * kStepElems<GATED> + lane * 8;
+    const uint16_t *xr[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        const int slot = 16 * j + (lane & 15);
+        // an empty slot reads the group's first token: it only feeds that
+        // slot's output column, which is never stored
+        xr[j] = P.x + (size_t)tok[slot < n ? slot : 0] * P.d + 8 * (lane >> 4);
+    }
+    f32x4 ag[NT], au[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        ag[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        au[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const int last = sB - 1;
+    uint4 G0[PF], U0[PF], G1[PF], U1[PF], B0[PF][NT], B1[PF][NT];
+    if (sA < sB) tile_load<NT, GATED, PF>(wb, xr, sA, last, G0, U0, B0);  // d < 128: a quarter may be empty
+    for (int s = sA; s < sB; s += 2 * PF) {
+        if (s + PF < sB) tile_load<NT, GATED, PF>(wb, xr, s + PF, last, G1, U1, B1);
+        tile_mfma<NT, GATED, PF>(min(PF, sB - s), G0, U0, B0, ag, au);
+        if (s + 2 * PF < sB) tile_load<NT, GATED, PF>(wb, xr, s + 2 * PF, last, G0, U0, B0);
+        if (s + PF < sB) tile_mfma<NT, GATED, PF>(min(PF, sB - s - PF), G1, U1, B1, ag, au);
+    }
+    // red[(j * 2 + {a, b}) * kTileQuarters + q][lane]
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        red[((j * 2 + 0) * kTileQuarters + q) * 64 + lane] = make_float4(ag[j][0], ag[j][1], ag[j][2], ag[j][3]);
+        red[((j * 2 + 1) * kTileQuarters + q) * 64 + lane] = make_float4(au[j][0], au[j][1], au[j][2], au[j][3]);
+    }
+}
+
+// h of a tile unit from the four quarters, summed in quarter order; wavefront
+// j of the half takes token tile j.
+template <int NT, bool GATED>
+__device__ __forceinline__ void tile_epilogue(const GUParams &P, int e, int nt, int n, int p0,
+                                              const int *tok, int j, int lane, const float4 *red) {
+    const int qs = 16 * j + (lane & 15);
+    if (j >= NT || qs >= n) return;
+    float4 a = red[((j * 2 + 0) * kTileQuarters + 0) * 64 + lane];
+    float4 b = red[((j * 2 + 1) * kTileQuarters + 0) * 64 + lane];
+#pragma unroll
+    for (int q = 1; q < kTileQuarters; ++q) {
+        const float4 pa = red[((j * 2 + 0) * kTileQuarters + q) * 64 + lane];
+        const float4 pb = red[((j * 2 + 1) * kTileQuarters + q) * 64 + lane];
+        a.x += pa.x; a.y += pa.y; a.z += pa.z; a.w += pa.w;
+        b.x += pb.x; b.y += pb.y; b.z += pb.z; b.w += pb.w;
+    }
+    const bool sig = (P.flags & PP_AGG_SIGMOID) != 0;
+    const float scl = sig ? P.gsig[(size_t)tok[qs] * P.E + e] : 1.0f;
+    const int r0 = nt * 16 + 4 * (lane >> 4);
+    const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+    uint16_t hi[4], lo[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) split_bf16(act<GATED>(P, e, r0 + i, av[i], bv[i]) * scl, hi[i], lo[i]);
+    const size_t row = (size_t)(p0 + qs) * kExpertWidth + r0;
+    *reinterpret_cast<uint2 *>(P.h_hi + row) =
+        make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+    *reinterpret_cast<uint2 *>(P.h_lo + row) =
+        make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+}
+
+// All tile units of the plan: half h of workgroup b takes units b + h * grid,
+// then the next 2 * grid, ...; barriers stay outside the per-half work so
+// that both halves meet them whether or not they hold a unit.  A unit of a
+// group with more than 16 tokens takes two token tiles (and one K-step per
+// register buffer, which keeps the kernel within its registers).
+template <bool GATED>
+__device__ void tile_units(const GUParams &P, const DecodePlan &D, int *tokh, float4 *red) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int half = wv / kTileQuarters, q = wv % kTileQuarters;
+    const int units = D.nG * 8, grid = (int)gridDim.x;
+    int *tok = tokh + half * kGroupTokens;
+    float4 *rh = red + half * (kTileMaxNT * 2 * kTileQuarters * 64);
+    for (int base = 0; base < units; base += kTileHalves * grid) {
+        const int u = base + half * grid + (int)blockIdx.x;
+        const bool act = u < units;
+        const int g = act ? u >> 3 : 0, nt = u & 7;
+        const unsigned long long m = D.mask[g];
+        const int n = __popcll(m);
+        if (act && q == 0 && ((m >> lane) & 1ull)) tok[__popcll(m & ((1ull << lane) - 1ull))] = lane;
+        __syncthreads();
+        if (act) {
+            if (n <= 16)
+                tile_quarter<1, GATED, kTilePF>(P, D.e[g], nt, n, tok, q, lane, rh);
+            else
+                tile_quarter<2, GATED, 1>(P, D.e[g], nt, n, tok, q, lane, rh);
+        }
+        __syncthreads();
+        if (act) {
+            if (n <= 16)
+                tile_epilogue<1, GATED>(P, D.e[g], nt, n, D.pair[g], tok, q, lane, rh);
+            else
+                tile_epilogue<2, GATED>(P, D.e[g], nt, n, D.pair[g], tok, q, lane, rh);
+        }
+        __syncthreads();
+    }
+}
+
 template <bool GATED, int NTMAX, int PF>
 __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     __shared__ uint4 xf[kXBufBytes / 16];
-    __shared__ int stok[kGroupTokens];
+    __shared__ int stok[kTileHalves * kGroupTokens];
     __shared__ int s_flag;
     __shared__ DecodePlan D;
     const int tid = threadIdx.x;
     decode_plan<true>(P, D);
     const int nG = D.nG, npairs = D.npairs;
+    // Sparse groups (at most 4 tokens per group on average) and between one
+    // and one and a half neuron tiles per workgroup: neuron-tile units, no K
+    // split (with more tiles, workgroups holding two units form a tail).
+    // Batches of up to 32 tokens, so at most two token tiles per group, read
+    // from x directly; the 64-token kernel keeps its registers for the K split.
+    const int tiles = nG * 8, grid = (int)gridDim.x;
+    if (NTMAX <= 2 && tiles >= grid && 2 * tiles <= 3 * grid && npairs <= 4 * nG) {
+        tile_units<GATED>(P, D, stok, reinterpret_cast<float4 *>(xf));
+        return;
+    }
     // K-slices: KS per group, and one more for the first `extra` groups, so
     // that the units fill the resident workgroups exactly -- every CU then
     // streams the same number of units (with units left over, the CUs that
