@@ -163,41 +163,84 @@ __device__ __forceinline__ void tile_epilogue(const GUParams &P, int e, int nt, 
         make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
 }
 
-// All tile units of the plan: half h of workgroup b takes units b + h * grid,
-// then the next 2 * grid, ...; barriers stay outside the per-half work so
-// that both halves meet them whether or not they hold a unit.  A unit of a
-// group with more than 16 tokens takes two token tiles (and one K-step per
-// register buffer, which keeps the kernel within its registers).
+// Sum of one int per thread over the kGuThreads threads, returned to every
+// thread; `sm` (16-byte aligned) holds one int per wavefront and is free
+// again after the caller's next barrier.
+__device__ __forceinline__ int block_sum(int v, int *sm) {
+    static_assert(kGuThreads == 512, "eight wavefront sums, read as two int4");
+    const int wv = threadIdx.x >> 6;
+    const int w = __builtin_amdgcn_readlane(wave_scan_i32(v), 63);
+    if ((threadIdx.x & 63) == 0) sm[wv] = w;
+    __syncthreads();
+    const int4 a = reinterpret_cast<const int4 *>(sm)[0], b = reinterpret_cast<const int4 *>(sm)[1];
+    return ((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w));
+}
+
+// Position of the n-th (from 0) set bit of w, which has more than n set bits.
+__device__ __forceinline__ int nth_set_bit(unsigned long long w, int n) {
+    int pos = 0;
+#pragma unroll
+    for (int sh = 32; sh >= 1; sh >>= 1) {
+        const int c = __popcll(w & ((1ull << sh) - 1ull));
+        if (n >= c) {
+            n -= c;
+            w >>= sh;
+            pos += sh;
+        }
+    }
+    return pos;
+}
+
+// Tile units without the batch plan: the kept experts come as bitmask words
+// (word i: experts 64 i .. 64 i + 63), unit u is tile u % 8 of the
+// (u / 8)-th kept expert, found by popcounts, so a workgroup's weights
+// stream once it has the words; the unit's first pair row (tokens of the
+// kept experts before it) is a wavefront sum of mask popcounts at the end,
+// and workgroup 0 stores the batch plan for the down projection after its
+// units.  Half h of workgroup b takes units b + h * grid, then the next
+// 2 * grid, ... (every workgroup one unit before any takes two); barriers
+// stay outside the per-half work, so both halves meet them whether or not
+// they hold a unit.  A unit of a group with more than 16 tokens takes two
+// token tiles (and one K-step per register buffer, which keeps the kernel
+// within its registers).
 template <bool GATED>
-__device__ void tile_units(const GUParams &P, const DecodePlan &D, int *tokh, float4 *red) {
+__device__ void tile_units_bits(const GUParams &P, DecodePlan &D, unsigned long long m_own,
+                                const unsigned long long *s_mask,
+                                const unsigned long long *kept, int nG, int *tokh, float4 *red) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int half = wv / kTileQuarters, q = wv % kTileQuarters;
-    const int units = D.nG * 8, grid = (int)gridDim.x;
+    const int units = nG * 8, grid = (int)gridDim.x;
     int *tok = tokh + half * kGroupTokens;
     float4 *rh = red + half * (kTileMaxNT * 2 * kTileQuarters * 64);
     for (int base = 0; base < units; base += kTileHalves * grid) {
         const int u = base + half * grid + (int)blockIdx.x;
         const bool act = u < units;
-        const int g = act ? u >> 3 : 0, nt = u & 7;
-        const unsigned long long m = D.mask[g];
+        int g = act ? u >> 3 : 0, wi = 0;
+        while (wi < kMaxExperts / 64 - 1 && g >= __popcll(kept[wi])) g -= __popcll(kept[wi++]);
+        const int e = act ? 64 * wi + nth_set_bit(kept[wi], g) : 0, nt = u & 7;
+        const unsigned long long m = s_mask[e];
         const int n = __popcll(m);
         if (act && q == 0 && ((m >> lane) & 1ull)) tok[__popcll(m & ((1ull << lane) - 1ull))] = lane;
         __syncthreads();
         if (act) {
             if (n <= 16)
-                tile_quarter<1, GATED, kTilePF>(P, D.e[g], nt, n, tok, q, lane, rh);
+                tile_quarter<1, GATED, kTilePF>(P, e, nt, n, tok, q, lane, rh);
             else
-                tile_quarter<2, GATED, 1>(P, D.e[g], nt, n, tok, q, lane, rh);
+                tile_quarter<2, GATED, 1>(P, e, nt, n, tok, q, lane, rh);
         }
         __syncthreads();
-        if (act) {
+        if (act && q < ((n + 15) >> 4)) {
+            int c = 0;
+            for (int e2 = lane; e2 < e; e2 += 64) c += __popcll(s_mask[e2]);
+            const int p0 = __builtin_amdgcn_readlane(wave_scan_i32(c), 63);
             if (n <= 16)
-                tile_epilogue<1, GATED>(P, D.e[g], nt, n, D.pair[g], tok, q, lane, rh);
+                tile_epilogue<1, GATED>(P, e, nt, n, p0, tok, q, lane, rh);
             else
-                tile_epilogue<2, GATED>(P, D.e[g], nt, n, D.pair[g], tok, q, lane, rh);
+                tile_epilogue<2, GATED>(P, e, nt, n, p0, tok, q, lane, rh);
         }
         __syncthreads();
     }
+    if (blockIdx.x == 0) decode_plan<true>(P, D, m_own);
 }
 
 template <bool GATED, int NTMAX, int PF>
@@ -206,19 +249,35 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     __shared__ int stok[kTileHalves * kGroupTokens];
     __shared__ int s_flag;
     __shared__ DecodePlan D;
+    __shared__ unsigned long long s_mask[kMaxExperts];
+    __shared__ unsigned long long s_kept[kMaxExperts / 64];
+    __shared__ __align__(16) int s_sum[kGuThreads / 64];
     const int tid = threadIdx.x;
-    decode_plan<true>(P, D);
-    const int nG = D.nG, npairs = D.npairs;
+    const unsigned long long m_own = tid < P.E ? P.emask[tid] : 0ull;
+    if (tid < kMaxExperts) s_mask[tid] = m_own;
+    {
+        const unsigned long long kb = __ballot(m_own != 0ull);
+        if (tid < kMaxExperts && (tid & 63) == 0) s_kept[tid >> 6] = kb;
+    }
+    const int grid = (int)gridDim.x;
     // Sparse groups (at most 4 tokens per group on average) and between one
     // and one and a half neuron tiles per workgroup: neuron-tile units, no K
     // split (with more tiles, workgroups holding two units form a tail).
     // Batches of up to 32 tokens, so at most two token tiles per group, read
     // from x directly; the 64-token kernel keeps its registers for the K split.
-    const int tiles = nG * 8, grid = (int)gridDim.x;
-    if (NTMAX <= 2 && tiles >= grid && 2 * tiles <= 3 * grid && npairs <= 4 * nG) {
-        tile_units<GATED>(P, D, stok, reinterpret_cast<float4 *>(xf));
-        return;
+    if (NTMAX <= 2) {
+        // kept experts and pairs in one block sum: (pairs << 10) + experts
+        const int packed = block_sum((m_own != 0ull ? 1 : 0) + (__popcll(m_own) << 10), s_sum);
+        const int nG = packed & 1023, npairs = packed >> 10;
+        const int tiles = nG * 8;
+        if (tiles >= grid && 2 * tiles <= 3 * grid && npairs <= 4 * nG) {
+            tile_units_bits<GATED>(P, D, m_own, s_mask, s_kept, nG, stok,
+                                   reinterpret_cast<float4 *>(xf));
+            return;
+        }
     }
+    decode_plan<true>(P, D, m_own);
+    const int nG = D.nG, npairs = D.npairs;
     // K-slices: KS per group, and one more for the first `extra` groups, so
     // that the units fill the resident workgroups exactly -- every CU then
     // streams the same number of units (with units left over, the CUs that

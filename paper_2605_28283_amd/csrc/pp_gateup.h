@@ -264,10 +264,10 @@ struct DecodePlan {
     int nG, npairs;
 };
 
+// m: this thread's expert's token mask (P.emask[threadIdx.x], 0 past E).
 template <bool GLOBAL>
-__device__ void decode_plan(const GUParams &P, DecodePlan &D) {
+__device__ void decode_plan(const GUParams &P, DecodePlan &D, unsigned long long m) {
     const int tid = threadIdx.x, e = tid;
-    const unsigned long long m = (e < P.E) ? P.emask[e] : 0ull;
     const int act = m != 0ull ? 1 : 0, pc = __popcll(m);
     int slot, poff, nG, npairs;
     block_excl_scan2(act, pc, &slot, &poff, &nG, &npairs, D.scan);

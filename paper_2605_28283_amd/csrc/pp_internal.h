@@ -276,6 +276,17 @@ __device__ __forceinline__ float wave_scan_f32(float x) {
     return x;
 }
 
+// The same DPP prefix sum for one int per lane.
+__device__ __forceinline__ int wave_scan_i32(int x) {
+    x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x111, 0xF, 0xF, false);
+    x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x112, 0xF, 0xF, false);
+    x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x114, 0xF, 0xF, false);
+    x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x118, 0xF, 0xF, false);
+    x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x142, 0xA, 0xF, false);
+    x += (int)__builtin_amdgcn_update_dpp(0u, (uint32_t)x, 0x143, 0xC, 0xF, false);
+    return x;
+}
+
 __device__ __forceinline__ float lane_value(float x, int lane) {
     return __uint_as_float(__builtin_amdgcn_readlane(__float_as_uint(x), lane));
 }
