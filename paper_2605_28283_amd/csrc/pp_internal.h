@@ -292,15 +292,7 @@ __device__ __forceinline__ float lane_value(float x, int lane) {
 }
 
 // Inclusive scan of one int per lane across a 64-lane wavefront.
-__device__ __forceinline__ int wave_incl_scan(int v) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        int n = __shfl_up(v, o, 64);
-        if (lane >= o) v += n;
-    }
-    return v;
-}
+__device__ __forceinline__ int wave_incl_scan(int v) { return wave_scan_i32(v); }
 
 // Exclusive scan over a block of nthreads (multiple of 64, <= 1024) for two
 // ints at once.  `sm` needs 2 * (nthreads/64) ints of shared memory.  Returns
@@ -308,20 +300,22 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 __device__ __forceinline__ void block_excl_scan2(int v0, int v1, int *e0, int *e1, int *tot0,
                                                  int *tot1, int *sm) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    int i0 = wave_incl_scan(v0), i1 = wave_incl_scan(v1);
+    const int i0 = wave_incl_scan(v0), i1 = wave_incl_scan(v1);
     if (lane == 63) {
         sm[wv] = i0;
         sm[nw + wv] = i1;
     }
     __syncthreads();
     int b0 = 0, b1 = 0, t0 = 0, t1 = 0;
-    for (int w = 0; w < nw; ++w) {
-        if (w < wv) {
-            b0 += sm[w];
-            b1 += sm[nw + w];
+#pragma unroll
+    for (int w = 0; w < 16; ++w) {
+        if (w < nw) {  // uniform: all of the wavefront totals are read at once
+            const int a = sm[w], c = sm[nw + w];
+            b0 += w < wv ? a : 0;
+            b1 += w < wv ? c : 0;
+            t0 += a;
+            t1 += c;
         }
-        t0 += sm[w];
-        t1 += sm[nw + w];
     }
     *e0 = b0 + i0 - v0;
     *e1 = b1 + i1 - v1;
