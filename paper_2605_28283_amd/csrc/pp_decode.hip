@@ -602,7 +602,7 @@ __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
     for (int rt = blockIdx.x * R; rt < RT; rt += gridDim.x * R) {
         for (int i = lane; i < P.T * YS; i += 64) acc[i / YS][i % YS] = 0.0f;
         RowCursor c;
-        c.u = wv;
+        c.u = __builtin_amdgcn_readfirstlane(wv);
         c.j = 0;
         c.n = 0;
         c.stride = NW;
