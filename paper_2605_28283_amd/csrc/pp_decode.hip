@@ -32,6 +32,7 @@ namespace {
 
 constexpr int kDnThreads = 512;    // down projection: 8 wavefronts per workgroup
 constexpr int kDnR = 1;            // 16-row tiles per down item (sparse groups)
+constexpr int kDnRing = 4;         // sparse groups: items per wavefront ring (three in flight)
 constexpr int kShRows = 128;       // dense groups: rows per unit (8 wavefronts x 16)
 constexpr int kShYS = kShRows + 4;
 constexpr int kShTiles = kDecodeTile / 16;
@@ -608,19 +609,20 @@ __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
         c.stride = NW;
         c.nU = nU;
         c.enter(P.plan);
-        RowItem<R> I0, I1, I2;
-        load_row_item<R>(P, c, rt, RT, lane, I0);
-        load_row_item<R>(P, c, rt, RT, lane, I1);
-        for (;;) {
-            if (!I0.live) break;
-            load_row_item<R>(P, c, rt, RT, lane, I2);
-            apply_row_item<R, YS>(I0, lane, acc);
-            if (!I1.live) break;
-            load_row_item<R>(P, c, rt, RT, lane, I0);
-            apply_row_item<R, YS>(I1, lane, acc);
-            if (!I2.live) break;
-            load_row_item<R>(P, c, rt, RT, lane, I1);
-            apply_row_item<R, YS>(I2, lane, acc);
+        // ring of kDnRing items: the next item's loads go out before each apply
+        RowItem<R> it[kDnRing];
+#pragma unroll
+        for (int q = 0; q < kDnRing - 1; ++q) load_row_item<R>(P, c, rt, RT, lane, it[q]);
+        for (bool more = true; more;) {
+#pragma unroll
+            for (int q = 0; q < kDnRing; ++q) {
+                if (!it[q].live) {
+                    more = false;
+                    break;
+                }
+                load_row_item<R>(P, c, rt, RT, lane, it[(q + kDnRing - 1) % kDnRing]);
+                apply_row_item<R, YS>(it[q], lane, acc);
+            }
         }
         __syncthreads();
         for (int i = tid; i < P.T * 16 * R; i += blockDim.x) {
