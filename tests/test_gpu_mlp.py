@@ -68,6 +68,24 @@ def test_mlp_comparison_rules(oracle_mod, mode):
         np.testing.assert_array_equal(res["y"], np.tile(L.b_proj, (33, 1)))
 
 
+@pytest.mark.parametrize("T", [24, 32])
+def test_mlp_neuron_tile_units(oracle_mod, T):
+    """The non-gated layer on the neuron-tile gate/up units (sparse batch,
+    64..96 kept experts of 96 on a 256-CU MI355X): top-6 with expert 0 forced
+    into every selection (a group of T > 16 tokens, two token tiles), input
+    bias per neuron, output bias once per token; against the oracle."""
+    L = make_mlp_layer(1024, 96 * 128, 96, 82)
+    L.bias = np.zeros(96, np.float32)
+    L.bias[0] = 40.0
+    x, _ = make_tokens(T, 1024, 82 + T)
+    with DevLayer(L, 64, flags=TOPK | SIG) as dl:
+        res = parity(oracle_mod, dl, "decode", x, 6.0)
+        assert (res["idx"][:, 0] == 0).all()
+        kept = len(set(res["idx"][:, :6].ravel().tolist()))
+        print("mlp neuron tiles T=%d: %d kept experts" % (T, kept), flush=True)
+        assert 64 <= kept <= 96
+
+
 @pytest.fixture(scope="module")
 def gpt2m():
     w = WORKLOADS["gpt2m_decode"]

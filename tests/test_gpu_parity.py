@@ -140,19 +140,21 @@ def test_decode_down_modes_ragged_rows(oracle_mod):
                 np.testing.assert_array_equal(a["y"], b[2])  # deterministic
 
 
+@pytest.mark.parametrize("flags", [TOPK, TOPK | SIG])
 @pytest.mark.parametrize("T", [24, 32])
-def test_decode_neuron_tile_units(oracle_mod, T):
+def test_decode_neuron_tile_units(oracle_mod, T, flags):
     """Decode batches whose plan takes the neuron-tile gate/up units on a
     256-CU MI355X (sparse groups, between one and one and a half 16-neuron
     tiles per workgroup: 64..96 kept experts): top-6 of 96 experts with
     expert 0 forced into every token's selection by its router bias, so one
     group spans two token tiles (more than 16 tokens) and the others are
-    small (70 and 82 kept experts); against the oracle, deterministic."""
+    small (70 and 82 kept experts); with the sum and the sigmoid-weighted
+    aggregation; against the oracle, deterministic."""
     L = make_layer(1024, 96 * 128, 96, 51)
     L.bias = np.zeros(96, np.float32)
     L.bias[0] = 40.0
     x, _ = make_tokens(T, 1024, 52 + T)
-    with DevLayer(L, 64, flags=TOPK) as dl:
+    with DevLayer(L, 64, flags=flags) as dl:
         a = parity(oracle_mod, dl, "decode", x, 6.0)
         assert (a["idx"][:, 0] == 0).all()
         kept = len(set(a["idx"][:, :6].ravel().tolist()))
