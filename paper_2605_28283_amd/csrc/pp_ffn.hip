@@ -249,14 +249,16 @@ __global__ __launch_bounds__(256, 2) void down_pf_k(DNParams P) {
 // y[t] += the rows of t's pairs, kept experts in ascending order (a fixed
 // order: deterministic).  One workgroup per token: wavefront 0 lists the
 // token's pair rows in LDS (a ballot prefix over the expert bitmask), then
-// every thread sums its float4 columns with 8 rows in flight.  y holds the
+// every thread sums its four float4 columns, eight rows at a time with all
+// of a batch's loads in flight.  y holds the
 // output bias (or 0) and the atomic contributions of pairs past the buffer.
 __global__ __launch_bounds__(256) void combine_pf_k(const uint32_t *__restrict__ selmask, int T,
                                                     int E, int d, const int32_t *__restrict__ posq,
                                                     const int32_t *__restrict__ ebase,
                                                     const float *__restrict__ part, size_t cap,
                                                     float *__restrict__ y) {
-    constexpr int kBatch = 8;
+    constexpr int kBatch = 8;   // pair rows in flight
+    constexpr int kChunks = 4;  // float4 columns per thread and row (d = 4096 in one pass)
     __shared__ int plist[kMaxExperts];
     __shared__ int s_k;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -277,27 +279,43 @@ __global__ __launch_bounds__(256) void combine_pf_k(const uint32_t *__restrict__
         if (lane == 0) s_k = k;
     }
     __syncthreads();
-    const int k = s_k;
-    for (int c4 = tid; c4 < d / 4; c4 += 256) {
-        float4 acc = reinterpret_cast<const float4 *>(y + (size_t)t * d)[c4];
-        for (int i0 = 0; i0 < k; i0 += kBatch) {
-            float4 v[kBatch];
+    const int k = s_k, d4 = d / 4;
+    float4 *yt = reinterpret_cast<float4 *>(y + (size_t)t * d);
+    // a thread's kChunks float4 columns of kBatch rows are all in flight at once
+    for (int c0 = 0; c0 < d4; c0 += kChunks * 256) {
+        float4 acc[kChunks];
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                const int p = plist[min(i0 + u, k - 1)];
-                v[u] = reinterpret_cast<const float4 *>(part + (size_t)max(p, 0) * d)[c4];
+        for (int u = 0; u < kChunks; ++u) {
+            const int c4 = c0 + tid + 256 * u;
+            acc[u] = c4 < d4 ? yt[c4] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        for (int i0 = 0; i0 < k; i0 += kBatch) {
+            float4 v[kBatch][kChunks];
+#pragma unroll
+            for (int r = 0; r < kBatch; ++r) {
+                const float4 *row =
+                    reinterpret_cast<const float4 *>(part + (size_t)max(plist[min(i0 + r, k - 1)], 0) * d);
+#pragma unroll
+                for (int u = 0; u < kChunks; ++u) v[r][u] = row[min(c0 + tid + 256 * u, d4 - 1)];
             }
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                if (i0 + u < k && plist[i0 + u] >= 0) {
-                    acc.x += v[u].x;
-                    acc.y += v[u].y;
-                    acc.z += v[u].z;
-                    acc.w += v[u].w;
+            for (int r = 0; r < kBatch; ++r) {
+                if (i0 + r < k && plist[i0 + r] >= 0) {
+#pragma unroll
+                    for (int u = 0; u < kChunks; ++u) {
+                        acc[u].x += v[r][u].x;
+                        acc[u].y += v[r][u].y;
+                        acc[u].z += v[r][u].z;
+                        acc[u].w += v[r][u].w;
+                    }
                 }
             }
         }
-        reinterpret_cast<float4 *>(y + (size_t)t * d)[c4] = acc;
+#pragma unroll
+        for (int u = 0; u < kChunks; ++u) {
+            const int c4 = c0 + tid + 256 * u;
+            if (c4 < d4) yt[c4] = acc[u];
+        }
     }
 }
 
