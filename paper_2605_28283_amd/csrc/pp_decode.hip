@@ -10,8 +10,8 @@
 //                 projection, bias and GELU; code shared with prefill); the
 //                 K-split (one slice more for some groups) makes the units
 //                 fill the resident workgroups exactly, one round.  Sparse
-//                 batches of up to 32 tokens with one to one and a half
-//                 16-neuron tiles per workgroup use neuron-tile units instead:
+//                 batches (groups of up to 32 tokens) with one to one and a
+//                 half 16-neuron tiles per workgroup use neuron-tile units:
 //                 one tile over all of K per half workgroup, its K quarters
 //                 summed in LDS, so no partial sums pass between workgroups.
 //   down_dec_k  : sparse groups (<= 8 tokens per group on average): unit = one
@@ -264,14 +264,16 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     // Sparse groups (at most 4 tokens per group on average) and between one
     // and one and a half neuron tiles per workgroup: neuron-tile units, no K
     // split (with more tiles, workgroups holding two units form a tail).
-    // Batches of up to 32 tokens, so at most two token tiles per group, read
-    // from x directly; the 64-token kernel keeps its registers for the K split.
-    if (NTMAX <= 2) {
-        // kept experts and pairs in one block sum: (pairs << 10) + experts
+    // At most two token tiles per group (groups of up to 32 tokens), read from
+    // x directly.
+    {
+        // kept experts and pairs in one block sum: (pairs << 10) + experts,
+        // and whether a group spans more than two token tiles
+        const int over32 = NTMAX > 2 ? __syncthreads_or(__popcll(m_own) > 32) : 0;
         const int packed = block_sum((m_own != 0ull ? 1 : 0) + (__popcll(m_own) << 10), s_sum);
         const int nG = packed & 1023, npairs = packed >> 10;
         const int tiles = nG * 8;
-        if (tiles >= grid && 2 * tiles <= 3 * grid && npairs <= 4 * nG) {
+        if (!over32 && tiles >= grid && 2 * tiles <= 3 * grid && npairs <= 4 * nG) {
             tile_units_bits<GATED>(P, D, m_own, s_mask, s_kept, nG, stok,
                                    reinterpret_cast<float4 *>(xf));
             return;
