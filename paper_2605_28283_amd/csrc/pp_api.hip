@@ -96,7 +96,7 @@ pp_status run_ffn(pp_layer *L, const uint16_t *x, int32_t T, float tau, const fl
         const float *it = inv_temp ? inv_temp + t0 : nullptr;
         hipError_t e = launch_route(L, xs, n, tau, it, idx, cnt, nullptr, !prefill, s);
         if (e == hipSuccess)
-            e = prefill ? launch_prefill_ffn(L, xs, n, ys, s) : launch_decode_ffn(L, xs, n, ys, s);
+            e = prefill ? launch_prefill_ffn(L, xs, n, cnt, ys, s) : launch_decode_ffn(L, xs, n, ys, s);
         if (e != hipSuccess) return hip_status(e);
     }
     return PP_OK;

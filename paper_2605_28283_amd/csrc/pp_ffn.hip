@@ -9,17 +9,20 @@
 //
 //   dispatch_k  : per expert, the ascending list of tokens that kept it (block
 //                 scan + scatter) and the plan, written by the last expert to
-//                 finish; further workgroups set y to the output bias (0 for
-//                 SwiGLU layers).
+//                 finish; when the batch has more pairs than the pair-row
+//                 buffer holds, further workgroups set y to the output bias
+//                 (0 for SwiGLU layers) for the atomic adds of the pairs past
+//                 it.
 //   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
 //                 SiLU product of one group (shared with the decode kernel).
 //   down_pf_k   : unit = (expert, 256 rows); the expert's down block stays in
 //                 registers across its token groups; each (token, expert)
 //                 pair's rows go to a pair-row buffer (pairs past its 1 GiB
 //                 capacity add into y with fp32 atomics).
-//   combine_pf_k: y[t] += t's pair rows, kept experts in ascending order --
-//                 no float atomics while the buffer holds every pair, so the
-//                 result is deterministic.
+//   combine_pf_k: y[t] = output bias + t's pair rows, kept experts in
+//                 ascending order (y[t] + the rows for a token with pairs past
+//                 the buffer) -- no float atomics while the buffer holds every
+//                 pair, so the result is deterministic.
 // Units of one expert are placed on one XCD (shared weights or h in L2).
 #include "pp_gateup.h"
 
@@ -66,8 +69,9 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
 
 // ------------------------------------------------------------------ prefill
 
-__global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ selmask, int T,
-                                                  int E, int32_t *__restrict__ ecount,
+__global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ selmask,
+                                                  const int32_t *__restrict__ count, size_t cap,
+                                                  int T, int E, int32_t *__restrict__ ecount,
                                                   int32_t *__restrict__ tokl, int stride,
                                                   float *__restrict__ y, size_t ny4,
                                                   const float *__restrict__ bproj, int d4,
@@ -77,7 +81,16 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
     __shared__ int scan[8];
     __shared__ int s_flag;
     const int e = blockIdx.x, tid = threadIdx.x;
-    if (e >= E) {  // workgroups past the experts set y to the output bias (or 0)
+    if (e >= E) {
+        // workgroups past the experts set y to the output bias (or 0) if some
+        // pairs will not fit the pair-row buffer and add into y instead
+        static_assert(sizeof(scan) >= 4 * sizeof(int), "four wavefront sums");
+        size_t c = 0;
+        for (int t = tid; t < T; t += blockDim.x) c += (size_t)count[t];
+        const int cw = __builtin_amdgcn_readlane(wave_scan_i32((int)c), 63);
+        if ((tid & 63) == 0) scan[tid >> 6] = cw;
+        __syncthreads();
+        if ((size_t)scan[0] + scan[1] + scan[2] + scan[3] <= cap) return;
         float4 *y4 = reinterpret_cast<float4 *>(y);
         const float4 *b4 = reinterpret_cast<const float4 *>(bproj);
         const size_t nz = (size_t)(gridDim.x - E) * blockDim.x;
@@ -246,26 +259,29 @@ __global__ __launch_bounds__(256, 2) void down_pf_k(DNParams P) {
     }
 }
 
-// y[t] += the rows of t's pairs, kept experts in ascending order (a fixed
-// order: deterministic).  One workgroup per token: wavefront 0 lists the
-// token's pair rows in LDS (a ballot prefix over the expert bitmask), then
-// every thread sums its four float4 columns, eight rows at a time with all
-// of a batch's loads in flight.  y holds the
-// output bias (or 0) and the atomic contributions of pairs past the buffer.
+// y[t] = the output bias (or 0) + the rows of t's pairs, kept experts in
+// ascending order (a fixed order: deterministic).  One workgroup per token:
+// wavefront 0 lists the token's pair rows in LDS (a ballot prefix over the
+// expert bitmask), then every thread sums its four float4 columns, eight rows
+// at a time with all of a batch's loads in flight.  A token with pairs past
+// the buffer starts from y instead, which then holds the output bias and
+// those pairs' atomic contributions.
 __global__ __launch_bounds__(256) void combine_pf_k(const uint32_t *__restrict__ selmask, int T,
                                                     int E, int d, const int32_t *__restrict__ posq,
                                                     const int32_t *__restrict__ ebase,
                                                     const float *__restrict__ part, size_t cap,
+                                                    const float *__restrict__ bproj,
                                                     float *__restrict__ y) {
     constexpr int kBatch = 8;   // pair rows in flight
     constexpr int kChunks = 4;  // float4 columns per thread and row (d = 4096 in one pass)
     __shared__ int plist[kMaxExperts];
-    __shared__ int s_k;
+    __shared__ int s_k, s_spill;
     const int tid = threadIdx.x, lane = tid & 63;
     const int t = blockIdx.x;
     if (tid < 64) {
         const uint32_t *sm = selmask + (size_t)t * 8;
         int k = 0;
+        bool spill = false;
         for (int e0 = 0; e0 < E; e0 += 64) {
             const int e = e0 + lane;
             const bool kept = e < E && ((sm[e >> 5] >> (e & 31)) & 1u);
@@ -273,21 +289,28 @@ __global__ __launch_bounds__(256) void combine_pf_k(const uint32_t *__restrict__
             if (kept) {
                 const size_t pair = (size_t)ebase[e] + posq[(size_t)t * E + e];
                 plist[k + __popcll(bal & ((1ull << lane) - 1ull))] = pair < cap ? (int)pair : -1;
+                spill = spill || pair >= cap;
             }
             k += __popcll(bal);
         }
-        if (lane == 0) s_k = k;
+        spill = __ballot(spill) != 0ull;
+        if (lane == 0) {
+            s_k = k;
+            s_spill = spill ? 1 : 0;
+        }
     }
     __syncthreads();
     const int k = s_k, d4 = d / 4;
     float4 *yt = reinterpret_cast<float4 *>(y + (size_t)t * d);
+    // the starting value: y (bias + atomic adds) or the bias itself
+    const float4 *y0 = s_spill ? yt : reinterpret_cast<const float4 *>(bproj);
     // a thread's kChunks float4 columns of kBatch rows are all in flight at once
     for (int c0 = 0; c0 < d4; c0 += kChunks * 256) {
         float4 acc[kChunks];
 #pragma unroll
         for (int u = 0; u < kChunks; ++u) {
             const int c4 = c0 + tid + 256 * u;
-            acc[u] = c4 < d4 ? yt[c4] : make_float4(0.f, 0.f, 0.f, 0.f);
+            acc[u] = (c4 < d4 && y0) ? y0[c4] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
         for (int i0 = 0; i0 < k; i0 += kBatch) {
             float4 v[kBatch][kChunks];
@@ -348,12 +371,13 @@ counter_layout counters_for(const pp_dims &dm, int max_tokens) {
     return c;
 }
 
-hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s) {
+hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, const int32_t *count,
+                              float *y, hipStream_t s) {
     const pp_dims &dm = L->dm;
     const counter_layout cl = counters_for(dm, L->max_tokens);
     prof_mark(L, PP_KERNEL_DISPATCH, s, true);
-    hipLaunchKernelGGL(dispatch_k, dim3(dm.E + L->num_cu), dim3(256), 0, s, L->selmask, T, dm.E,
-                       L->ecount,
+    hipLaunchKernelGGL(dispatch_k, dim3(dm.E + L->num_cu), dim3(256), 0, s, L->selmask, count,
+                       L->pf_cap, T, dm.E, L->ecount,
                        L->tokl, L->max_tokens, y, (size_t)T * dm.d / 4, L->bproj, dm.d / 4,
                        L->pf_posq, L->pf_ebase, L->counters + cl.dispatch_base(),
                        plan_view(L, true));
@@ -376,7 +400,7 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     prof_mark(L, PP_KERNEL_DOWN, s, true);
     hipLaunchKernelGGL(down_pf_k, dim3(occ_dn * L->num_cu), dim3(256), 0, s, dp);
     hipLaunchKernelGGL(combine_pf_k, dim3(T), dim3(256), 0, s, L->selmask, T, dm.E, dm.d,
-                       L->pf_posq, L->pf_ebase, L->pf_part, L->pf_cap, y);
+                       L->pf_posq, L->pf_ebase, L->pf_part, L->pf_cap, L->bproj, y);
     prof_mark(L, PP_KERNEL_DOWN, s, false);
     return hipGetLastError();
 }

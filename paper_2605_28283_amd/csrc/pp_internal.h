@@ -132,7 +132,8 @@ hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const 
                         int32_t *idx, int32_t *count, float *gate_w, bool build_plan,
                         hipStream_t s);
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
-hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
+hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, const int32_t *count,
+                              float *y, hipStream_t s);
 
 inline PlanView plan_view(pp_layer *L, bool prefill) {
     const int G = plan_max_groups(L->dm, L->max_tokens);

@@ -283,6 +283,22 @@ def test_llama8b_prefill(oracle_mod, llama8b):
         assert np.abs(y - res["y"]).max() <= 1e-3 * rms
 
 
+def test_llama8b_prefill_past_pair_buffer(oracle_mod, llama8b):
+    """More (token, expert) pairs than the pair-row buffer holds (65536 rows of
+    d = 4096 floats): those pairs add into y atomically, the rest are summed per
+    token, and y starts from the output bias only where a token has no pair
+    past the buffer.  Even tokens route nearly flat (inverse temperature 0.01:
+    most experts kept at tau 0.95), odd tokens sharply (inverse temperature 20:
+    one or two kept), so tokens with and without such pairs share the call."""
+    L, w, dl = llama8b
+    T = 2048
+    x, _ = make_tokens(T, w.d, 91)
+    it = np.where(np.arange(T) % 2 == 0, 0.01, 20.0).astype(np.float32)
+    res = parity(oracle_mod, dl, "prefill", x, 0.95, it, rows=np.arange(0, T, 127))
+    assert int(res["cnt"].sum()) > 65536
+    assert res["cnt"][1::2].max() <= 8
+
+
 def test_qwen_skewed(oracle_mod):
     w = WORKLOADS["qwen7b_skewed"]
     L = workload_layer(w, 0)
