@@ -56,7 +56,7 @@ void free_layer(pp_layer *L) {
     void *bufs[] = {L->Wr,     L->bias,  L->Wgu,     L->Wd,    L->bfc,   L->bproj, L->gpart, L->counters,
                     L->selmask, L->gsig, L->idx_tmp, L->cnt_tmp, L->abpart, L->h_hi,
                     L->h_lo,   L->ypart, L->ecount,  L->tokl,  L->plan,  L->dec_tok,
-                    L->pf_part, L->pf_ebase, L->pf_posq,
+                    L->pf_cut, L->pf_ebase,
                     L->emask};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
@@ -96,7 +96,7 @@ pp_status run_ffn(pp_layer *L, const uint16_t *x, int32_t T, float tau, const fl
         const float *it = inv_temp ? inv_temp + t0 : nullptr;
         hipError_t e = launch_route(L, xs, n, tau, it, idx, cnt, nullptr, !prefill, s);
         if (e == hipSuccess)
-            e = prefill ? launch_prefill_ffn(L, xs, n, cnt, ys, s) : launch_decode_ffn(L, xs, n, ys, s);
+            e = prefill ? launch_prefill_ffn(L, xs, n, ys, s) : launch_decode_ffn(L, xs, n, ys, s);
         if (e != hipSuccess) return hip_status(e);
     }
     return PP_OK;
@@ -188,11 +188,9 @@ pp_status create_layer(pp_layer **out, int32_t d, int32_t d_ff, int32_t E, int32
     chk(dev_alloc(&L->ypart, (size_t)kDecodeChunks * kDecodeTile * d));
     chk(dev_alloc(&L->ecount, (size_t)E));
     chk(dev_alloc(&L->tokl, (size_t)E * max_tokens));
-    L->pf_cap = kPfPartBytes / (sizeof(float) * (size_t)d);
-    if (L->pf_cap > (size_t)max_tokens * E) L->pf_cap = (size_t)max_tokens * E;
-    chk(dev_alloc(&L->pf_part, L->pf_cap * d));
+    L->pf_ncut = (max_tokens + kPfChunk - 1) / kPfChunk + 1;
+    chk(dev_alloc(&L->pf_cut, (size_t)E * L->pf_ncut));
     chk(dev_alloc(&L->pf_ebase, (size_t)E));
-    chk(dev_alloc(&L->pf_posq, (size_t)max_tokens * E));
     chk(dev_alloc(&L->plan, (size_t)4 + 4 * (size_t)plan_max_groups(L->dm, max_tokens) + E + 1));
     chk(dev_alloc(&L->dec_tok, (size_t)kDecodeTile * E));
     chk(dev_alloc(&L->emask, (size_t)E));

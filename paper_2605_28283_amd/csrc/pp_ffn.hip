@@ -8,22 +8,15 @@
 // a group.
 //
 //   dispatch_k  : per expert, the ascending list of tokens that kept it (block
-//                 scan + scatter) and the plan, written by the last expert to
-//                 finish; when the batch has more pairs than the pair-row
-//                 buffer holds, further workgroups set y to the output bias
-//                 (0 for SwiGLU layers) for the atomic adds of the pairs past
-//                 it.
+//                 scan + scatter), where each chunk of kPfChunk tokens starts
+//                 in it, and the plan, written by the last expert to finish.
 //   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
 //                 SiLU product of one group (shared with the decode kernel).
-//   down_pf_k   : unit = (expert, 256 rows); the expert's down block stays in
-//                 registers across its token groups; each (token, expert)
-//                 pair's rows go to a pair-row buffer (pairs past its 1 GiB
-//                 capacity add into y with fp32 atomics).
-//   combine_pf_k: y[t] = output bias + t's pair rows, kept experts in
-//                 ascending order (y[t] + the rows for a token with pairs past
-//                 the buffer) -- no float atomics while the buffer holds every
-//                 pair, so the result is deterministic.
-// Units of one expert are placed on one XCD (shared weights or h in L2).
+//   down_rows_k : unit = (R rows of d, chunk of kPfChunk tokens); the chunk's
+//                 y rows are summed in LDS over the experts in ascending
+//                 order and written once -- no float atomics, deterministic.
+// Units sharing weights (an expert's K-slices and groups; a row block's token
+// chunks) are placed on one XCD, where they meet in L2.
 #include "pp_gateup.h"
 
 namespace pp {
@@ -35,8 +28,11 @@ struct DNParams {
     const uint16_t *h_hi;
     const uint16_t *h_lo;
     float *y;
-    float *part;     // [cap][d] pair rows
-    size_t cap;
+    const float *bproj;    // [d] output bias, or NULL (0)
+    const int32_t *cut;    // [E][ncut]: expert e's tokens below token c * kPfChunk
+    int ncut;
+    const int32_t *ebase;  // [E] first pair (h row) of each expert's bucket
+    int tstride;           // toklist row stride per expert
     PlanView plan;
 };
 
@@ -69,35 +65,16 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
 
 // ------------------------------------------------------------------ prefill
 
-__global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ selmask,
-                                                  const int32_t *__restrict__ count, size_t cap,
-                                                  int T, int E, int32_t *__restrict__ ecount,
+__global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ selmask, int T,
+                                                  int E, int32_t *__restrict__ ecount,
                                                   int32_t *__restrict__ tokl, int stride,
-                                                  float *__restrict__ y, size_t ny4,
-                                                  const float *__restrict__ bproj, int d4,
-                                                  int32_t *__restrict__ posq,
+                                                  int32_t *__restrict__ cut, int ncut,
                                                   int32_t *__restrict__ ebase, uint32_t *cnt,
                                                   PlanView plan) {
+    static_assert(kPfChunk % 256 == 0, "chunk starts fall on scan blocks");
     __shared__ int scan[8];
     __shared__ int s_flag;
     const int e = blockIdx.x, tid = threadIdx.x;
-    if (e >= E) {
-        // workgroups past the experts set y to the output bias (or 0) if some
-        // pairs will not fit the pair-row buffer and add into y instead
-        static_assert(sizeof(scan) >= 4 * sizeof(int), "four wavefront sums");
-        size_t c = 0;
-        for (int t = tid; t < T; t += blockDim.x) c += (size_t)count[t];
-        const int cw = __builtin_amdgcn_readlane(wave_scan_i32((int)c), 63);
-        if ((tid & 63) == 0) scan[tid >> 6] = cw;
-        __syncthreads();
-        if ((size_t)scan[0] + scan[1] + scan[2] + scan[3] <= cap) return;
-        float4 *y4 = reinterpret_cast<float4 *>(y);
-        const float4 *b4 = reinterpret_cast<const float4 *>(bproj);
-        const size_t nz = (size_t)(gridDim.x - E) * blockDim.x;
-        for (size_t i = (size_t)(e - E) * blockDim.x + tid; i < ny4; i += nz)
-            y4[i] = b4 ? b4[i % d4] : make_float4(0.f, 0.f, 0.f, 0.f);
-        return;
-    }
     const int w = e >> 5, b = e & 31;
     int base = 0;
     for (int t0 = 0; t0 < T; t0 += blockDim.x) {
@@ -105,13 +82,14 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
         const int f = (t < T && ((selmask[(size_t)t * 8 + w] >> b) & 1u)) ? 1 : 0;
         int ex, ex1, tot, tot1;
         block_excl_scan2(f, 0, &ex, &ex1, &tot, &tot1, scan);
-        if (f) {
-            tokl[(size_t)e * stride + base + ex] = t;
-            posq[(size_t)t * E + e] = base + ex;
-        }
+        if (f) tokl[(size_t)e * stride + base + ex] = t;
+        if (tid == 0 && t0 % kPfChunk == 0) cut[(size_t)e * ncut + t0 / kPfChunk] = base;
         base += tot;
     }
-    if (tid == 0) st_dev_u32(reinterpret_cast<uint32_t *>(ecount + e), (uint32_t)base);
+    if (tid == 0) {
+        cut[(size_t)e * ncut + (T + kPfChunk - 1) / kPfChunk] = base;
+        st_dev_u32(reinterpret_cast<uint32_t *>(ecount + e), (uint32_t)base);
+    }
     if (!arrive_last(cnt, (unsigned)E, &s_flag)) return;
     // prefill plan: expert e's bucket becomes ceil(c_e / 64) groups
     const int c = (tid < E) ? (int)ld_dev_u32(reinterpret_cast<uint32_t *>(ecount + tid)) : 0;
@@ -136,209 +114,220 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
     }
 }
 
-// Unit = (expert, 256 rows of d): the four wavefronts hold the expert's
-// 256 x 128 down block in registers (four 16-row tiles each, loaded once) and
-// run it over the expert's token groups of 64.  A group's h (hi and lo, MFMA B
-// order) is staged in LDS while the next group's is being loaded; the
-// 64 x 256 result is transposed through LDS and stored as the pairs' rows
-// (each store instruction 64 consecutive floats of one pair's row), which
-// combine_pf_k sums per token.  Pairs past the buffer's capacity add into y
-// with fp32 atomics instead.  Units of one expert share its h rows and go to
-// the same XCD.
-constexpr int kPfRows = 256;
-__global__ __launch_bounds__(256, 2) void down_pf_k(DNParams P) {
-    constexpr int MT = 4;
-    __shared__ union {
-        struct {
-            uint4 hi[4 * 4 * 64];  // [token tile][K-step][lane]
-            uint4 lo[4 * 4 * 64];
-        } h;
-        float y[kGroupTokens][kPfRows];
-    } S;
-    __shared__ int stok[kGroupTokens];
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int n_rb = (P.d + kPfRows - 1) / kPfRows;
-    const int units = P.E * n_rb;
-    const int slots = 8 * ((units + 7) / 8);
-    const int RT = P.d / 16;
-    const uint4 z = make_uint4(0, 0, 0, 0);
+// Unit = (R rows of d, a chunk of kPfChunk consecutive tokens).  The chunk's
+// outputs in those rows stay in LDS for the whole unit, starting from the
+// output bias (or 0).  The experts are taken in ascending order; the tokens
+// of the chunk that kept expert e are a contiguous run of its ascending
+// bucket (positions cut[e][c] .. cut[e][c + 1]), so their h rows are
+// consecutive.  A step is one expert's R x 128 down block, staged in LDS, and
+// up to eight 16-token tiles of its run, one per wavefront (bf16 MFMA
+// 16x16x32: A = the down block, B = the tokens' h, hi then lo per K-step);
+// each tile is added to its tokens' LDS rows, and barriers separate the
+// steps.  Every output is thus the bias plus its token's pair contributions
+// in ascending expert order -- deterministic, with no atomics and no per-pair
+// rows in memory.  Every step issues the same loads (bounds-checked buffer
+// loads: lanes past the run read zeros without touching memory), kRowAhead
+// steps ahead, so each wait is for one step's data only.  The token chunks of
+// one row block are neighbouring units, placed on one XCD, so they share the
+// down blocks in L2.
+constexpr int kRowAhead = 4;  // steps whose loads are in flight
 
-    for (int slot = blockIdx.x; slot < slots; slot += gridDim.x) {
-        const int unit = xcd_order(slot, units);
-        if (unit >= units) continue;
-        const int e = unit / n_rb, rb = unit - e * n_rb;
-        const int g0 = P.plan.egrp[e], g1 = P.plan.egrp[e + 1];
-        if (g0 >= g1) continue;
-        const int nrows = min(kPfRows, P.d - rb * kPfRows);
-        uint4 w[MT][4];
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+template <int R>
+struct DownRowsLds {
+    float y[kPfChunk * (R + 4)];  // [token][row], rows padded by 4 floats
+    u32x4_t w[R / 16 * 4 * 64];   // [row tile][K-step][lane]: A fragments
+    int e[kMaxExperts];           // experts with tokens in the chunk, ascending
+    int a[kMaxExperts];           // their run's first bucket position
+    int n[kMaxExperts];           // tokens in the run
+    int p[kMaxExperts];           // first pair (h row) of the run
+    int m, steps;
+};
+
+// One step's loads as held by a thread.
+struct RowStep {
+    u32x4_t w0, w1;         // its share of the down block (R = 64: both)
+    u32x4_t bh[4], bl[4];   // the wavefront's tile: h hi / lo B fragments
+    unsigned tok;           // token of the lane's slot (0 past the run)
+};
+
+// Steps in order: list entry k, round r (tiles 8 r .. 8 r + 7 of its run).
+struct RowCursor {
+    int k, r;
+};
+
+template <int R>
+__device__ __forceinline__ void rows_next(RowCursor &c, const DownRowsLds<R> &S, int m) {
+    if (c.k < m && 8 * 16 * (c.r + 1) < S.n[c.k]) {
+        ++c.r;
+    } else {
+        ++c.k;
+        c.r = 0;
+    }
+}
+
+// A raw buffer over [base, base + bytes): loads past it read zeros without a
+// memory access.  base and bytes are wavefront-uniform (scalar registers).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void *base, unsigned bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    const uint32_t nb = __builtin_amdgcn_readfirstlane(bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void *>(((uint64_t)hi << 32) | lo), (short)0, (int)nb, 0x00020000);
+}
+
+// Issues step c's loads (past the list: all out of range, zeros).
+template <int R>
+__device__ __forceinline__ void rows_issue(RowStep &st, const DNParams &P, const DownRowsLds<R> &S,
+                                           RowCursor c, int m, int rb, int tid) {
+    constexpr int MT = R / 16, WN = MT * 4 * 64;
+    static_assert(WN <= 2 * 512, "at most two uint4 of a down block per thread");
+    // every descriptor operand is wavefront-uniform, so it lives in SGPRs
+    const int lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ck = __builtin_amdgcn_readfirstlane(c.k), cr = __builtin_amdgcn_readfirstlane(c.r);
+    const bool live = ck < m;
+    const int kc = live ? ck : 0;
+    const int e = __builtin_amdgcn_readfirstlane(S.e[kc]);
+    const int n = live ? __builtin_amdgcn_readfirstlane(S.n[kc]) : 0;
+    const int p0 = __builtin_amdgcn_readfirstlane(S.p[kc]);
+    const int a0 = __builtin_amdgcn_readfirstlane(S.a[kc]);
+    const int t16 = 16 * (wv + 8 * cr);  // the tile's first place in the run
+    const int nt = max(0, min(16, n - t16));  // tokens in the tile
+    // down block: contiguous WN uint4
+    const auto rw = rows_rsrc(P.Wd + ((size_t)e * (P.d / 16) + (size_t)rb * MT) * 256 * 8,
+                              live ? WN * 16u : 0u);
+    st.w0 = __builtin_amdgcn_raw_buffer_load_b128(rw, (unsigned)tid * 16u, 0, 0);
+    if (WN > 512) st.w1 = __builtin_amdgcn_raw_buffer_load_b128(rw, (unsigned)(512 + tid) * 16u, 0, 0);
+    // the tile's h rows and tokens
+    const size_t q0 = (size_t)p0 + t16;
+    const auto rh = rows_rsrc(P.h_hi + q0 * kExpertWidth, (unsigned)nt * kExpertWidth * 2u);
+    const auto rl = rows_rsrc(P.h_lo + q0 * kExpertWidth, (unsigned)nt * kExpertWidth * 2u);
+    const unsigned o = ((unsigned)(lane & 15) * kExpertWidth + 8u * (lane >> 4)) * 2u;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        st.bh[s] = __builtin_amdgcn_raw_buffer_load_b128(rh, o + s * kKStep * 2u, 0, 0);
+        st.bl[s] = __builtin_amdgcn_raw_buffer_load_b128(rl, o + s * kKStep * 2u, 0, 0);
+    }
+    const auto rt = rows_rsrc(P.plan.toklist + (size_t)e * P.tstride + a0 + t16, (unsigned)nt * 4u);
+    st.tok = __builtin_amdgcn_raw_buffer_load_b32(rt, (unsigned)(lane & 15) * 4u, 0, 0);
+}
+
+// Runs step c: its down block to LDS, then the wavefront's tile.
+template <int R>
+__device__ __forceinline__ void rows_run(DownRowsLds<R> &S, const RowStep &st, RowCursor c, int m,
+                                         int t0, int tid) {
+    constexpr int MT = R / 16, YS = R + 4, WN = MT * 4 * 64;
+    const int lane = tid & 63, wv = tid >> 6;
+    __syncthreads();  // the previous step's block and rows are done with
+    if (WN >= 512 || tid < WN) S.w[tid] = st.w0;
+    if (WN > 512) S.w[512 + tid] = st.w1;
+    __syncthreads();
+    if (c.k >= m) return;
+    const int n = S.n[c.k], t16 = 16 * (wv + 8 * c.r);
+    if (t16 >= n) return;
+    f32x4 acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const uint4 bh = *reinterpret_cast<const uint4 *>(&st.bh[s]);
+        const uint4 bl = *reinterpret_cast<const uint4 *>(&st.bl[s]);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const int rt = min(rb * (kPfRows / 16) + wv * MT + mt, RT - 1);  // past d: unused
-            const uint16_t *wp = P.Wd + (((size_t)e * RT + rt) * 4 * 64 + lane) * 8;
-#pragma unroll
-            for (int s = 0; s < 4; ++s) w[mt][s] = ldg16(wp + s * 512);
+            const uint4 a = *reinterpret_cast<const uint4 *>(&S.w[(mt * 4 + s) * 64 + lane]);
+            acc[mt] = mfma16(a, bh, acc[mt]);
+            acc[mt] = mfma16(a, bl, acc[mt]);
         }
-        // h of one group in B-fragment order: thread slot i = tid + 256 k holds
-        // token tile i / 256, K-step (i / 64) % 4, lane i % 64
-        uint4 hv[4], lv[4];
-        auto load_h = [&](int g) {
-            const int n = P.plan.grp_n[g], p0 = P.plan.grp_pair[g];
+    }
+    // lane: rows 4 (lane / 16) + i of each row tile, its slot's token
+    if (t16 + (lane & 15) < n) {
+        float *yr = &S.y[((int)st.tok - t0) * YS + 4 * (lane >> 4)];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int i = tid + 256 * k;
-                const int j = i >> 8, s = (i >> 6) & 3, l = i & 63;
-                const int q = 16 * j + (l & 15);
-                hv[k] = lv[k] = z;
-                if (q < n) {
-                    const size_t o = (size_t)(p0 + q) * kExpertWidth + s * kKStep + 8 * (l >> 4);
-                    hv[k] = ldg16(P.h_hi + o);
-                    lv[k] = ldg16(P.h_lo + o);
-                }
-            }
-        };
-        load_h(g0);
-        for (int g = g0; g < g1; ++g) {
-            const int n = P.plan.grp_n[g];
-            __syncthreads();  // the previous group's atomics have read S.y
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                S.h.hi[tid + 256 * k] = hv[k];
-                S.h.lo[tid + 256 * k] = lv[k];
-            }
-            if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
-            __syncthreads();
-            if (g + 1 < g1) load_h(g + 1);
-            const int NT = (n + 15) >> 4;
-            f32x4 acc[MT][4];
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (j < NT) {
-#pragma unroll
-                    for (int s = 0; s < 4; ++s) {
-                        const uint4 bh = S.h.hi[(j * 4 + s) * 64 + lane];
-                        const uint4 bl = S.h.lo[(j * 4 + s) * 64 + lane];
-#pragma unroll
-                        for (int mt = 0; mt < MT; ++mt) {
-                            acc[mt][j] = mfma16(w[mt][s], bh, acc[mt][j]);
-                            acc[mt][j] = mfma16(w[mt][s], bl, acc[mt][j]);
-                        }
-                    }
-                }
-            }
-            __syncthreads();  // h is no longer read: its LDS becomes the transpose buffer
-            // lane holds rows 4 (lane / 16) + i of its tile, token slot 16 j + lane % 16
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const int r0 = (wv * MT + mt) * 16 + 4 * (lane >> 4);
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (j < NT)
-                        *reinterpret_cast<float4 *>(&S.y[16 * j + (lane & 15)][r0]) = make_float4(
-                            acc[mt][j][0], acc[mt][j][1], acc[mt][j][2], acc[mt][j][3]);
-            }
-            __syncthreads();
-            const int p0 = P.plan.grp_pair[g];
-            for (int q = wv; q < n; q += 4) {
-                const size_t pair = (size_t)(p0 + q);
-                if (pair < P.cap) {  // the pair's row, summed per token by combine_pf_k
-                    static_assert(kPfRows == 4 * 64, "one float4 per lane covers a row");
-                    float4 *pr = reinterpret_cast<float4 *>(P.part + pair * P.d + (size_t)rb * kPfRows);
-                    if (4 * lane < nrows) pr[lane] = *reinterpret_cast<const float4 *>(&S.y[q][4 * lane]);
-                } else {  // past the buffer: straight into y
-                    float *yr = P.y + (size_t)stok[q] * P.d + (size_t)rb * kPfRows;
-#pragma unroll
-                    for (int c = 0; c < kPfRows / 64; ++c)
-                        if (64 * c + lane < nrows) atomicAdd(yr + 64 * c + lane, S.y[q][64 * c + lane]);
-                }
-            }
+        for (int mt = 0; mt < MT; ++mt) {
+            float4 v = *reinterpret_cast<float4 *>(yr + 16 * mt);
+            v.x += acc[mt][0];
+            v.y += acc[mt][1];
+            v.z += acc[mt][2];
+            v.w += acc[mt][3];
+            *reinterpret_cast<float4 *>(yr + 16 * mt) = v;
         }
     }
 }
 
-// y[t] = the output bias (or 0) + the rows of t's pairs, kept experts in
-// ascending order (a fixed order: deterministic).  One workgroup per token:
-// wavefront 0 lists the token's pair rows in LDS (a ballot prefix over the
-// expert bitmask), then every thread sums its four float4 columns, eight rows
-// at a time with all of a batch's loads in flight.  A token with pairs past
-// the buffer starts from y instead, which then holds the output bias and
-// those pairs' atomic contributions.
-__global__ __launch_bounds__(256) void combine_pf_k(const uint32_t *__restrict__ selmask, int T,
-                                                    int E, int d, const int32_t *__restrict__ posq,
-                                                    const int32_t *__restrict__ ebase,
-                                                    const float *__restrict__ part, size_t cap,
-                                                    const float *__restrict__ bproj,
-                                                    float *__restrict__ y) {
-    constexpr int kBatch = 8;   // pair rows in flight
-    constexpr int kChunks = 4;  // float4 columns per thread and row (d = 4096 in one pass)
-    __shared__ int plist[kMaxExperts];
-    __shared__ int s_k, s_spill;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int t = blockIdx.x;
-    if (tid < 64) {
-        const uint32_t *sm = selmask + (size_t)t * 8;
-        int k = 0;
-        bool spill = false;
-        for (int e0 = 0; e0 < E; e0 += 64) {
-            const int e = e0 + lane;
-            const bool kept = e < E && ((sm[e >> 5] >> (e & 31)) & 1u);
-            const unsigned long long bal = __ballot(kept);
-            if (kept) {
-                const size_t pair = (size_t)ebase[e] + posq[(size_t)t * E + e];
-                plist[k + __popcll(bal & ((1ull << lane) - 1ull))] = pair < cap ? (int)pair : -1;
-                spill = spill || pair >= cap;
+template <int R>
+__global__ __launch_bounds__(512, 1) void down_rows_k(DNParams P) {
+    constexpr int YS = R + 4;  // LDS row stride of y in floats
+    __shared__ DownRowsLds<R> S;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int nC = (P.T + kPfChunk - 1) / kPfChunk;
+    const int units = (P.d / R) * nC;
+    const int slots = 8 * ((units + 7) / 8);
+    for (int slot = blockIdx.x; slot < slots; slot += gridDim.x) {
+        const int unit = xcd_order(slot, units);
+        if (unit >= units) continue;
+        const int rb = unit / nC, c = unit - rb * nC;
+        const int t0 = c * kPfChunk, nt = min(kPfChunk, P.T - t0);
+        if (wv == 0) {
+            int m = 0, steps = 0;
+            for (int e0 = 0; e0 < P.E; e0 += 64) {
+                const int e = e0 + lane;
+                int a = 0, b = 0;
+                if (e < P.E) {
+                    a = P.cut[(size_t)e * P.ncut + c];
+                    b = P.cut[(size_t)e * P.ncut + c + 1];
+                }
+                const unsigned long long bal = __ballot(b > a);
+                if (b > a) {
+                    const int k = m + __popcll(bal & ((1ull << lane) - 1ull));
+                    S.e[k] = e;
+                    S.a[k] = a;
+                    S.n[k] = b - a;
+                    S.p[k] = P.ebase[e] + a;
+                }
+                m += __popcll(bal);
+                const int rounds = b > a ? (b - a + 127) / 128 : 0;
+                steps += __builtin_amdgcn_readlane(wave_scan_i32(rounds), 63);
             }
-            k += __popcll(bal);
-        }
-        spill = __ballot(spill) != 0ull;
-        if (lane == 0) {
-            s_k = k;
-            s_spill = spill ? 1 : 0;
-        }
-    }
-    __syncthreads();
-    const int k = s_k, d4 = d / 4;
-    float4 *yt = reinterpret_cast<float4 *>(y + (size_t)t * d);
-    // the starting value: y (bias + atomic adds) or the bias itself
-    const float4 *y0 = s_spill ? yt : reinterpret_cast<const float4 *>(bproj);
-    // a thread's kChunks float4 columns of kBatch rows are all in flight at once
-    for (int c0 = 0; c0 < d4; c0 += kChunks * 256) {
-        float4 acc[kChunks];
-#pragma unroll
-        for (int u = 0; u < kChunks; ++u) {
-            const int c4 = c0 + tid + 256 * u;
-            acc[u] = (c4 < d4 && y0) ? y0[c4] : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-        for (int i0 = 0; i0 < k; i0 += kBatch) {
-            float4 v[kBatch][kChunks];
-#pragma unroll
-            for (int r = 0; r < kBatch; ++r) {
-                const float4 *row =
-                    reinterpret_cast<const float4 *>(part + (size_t)max(plist[min(i0 + r, k - 1)], 0) * d);
-#pragma unroll
-                for (int u = 0; u < kChunks; ++u) v[r][u] = row[min(c0 + tid + 256 * u, d4 - 1)];
+            if (lane == 0) {
+                S.m = m;
+                S.steps = steps;
             }
+        }
+        for (int i = tid; i < nt * (R / 4); i += 512) {
+            const int t = i / (R / 4), q = i - t * (R / 4);
+            *reinterpret_cast<float4 *>(&S.y[t * YS + 4 * q]) =
+                P.bproj ? *reinterpret_cast<const float4 *>(P.bproj + rb * R + 4 * q)
+                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        __syncthreads();
+        const int m = S.m, steps = S.steps;
+        if (m > 0) {
+            RowStep st[kRowAhead];
+            RowCursor ci = {0, 0}, cr = {0, 0};  // next step to issue / to run
 #pragma unroll
-            for (int r = 0; r < kBatch; ++r) {
-                if (i0 + r < k && plist[i0 + r] >= 0) {
+            for (int i = 0; i < kRowAhead; ++i) {
+                rows_issue<R>(st[i], P, S, ci, m, rb, tid);
+                rows_next<R>(ci, S, m);
+            }
+            for (int s0 = 0; s0 < steps; s0 += kRowAhead) {
 #pragma unroll
-                    for (int u = 0; u < kChunks; ++u) {
-                        acc[u].x += v[r][u].x;
-                        acc[u].y += v[r][u].y;
-                        acc[u].z += v[r][u].z;
-                        acc[u].w += v[r][u].w;
-                    }
+                for (int i = 0; i < kRowAhead; ++i) {
+                    rows_run<R>(S, st[i], cr, m, t0, tid);
+                    rows_next<R>(cr, S, m);
+                    rows_issue<R>(st[i], P, S, ci, m, rb, tid);
+                    rows_next<R>(ci, S, m);
                 }
             }
         }
-#pragma unroll
-        for (int u = 0; u < kChunks; ++u) {
-            const int c4 = c0 + tid + 256 * u;
-            if (c4 < d4) yt[c4] = acc[u];
+        __syncthreads();
+        for (int i = tid; i < nt * (R / 4); i += 512) {
+            const int t = i / (R / 4), q = i - t * (R / 4);
+            *reinterpret_cast<float4 *>(P.y + (size_t)(t0 + t) * P.d + rb * R + 4 * q) =
+                *reinterpret_cast<const float4 *>(&S.y[t * YS + 4 * q]);
         }
+        __syncthreads();
     }
 }
 
@@ -353,8 +342,11 @@ DNParams dn_params(pp_layer *L, int T, float *y) {
     P.h_hi = L->h_hi;
     P.h_lo = L->h_lo;
     P.y = y;
-    P.part = L->pf_part;
-    P.cap = L->pf_cap;
+    P.bproj = L->bproj;
+    P.cut = L->pf_cut;
+    P.ncut = L->pf_ncut;
+    P.ebase = L->pf_ebase;
+    P.tstride = L->max_tokens;
     P.plan = plan_view(L, true);
     return P;
 }
@@ -371,16 +363,13 @@ counter_layout counters_for(const pp_dims &dm, int max_tokens) {
     return c;
 }
 
-hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, const int32_t *count,
-                              float *y, hipStream_t s) {
+hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s) {
     const pp_dims &dm = L->dm;
     const counter_layout cl = counters_for(dm, L->max_tokens);
     prof_mark(L, PP_KERNEL_DISPATCH, s, true);
-    hipLaunchKernelGGL(dispatch_k, dim3(dm.E + L->num_cu), dim3(256), 0, s, L->selmask, count,
-                       L->pf_cap, T, dm.E, L->ecount,
-                       L->tokl, L->max_tokens, y, (size_t)T * dm.d / 4, L->bproj, dm.d / 4,
-                       L->pf_posq, L->pf_ebase, L->counters + cl.dispatch_base(),
-                       plan_view(L, true));
+    hipLaunchKernelGGL(dispatch_k, dim3(dm.E), dim3(256), 0, s, L->selmask, T, dm.E, L->ecount,
+                       L->tokl, L->max_tokens, L->pf_cut, L->pf_ncut, L->pf_ebase,
+                       L->counters + cl.dispatch_base(), plan_view(L, true));
     prof_mark(L, PP_KERNEL_DISPATCH, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
@@ -396,11 +385,19 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, const int32
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     const DNParams dp = dn_params(L, T, y);
-    static const int occ_dn = resident(down_pf_k, 256);
+    // the widest row block (64, 32 or 16 rows) that still gives every CU a unit
+    const int nC = (T + kPfChunk - 1) / kPfChunk;
+    const int R = (dm.d / 64) * nC >= L->num_cu ? 64 : ((dm.d / 32) * nC >= L->num_cu ? 32 : 16);
+    static const int occ64 = resident(down_rows_k<64>, 512);
+    static const int occ32 = resident(down_rows_k<32>, 512);
+    static const int occ16 = resident(down_rows_k<16>, 512);
     prof_mark(L, PP_KERNEL_DOWN, s, true);
-    hipLaunchKernelGGL(down_pf_k, dim3(occ_dn * L->num_cu), dim3(256), 0, s, dp);
-    hipLaunchKernelGGL(combine_pf_k, dim3(T), dim3(256), 0, s, L->selmask, T, dm.E, dm.d,
-                       L->pf_posq, L->pf_ebase, L->pf_part, L->pf_cap, L->bproj, y);
+    if (R == 64)
+        hipLaunchKernelGGL(down_rows_k<64>, dim3(occ64 * L->num_cu), dim3(512), 0, s, dp);
+    else if (R == 32)
+        hipLaunchKernelGGL(down_rows_k<32>, dim3(occ32 * L->num_cu), dim3(512), 0, s, dp);
+    else
+        hipLaunchKernelGGL(down_rows_k<16>, dim3(occ16 * L->num_cu), dim3(512), 0, s, dp);
     prof_mark(L, PP_KERNEL_DOWN, s, false);
     return hipGetLastError();
 }

@@ -17,12 +17,12 @@ constexpr int kDecodeTile = 64;        // tokens per decode slice (one u64 token
 constexpr int kDecodeChunks = 16;      // expert chunks of the dense-group decode down projection
 constexpr int kRouteTile = 16;         // tokens / experts per router MFMA tile
 constexpr int kMaxWidth = 8192;        // largest supported d
+constexpr int kPfChunk = 512;          // tokens per prefill down unit (their y rows stay in LDS)
 constexpr int kGroupTokens = 64;       // tokens per prefill expert group
 constexpr int kMinStepsPerSlice = 8;   // K-steps each gate/up K-slice covers at least
 
 // Byte sizes of the scratch areas whose size does not follow from max_tokens.
 constexpr size_t kAbPartRows = 65536;  // K-split partial (a,b) rows of 256 floats
-constexpr size_t kPfPartBytes = (size_t)1 << 30;  // cap of the prefill pair-row buffer
 
 struct pp_dims {
     int d, d_ff, E, NS;      // NS = d / 32 K-steps
@@ -94,10 +94,9 @@ struct pp_layer {
     float *ypart;       // [kDecodeChunks][kDecodeTile][d] chunk partial outputs (decode, dense groups)
     int32_t *ecount;    // [E] tokens per expert (prefill)
     int32_t *tokl;      // [E][max_tokens] token ids per expert (prefill)
-    float *pf_part;     // prefill: [pf_cap][d] down-projection row of each (token, expert) pair
-    size_t pf_cap;      // pair rows pf_part holds (pairs past it add into y atomically)
+    int32_t *pf_cut;    // prefill: [E][pf_ncut] bucket position where each token chunk starts
+    int pf_ncut;        // token chunks of the largest batch + 1
     int32_t *pf_ebase;  // prefill: [E] first pair row of each expert's bucket
-    int32_t *pf_posq;   // prefill: [max_tokens][E] a token's place in each kept expert's bucket
     int32_t *plan;      // PlanView storage: 4 + 4 * plan_max_groups + E + 1 ints
     int32_t *dec_tok;   // [64 * E] token ids of the decode plan, pair order
     unsigned long long *emask;  // [E] decode: tokens that kept each expert (zero between calls)
@@ -132,8 +131,7 @@ hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const 
                         int32_t *idx, int32_t *count, float *gate_w, bool build_plan,
                         hipStream_t s);
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
-hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, const int32_t *count,
-                              float *y, hipStream_t s);
+hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
 
 inline PlanView plan_view(pp_layer *L, bool prefill) {
     const int G = plan_max_groups(L->dm, L->max_tokens);

@@ -283,13 +283,12 @@ def test_llama8b_prefill(oracle_mod, llama8b):
         assert np.abs(y - res["y"]).max() <= 1e-3 * rms
 
 
-def test_llama8b_prefill_past_pair_buffer(oracle_mod, llama8b):
-    """More (token, expert) pairs than the pair-row buffer holds (65536 rows of
-    d = 4096 floats): those pairs add into y atomically, the rest are summed per
-    token, and y starts from the output bias only where a token has no pair
-    past the buffer.  Even tokens route nearly flat (inverse temperature 0.01:
-    most experts kept at tau 0.95), odd tokens sharply (inverse temperature 20:
-    one or two kept), so tokens with and without such pairs share the call."""
+def test_llama8b_prefill_many_pairs(oracle_mod, llama8b):
+    """Over 100k (token, expert) pairs in one call, with very uneven tokens:
+    even tokens route nearly flat (inverse temperature 0.01: most experts kept
+    at tau 0.95), odd tokens sharply (inverse temperature 20: one or two
+    kept), so the experts' runs in each 512-token chunk are long and every
+    expert's down block meets tokens of both kinds."""
     L, w, dl = llama8b
     T = 2048
     x, _ = make_tokens(T, w.d, 91)
@@ -297,6 +296,15 @@ def test_llama8b_prefill_past_pair_buffer(oracle_mod, llama8b):
     res = parity(oracle_mod, dl, "prefill", x, 0.95, it, rows=np.arange(0, T, 127))
     assert int(res["cnt"].sum()) > 65536
     assert res["cnt"][1::2].max() <= 8
+
+
+def test_llama8b_prefill_ragged_chunks(oracle_mod, llama8b):
+    """700 tokens: one full 512-token chunk of the down projection and a ragged
+    one (the 32-row units); rows on both sides of the chunk edge and the last
+    token checked against the oracle."""
+    L, w, dl = llama8b
+    x, _ = make_tokens(700, w.d, 93, row_lognormal_sigma=0.5)
+    parity(oracle_mod, dl, "prefill", x, 0.8, rows=np.array([0, 255, 510, 511, 512, 513, 650, 699]))
 
 
 def test_qwen_skewed(oracle_mod):
@@ -310,9 +318,8 @@ def test_qwen_skewed(oracle_mod):
 
 
 def test_prefill_deterministic(oracle_mod, llama8b):
-    """Prefill sums each token's expert rows in a fixed order (no float
-    atomics while the pair-row buffer holds every pair): reruns give the same
-    bits."""
+    """Prefill sums each token's expert contributions in a fixed order (no
+    float atomics): reruns give the same bits."""
     L, w, dl = llama8b
     x, _ = make_tokens(300, w.d, 77, row_lognormal_sigma=0.5)
     a = dl.run("prefill", x, 0.8)
