@@ -71,20 +71,41 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
                                                   int32_t *__restrict__ cut, int ncut,
                                                   int32_t *__restrict__ ebase, uint32_t *cnt,
                                                   PlanView plan) {
-    static_assert(kPfChunk % 256 == 0, "chunk starts fall on scan blocks");
+    static_assert(kPfChunk % 256 == 0, "chunk starts fall on blocks of 256 tokens");
+    constexpr int kBlocks = 8;  // blocks of 256 tokens whose flags are loaded at once
     __shared__ int scan[8];
+    __shared__ __align__(16) int wc[2][kBlocks][4];  // per block and wavefront: tokens that kept e
     __shared__ int s_flag;
-    const int e = blockIdx.x, tid = threadIdx.x;
+    const int e = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int w = e >> 5, b = e & 31;
-    int base = 0;
-    for (int t0 = 0; t0 < T; t0 += blockDim.x) {
-        const int t = t0 + tid;
-        const int f = (t < T && ((selmask[(size_t)t * 8 + w] >> b) & 1u)) ? 1 : 0;
-        int ex, ex1, tot, tot1;
-        block_excl_scan2(f, 0, &ex, &ex1, &tot, &tot1, scan);
-        if (f) tokl[(size_t)e * stride + base + ex] = t;
-        if (tid == 0 && t0 % kPfChunk == 0) cut[(size_t)e * ncut + t0 / kPfChunk] = base;
-        base += tot;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    int base = 0, par = 0;
+    for (int T0 = 0; T0 < T; T0 += kBlocks * 256, par ^= 1) {
+        uint32_t word[kBlocks];
+#pragma unroll
+        for (int j = 0; j < kBlocks; ++j) {
+            const int t = T0 + 256 * j + tid;
+            word[j] = t < T ? selmask[(size_t)t * 8 + w] : 0u;
+        }
+        unsigned long long bal[kBlocks];
+#pragma unroll
+        for (int j = 0; j < kBlocks; ++j) {
+            bal[j] = __ballot((word[j] >> b) & 1u);
+            if (lane == 0) wc[par][j][wv] = __popcll(bal[j]);
+        }
+        __syncthreads();
+        // block j's tokens follow those of blocks 0 .. j - 1, in token order
+#pragma unroll
+        for (int j = 0; j < kBlocks; ++j) {
+            const int t = T0 + 256 * j + tid;
+            const int4 c = *reinterpret_cast<const int4 *>(wc[par][j]);
+            const int before = (wv > 0 ? c.x : 0) + (wv > 1 ? c.y : 0) + (wv > 2 ? c.z : 0);
+            if (tid == 0 && T0 + 256 * j < T && (T0 + 256 * j) % kPfChunk == 0)
+                cut[(size_t)e * ncut + (T0 + 256 * j) / kPfChunk] = base;
+            if ((bal[j] >> lane) & 1ull)
+                tokl[(size_t)e * stride + base + before + __popcll(bal[j] & below)] = t;
+            base += (c.x + c.y) + (c.z + c.w);
+        }
     }
     if (tid == 0) {
         cut[(size_t)e * ncut + (T + kPfChunk - 1) / kPfChunk] = base;
@@ -130,7 +151,7 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
 // steps ahead, so each wait is for one step's data only.  The token chunks of
 // one row block are neighbouring units, placed on one XCD, so they share the
 // down blocks in L2.
-constexpr int kRowAhead = 4;  // steps whose loads are in flight
+constexpr int kRowAhead = 3;  // steps whose loads are in flight
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -227,6 +248,22 @@ __device__ __forceinline__ void rows_run(DownRowsLds<R> &S, const RowStep &st, R
     if (c.k >= m) return;
     const int n = S.n[c.k], t16 = 16 * (wv + 8 * c.r);
     if (t16 >= n) return;
+    // lane: rows 4 (lane / 16) + i of each row tile, its slot's token.  The
+    // rows and all of the down block's fragments are read from LDS first (the
+    // barrier ordered the reads after the previous step's adds), then the
+    // products run back to back.
+    const bool own = t16 + (lane & 15) < n;
+    float *yr = &S.y[(own ? (int)st.tok - t0 : 0) * YS + 4 * (lane >> 4)];
+    float4 yv[MT];
+    uint4 a[MT][4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            a[mt][s] = *reinterpret_cast<const uint4 *>(&S.w[(mt * 4 + s) * 64 + lane]);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) yv[mt] = *reinterpret_cast<const float4 *>(yr + 16 * mt);
+    __builtin_amdgcn_sched_barrier(0);
     f32x4 acc[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -236,17 +273,14 @@ __device__ __forceinline__ void rows_run(DownRowsLds<R> &S, const RowStep &st, R
         const uint4 bl = *reinterpret_cast<const uint4 *>(&st.bl[s]);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const uint4 a = *reinterpret_cast<const uint4 *>(&S.w[(mt * 4 + s) * 64 + lane]);
-            acc[mt] = mfma16(a, bh, acc[mt]);
-            acc[mt] = mfma16(a, bl, acc[mt]);
+            acc[mt] = mfma16(a[mt][s], bh, acc[mt]);
+            acc[mt] = mfma16(a[mt][s], bl, acc[mt]);
         }
     }
-    // lane: rows 4 (lane / 16) + i of each row tile, its slot's token
-    if (t16 + (lane & 15) < n) {
-        float *yr = &S.y[((int)st.tok - t0) * YS + 4 * (lane >> 4)];
+    if (own) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            float4 v = *reinterpret_cast<float4 *>(yr + 16 * mt);
+            float4 v = yv[mt];
             v.x += acc[mt][0];
             v.y += acc[mt][1];
             v.z += acc[mt][2];
