@@ -60,22 +60,39 @@ __global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
     const int tb = blockIdx.x / P.KSr, ks = blockIdx.x - tb * P.KSr;
     if (P.build_plan && blockIdx.x == 0 && tid < P.E) P.emask[tid] = 0ull;
     const int s_end = min(kRouteWaves, P.NS - ks * kRouteWaves);  // K-steps in this slice
-    // stage the block's token rows of this slice as MFMA A fragments
+    // stage the block's token rows of this slice as MFMA A fragments; every
+    // load is issued (addresses clamped into the operands), then rows past T
+    // and K-steps past the slice are zeroed
     const uint4 z = make_uint4(0, 0, 0, 0);
+    {
+        const int s = wv, sc = min(s, s_end - 1);  // thread (wv, lane) stages K-step wv of every tile
+        uint4 v[kLgTiles];
 #pragma unroll
-    for (int i = 0; i < kLgTiles; ++i) {
-        const int j = i, s = wv, l = lane;  // thread (wv, lane) stages K-step wv of every tile
-        const int t = tb * 16 * kLgTiles + 16 * j + (l & 15);
-        xs[j][s][l] = (t < P.T && s < s_end)
-                          ? ldg16(P.x + (size_t)t * P.d + (ks * kRouteWaves + s) * kKStep + 8 * (l >> 4))
-                          : z;
+        for (int j = 0; j < kLgTiles; ++j) {
+            const int t = min(tb * 16 * kLgTiles + 16 * j + (lane & 15), P.T - 1);
+            v[j] = ldg16(P.x + (size_t)t * P.d + (ks * kRouteWaves + sc) * kKStep + 8 * (lane >> 4));
+        }
+#pragma unroll
+        for (int j = 0; j < kLgTiles; ++j) {
+            const int t = tb * 16 * kLgTiles + 16 * j + (lane & 15);
+            xs[j][s][lane] = (t < P.T && s < s_end) ? v[j] : z;
+        }
     }
     __syncthreads();
     if (wv >= P.nEt) return;
     // wavefront wv: expert tile wv for every token tile, K-steps of the slice
-    // accumulated in order in the MFMA accumulators
+    // accumulated in order in the MFMA accumulators; the slice's router
+    // fragments are all loaded first
     const int ec = wv * kRouteTile + (lane & 15);
     const bool ve = ec < P.E;
+    uint4 b[kRouteWaves];
+#pragma unroll
+    for (int s = 0; s < kRouteWaves; ++s) {
+        const int sc = min(s, s_end - 1);
+        const uint4 v = ldg16(P.Wr + (size_t)min(ec, P.E - 1) * P.d + (ks * kRouteWaves + sc) * kKStep +
+                              8 * (lane >> 4));
+        b[s] = ve ? v : z;
+    }
     f32x4 acc[kLgTiles];
 #pragma unroll
     for (int j = 0; j < kLgTiles; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -83,12 +100,9 @@ __global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
 #pragma unroll
     for (int s = 0; s < kRouteWaves; ++s) {
         if (s < s_end) {
-            const uint4 b = ve ? ldg16(P.Wr + (size_t)ec * P.d + (ks * kRouteWaves + s) * kKStep +
-                                       8 * (lane >> 4))
-                               : z;
 #pragma unroll
             for (int j = 0; j < kLgTiles; ++j)
-                if (j < ntile) acc[j] = mfma16(xs[j][s][lane], b, acc[j]);
+                if (j < ntile) acc[j] = mfma16(xs[j][s][lane], b[s], acc[j]);
         }
     }
     // lane holds tokens 4 (lane / 16) + i of each tile, expert ec
