@@ -79,41 +79,54 @@ __global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
         }
     }
     __syncthreads();
-    if (wv >= P.nEt) return;
     // wavefront wv: expert tile wv for every token tile, K-steps of the slice
     // accumulated in order in the MFMA accumulators; the slice's router
     // fragments are all loaded first
     const int ec = wv * kRouteTile + (lane & 15);
     const bool ve = ec < P.E;
-    uint4 b[kRouteWaves];
-#pragma unroll
-    for (int s = 0; s < kRouteWaves; ++s) {
-        const int sc = min(s, s_end - 1);
-        const uint4 v = ldg16(P.Wr + (size_t)min(ec, P.E - 1) * P.d + (ks * kRouteWaves + sc) * kKStep +
-                              8 * (lane >> 4));
-        b[s] = ve ? v : z;
-    }
     f32x4 acc[kLgTiles];
 #pragma unroll
     for (int j = 0; j < kLgTiles; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int ntile = min(kLgTiles, (P.T - tb * 16 * kLgTiles + 15) / 16);
+    if (wv < P.nEt) {
+        uint4 b[kRouteWaves];
 #pragma unroll
-    for (int s = 0; s < kRouteWaves; ++s) {
-        if (s < s_end) {
+        for (int s = 0; s < kRouteWaves; ++s) {
+            const int sc = min(s, s_end - 1);
+            const uint4 v = ldg16(P.Wr + (size_t)min(ec, P.E - 1) * P.d +
+                                  (ks * kRouteWaves + sc) * kKStep + 8 * (lane >> 4));
+            b[s] = ve ? v : z;
+        }
+        const int ntile = min(kLgTiles, (P.T - tb * 16 * kLgTiles + 15) / 16);
 #pragma unroll
-            for (int j = 0; j < kLgTiles; ++j)
-                if (j < ntile) acc[j] = mfma16(xs[j][s][lane], b[s], acc[j]);
+        for (int s = 0; s < kRouteWaves; ++s) {
+            if (s < s_end) {
+#pragma unroll
+                for (int j = 0; j < kLgTiles; ++j)
+                    if (j < ntile) acc[j] = mfma16(xs[j][s][lane], b[s], acc[j]);
+            }
         }
     }
-    // lane holds tokens 4 (lane / 16) + i of each tile, expert ec
-    if (!ve) return;
+    // the block's partial logits are one contiguous [rows][E] range of the
+    // slice: staged in LDS (lane holds tokens 4 (lane / 16) + i of each tile,
+    // expert ec), then written out with whole-row stores
+    __syncthreads();
+    float *ob = reinterpret_cast<float *>(&xs[0][0][0]);
+    static_assert(sizeof(xs) >= 16 * kLgTiles * kMaxExperts * sizeof(float), "staging fits");
+    if (wv < P.nEt && ve) {
 #pragma unroll
-    for (int j = 0; j < kLgTiles; ++j) {
+        for (int j = 0; j < kLgTiles; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int t = tb * 16 * kLgTiles + 16 * j + 4 * (lane >> 4) + i;
-            if (t < P.T) P.gpart[((size_t)ks * P.T + t) * P.E + ec] = acc[j][i];
-        }
+            for (int i = 0; i < 4; ++i) ob[(16 * j + 4 * (lane >> 4) + i) * P.E + ec] = acc[j][i];
+    }
+    __syncthreads();
+    const int t0 = tb * 16 * kLgTiles, rows = min(16 * kLgTiles, P.T - t0);
+    float *dst = P.gpart + ((size_t)ks * P.T + t0) * P.E;
+    const int n = rows * P.E;
+    if (P.E % 4 == 0) {
+        for (int i = tid; 4 * i < n; i += blockDim.x)
+            reinterpret_cast<float4 *>(dst)[i] = reinterpret_cast<const float4 *>(ob)[i];
+    } else {
+        for (int i = tid; i < n; i += blockDim.x) dst[i] = ob[i];
     }
 }
 
@@ -163,46 +176,60 @@ __device__ __forceinline__ unsigned long long pi_key(float g, int i) {
     return ((unsigned long long)u << 32) | (uint32_t)(0xFFFFFFFFu - (uint32_t)i);
 }
 
-// Routes one token per workgroup of kSelThreads threads.
+// Routes TPB tokens per workgroup of kSelThreads threads (kSelThreads / TPB
+// threads per token, at least one per expert).
 //   1. thread e < E: g_e = (sum of the K-slice partials in slice order + b_e)
 //      * inv_temp; g_max by a max reduction; e_e = exp(g_e - g_max).
 //   2. S = sum of e over the experts (lane order, then the wavefront sum).
 //   3. rank_i = #{j before i in pi} and B_i = sum of e_j over j before i,
-//      counted by (slice of j, i) threads and summed slice by slice.  Then
-//      C at position rank_i + 1 is (B_i + e_i) / S and C before it is B_i / S.
+//      counted per (slice of j, i) -- kSelThreads / EP slices of j, each
+//      summed in j order, by one thread per (slice, i) or one thread taking
+//      several slices in turn -- then summed slice by slice.  C at position
+//      rank_i + 1 is (B_i + e_i) / S and C before it is B_i / S.
 //   4. nucleus: expert i is kept iff rank_i == 0 or B_i / S < tau (every
 //      expert when tau >= 1), so k = #kept = min{i : C_i >= tau};
 //      strict: m = #{i : rank_i < E - 1, (B_i + e_i) / S < tau},
 //      k = max(1, m + [tau > 1]); top-k: k = round(tau) in [1, E];
 //      LTE: k = #{i : sigmoid(g_i) > tau}.  Kept iff rank_i < k.
 // Floating-point addition is monotone, so B grows with the rank and the kept
-// set is always a prefix of pi.  The work is O(E^2 / threads) with no
-// dependence on k; all orders of summation are fixed, independent of T.
+// set is always a prefix of pi.  The work is O(E^2) per token with no
+// dependence on k; all orders of summation are fixed and the same for every
+// TPB, so a token's selection does not depend on T or on the launch.
 constexpr int kSelThreads = 512;
 
 // Sum over the wavefront of one value per lane, in one fixed order, returned
 // identically to every lane.
 __device__ __forceinline__ float wave_sum(float v) { return lane_value(wave_scan_f32(v), 63); }
 
+template <int TPB>
 __global__ __launch_bounds__(kSelThreads) void select_k(RouteParams P) {
-    __shared__ uint4 kk[kMaxExperts];  // (key lo, key hi, e bits, -)
-    __shared__ float2 part[kSelThreads];
+    constexpr int TH = kSelThreads / TPB;  // threads per token
+    constexpr int WPT = TH / 64;           // wavefronts per token
+    static_assert(TH % 64 == 0, "whole wavefronts per token");
+    __shared__ uint4 kk[TPB][kMaxExperts];  // (key lo, key hi, e bits, -)
+    __shared__ float2 part[TPB][kSelThreads];
     __shared__ float wmax[kSelThreads / 64];
-    __shared__ uint32_t sm[8];
-    const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    __shared__ uint32_t sm[TPB][8];
+    __shared__ int kc[TPB];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int u = tid / TH, tt = tid - u * TH;  // token of the block, thread of the token
+    const int t = blockIdx.x * TPB + u;
+    const bool live = t < P.T;
+    const int tc = live ? t : P.T - 1;
     const int E = P.E;
     const bool strict = (P.flags & PP_SELECT_STRICT) != 0;
     const bool all = strict ? (P.tau > 1.0f) : (P.tau >= 1.0f);
-    if (tid < 8) sm[tid] = 0u;
+    if (tt < 8) sm[u][tt] = 0u;
+    if (tt == 0) kc[u] = 0;
     // 1. logits (all partial loads issued before the sum)
     float g = -INFINITY;
-    if (tid < E) {
+    if (tt < E) {
         float v[kMaxSlices];
 #pragma unroll
         for (int k = 0; k < kMaxSlices; ++k)
-            v[k] = P.gpart[((size_t)min(k, P.KSr - 1) * P.T + t) * E + tid];
-        const float b = P.bias[tid];
-        const float it = P.inv_temp ? P.inv_temp[t] : 1.0f;
+            v[k] = P.gpart[((size_t)min(k, P.KSr - 1) * P.T + tc) * E + tt];
+        const float b = P.bias[tt];
+        const float it = P.inv_temp ? P.inv_temp[tc] : 1.0f;
         float sum = 0.0f;
 #pragma unroll
         for (int k = 0; k < kMaxSlices; ++k)
@@ -215,55 +242,57 @@ __global__ __launch_bounds__(kSelThreads) void select_k(RouteParams P) {
         m = fmaxf(m, __uint_as_float(xor_lane_rt(__float_as_uint(m), st, lane)));
     if (lane == 0) wmax[wv] = m;
     __syncthreads();
-    float gmax = wmax[0];
+    float gmax = wmax[u * WPT];
 #pragma unroll
-    for (int w = 1; w < kSelThreads / 64; ++w) gmax = fmaxf(gmax, wmax[w]);
-    const float ex = (tid < E) ? expf(g - gmax) : 0.0f;
-    const unsigned long long key = pi_key(g, tid);
+    for (int w = 1; w < WPT; ++w) gmax = fmaxf(gmax, wmax[u * WPT + w]);
+    const float ex = (tt < E) ? expf(g - gmax) : 0.0f;
+    const unsigned long long key = pi_key(g, tt);
     // entries past E are zero keys, which come after every expert
-    if (tid < kMaxExperts)
-        kk[tid] = tid < E ? make_uint4((uint32_t)key, (uint32_t)(key >> 32), __float_as_uint(ex), 0u)
-                          : make_uint4(0u, 0u, 0u, 0u);
+    const int EP = E <= 64 ? 64 : (E <= 128 ? 128 : 256);
+    if (tt < EP)
+        kk[u][tt] = tt < E ? make_uint4((uint32_t)key, (uint32_t)(key >> 32), __float_as_uint(ex), 0u)
+                           : make_uint4(0u, 0u, 0u, 0u);
     __syncthreads();
     // 2. S, computed the same way by every wavefront
     float sl = 0.0f;
-    for (int i = lane; i < E; i += 64) sl += __uint_as_float(kk[i].z);
+    for (int i = lane; i < E; i += 64) sl += __uint_as_float(kk[u][i].z);
     const float S = wave_sum(sl);
-    // 3. ranks and preceding mass; EP = E rounded up to a power of two >= 64
-    const int EP = E <= 64 ? 64 : (E <= 128 ? 128 : 256);
+    // 3. ranks and preceding mass: (slice q of j, i) for q < nsl, i < EP
     const int nsl = kSelThreads / EP;
     {
-        const int i = tid & (EP - 1), sl_i = tid / EP;
-        // slice of j: [j0, j0 + per), per a multiple of 4; the slices cover
-        // 0..E-1 and stay inside the kMaxExperts entries of kk
+        const int i = tt & (EP - 1);
+        // slice of j: [q per, q per + per), per a multiple of 4; the slices
+        // cover 0..E-1 and stay inside the EP entries of kk
         const int per = (((E + nsl - 1) / nsl) + 3) & ~3;
-        const int j0 = sl_i * per;
-        float bm = 0.0f;
-        int cnt = 0;
-        if (i < E) {
-            const uint4 me = kk[i];
-            const unsigned long long ki = ((unsigned long long)me.y << 32) | me.x;
-            for (int j = j0; j < j0 + per; j += 4) {
-                uint4 o[4];
+        const int tq = TH >= EP ? TH / EP : 1;  // threads per expert: slices q = tt / EP + tq r
+        const unsigned long long ki =
+            i < E ? (((unsigned long long)kk[u][i].y << 32) | kk[u][i].x) : 0ull;
+        for (int q = tt / EP; q < nsl; q += tq) {
+            float bm = 0.0f;
+            int cnt = 0;
+            if (i < E) {
+                for (int j = q * per; j < q * per + per; j += 4) {
+                    uint4 o[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) o[u] = kk[j + u];
+                    for (int w = 0; w < 4; ++w) o[w] = kk[u][j + w];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const bool bef = (((unsigned long long)o[u].y << 32) | o[u].x) > ki;
-                    bm += bef ? __uint_as_float(o[u].z) : 0.0f;
-                    cnt += bef ? 1 : 0;
+                    for (int w = 0; w < 4; ++w) {
+                        const bool bef = (((unsigned long long)o[w].y << 32) | o[w].x) > ki;
+                        bm += bef ? __uint_as_float(o[w].z) : 0.0f;
+                        cnt += bef ? 1 : 0;
+                    }
                 }
             }
+            part[u][q * EP + i] = make_float2(bm, __int_as_float(cnt));
         }
-        part[tid] = make_float2(bm, __int_as_float(cnt));
     }
     __syncthreads();
     // 4. the tau cut
     float B = 0.0f;
     int rank = 0;
-    if (tid < E) {
+    if (tt < E) {
         for (int q = 0; q < nsl; ++q) {
-            const float2 pq = part[q * EP + tid];
+            const float2 pq = part[u][q * EP + tt];
             B += pq.x;
             rank += __float_as_int(pq.y);
         }
@@ -272,7 +301,7 @@ __global__ __launch_bounds__(kSelThreads) void select_k(RouteParams P) {
     const bool lte = (P.flags & PP_SELECT_LTE) != 0;
     const float sg = 1.0f / (1.0f + expf(-g));  // sigmoid(g_e): LTE score and gate
     int cond = 0;
-    if (tid < E) {
+    if (tt < E) {
         if (lte)
             cond = sg > P.tau ? 1 : 0;
         else if (strict)
@@ -280,7 +309,12 @@ __global__ __launch_bounds__(kSelThreads) void select_k(RouteParams P) {
         else
             cond = (all || rank == 0 || B / S < P.tau) ? 1 : 0;
     }
-    int k = __syncthreads_count(cond);
+    {
+        const int wc = __popcll(__ballot(cond));
+        if (lane == 0) atomicAdd(&kc[u], wc);
+    }
+    __syncthreads();
+    int k = kc[u];
     if (topk) {
         k = (int)fminf(floorf(P.tau + 0.5f), (float)E);
         k = k < 1 ? 1 : k;
@@ -289,23 +323,23 @@ __global__ __launch_bounds__(kSelThreads) void select_k(RouteParams P) {
         k = k < 1 ? 1 : k;
     }
     // 5. outputs: slot rank_i of token t holds expert i if kept, else nothing
-    if (tid < E) {
+    if (tt < E && live) {
         const bool kept = rank < k;
         const bool sig = (P.flags & PP_AGG_SIGMOID) != 0;
         const float w = sig ? sg : 1.0f;
-        P.idx[(size_t)t * E + rank] = kept ? tid : -1;
+        P.idx[(size_t)t * E + rank] = kept ? tt : -1;
         if (P.gate_w) P.gate_w[(size_t)t * E + rank] = kept ? w : 0.0f;
         if (kept) {
-            P.gsig[(size_t)t * E + tid] = w;
-            atomicOr(&sm[tid >> 5], 1u << (tid & 31));
+            P.gsig[(size_t)t * E + tt] = w;
+            atomicOr(&sm[u][tt >> 5], 1u << (tt & 31));
             if (P.build_plan)
-                __hip_atomic_fetch_or(P.emask + tid, 1ull << t, __ATOMIC_RELAXED,
+                __hip_atomic_fetch_or(P.emask + tt, 1ull << t, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT);
         }
     }
     __syncthreads();
-    if (tid < 8) P.selmask[(size_t)t * 8 + tid] = sm[tid];
-    if (tid == 0) P.count[t] = k;
+    if (tt < 8 && live) P.selmask[(size_t)t * 8 + tt] = sm[u][tt];
+    if (tt == 0 && live) P.count[t] = k;
 }
 
 }  // namespace
@@ -343,7 +377,12 @@ hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const 
         const int nTb = (T + 16 * kLgTiles - 1) / (16 * kLgTiles);
         hipLaunchKernelGGL(logits_k, dim3(nTb * P.KSr), dim3(1024), 0, s, P);
     }
-    hipLaunchKernelGGL(select_k, dim3(T), dim3(kSelThreads), 0, s, P);
+    // small batches: one token per workgroup (shortest latency); large ones:
+    // four tokens of 128 threads per workgroup (one workgroup wave on the chip)
+    if (T > kDecodeTile && dm.E <= 128)
+        hipLaunchKernelGGL(select_k<4>, dim3((T + 3) / 4), dim3(kSelThreads), 0, s, P);
+    else
+        hipLaunchKernelGGL(select_k<1>, dim3(T), dim3(kSelThreads), 0, s, P);
     prof_mark(L, PP_KERNEL_ROUTE, s, false);
     return hipGetLastError();
 }
