@@ -157,7 +157,9 @@ pp_status prunepath_ffn_decode(pp_layer *L, const uint16_t *x, int32_t T, float 
 /* prunepath_ffn_prefill -- same result as prunepath_ffn_decode (up to fp32
  * summation order), organised for long token batches: tokens are bucketed per
  * kept expert and each expert's bucket runs as a grouped bf16 MFMA GEMM
- * (the multi-token dispatch described in Sec. 4.5). */
+ * (the multi-token dispatch described in Sec. 4.5).  Deterministic: no
+ * floating-point atomics; each token's expert contributions are added to the
+ * output (bias) in ascending expert order. */
 pp_status prunepath_ffn_prefill(pp_layer *L, const uint16_t *x, int32_t T, float tau,
                                 const float *inv_temp, float *y, int32_t *expert_idx,
                                 int32_t *count, void *hip_stream);

@@ -7,9 +7,10 @@
 // row of the h scratch, rows numbered group by group, tokens ascending inside
 // a group.
 //
-//   dispatch_k  : per expert, the ascending list of tokens that kept it (block
-//                 scan + scatter), where each chunk of kPfChunk tokens starts
-//                 in it, and the plan, written by the last expert to finish.
+//   dispatch_k  : per expert, the ascending list of tokens that kept it
+//                 (ballot prefix over blocks of 256 tokens + scatter), where
+//                 each chunk of kPfChunk tokens starts in it, and the plan,
+//                 written by the last expert to finish.
 //   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
 //                 SiLU product of one group (shared with the decode kernel).
 //   down_rows_k : unit = (R rows of d, chunk of kPfChunk tokens); the chunk's
