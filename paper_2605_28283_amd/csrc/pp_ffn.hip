@@ -160,32 +160,39 @@ template <int R>
 struct DownRowsLds {
     float y[kPfChunk * (R + 4)];  // [token][row], rows padded by 4 floats
     u32x4_t w[R / 16 * 4 * 64];   // [row tile][K-step][lane]: A fragments
-    int e[kMaxExperts];           // experts with tokens in the chunk, ascending
-    int a[kMaxExperts];           // their run's first bucket position
-    int n[kMaxExperts];           // tokens in the run
-    int p[kMaxExperts];           // first pair (h row) of the run
+    int4 ent[kMaxExperts];        // experts with tokens in the chunk, ascending:
+                                  // (expert, tokens in the run, first pair (h row)
+                                  // of the run, its first bucket position)
     int m, steps;
 };
 
-// One step's loads as held by a thread.
+// One step's loads as held by a thread, with the step's (wavefront-uniform)
+// description: list entry k (m past the list), tokens n of its run and the
+// first place t16 of the wavefront's tile in the run.
 struct RowStep {
     u32x4_t w0, w1;         // its share of the down block (R = 64: both)
     u32x4_t bh[4], bl[4];   // the wavefront's tile: h hi / lo B fragments
     unsigned tok;           // token of the lane's slot (0 past the run)
+    int k, n, t16;
 };
 
 // Steps in order: list entry k, round r (tiles 8 r .. 8 r + 7 of its run).
+// The cursor carries its entry and the next one (read one step ahead), so
+// moving on needs no LDS round trip.
 struct RowCursor {
     int k, r;
+    int4 cur, next;
 };
 
 template <int R>
 __device__ __forceinline__ void rows_next(RowCursor &c, const DownRowsLds<R> &S, int m) {
-    if (c.k < m && 8 * 16 * (c.r + 1) < S.n[c.k]) {
+    if (c.k < m && 8 * 16 * (c.r + 1) < c.cur.y) {
         ++c.r;
     } else {
         ++c.k;
         c.r = 0;
+        c.cur = c.next;
+        c.next = S.ent[min(c.k + 1, m - 1)];
     }
 }
 
@@ -202,21 +209,23 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void *base, un
 
 // Issues step c's loads (past the list: all out of range, zeros).
 template <int R>
-__device__ __forceinline__ void rows_issue(RowStep &st, const DNParams &P, const DownRowsLds<R> &S,
-                                           RowCursor c, int m, int rb, int tid) {
+__device__ __forceinline__ void rows_issue(RowStep &st, const DNParams &P, const RowCursor &c,
+                                           int m, int rb, int tid) {
     constexpr int MT = R / 16, WN = MT * 4 * 64;
     static_assert(WN <= 2 * 512, "at most two uint4 of a down block per thread");
     // every descriptor operand is wavefront-uniform, so it lives in SGPRs
     const int lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ck = __builtin_amdgcn_readfirstlane(c.k), cr = __builtin_amdgcn_readfirstlane(c.r);
     const bool live = ck < m;
-    const int kc = live ? ck : 0;
-    const int e = __builtin_amdgcn_readfirstlane(S.e[kc]);
-    const int n = live ? __builtin_amdgcn_readfirstlane(S.n[kc]) : 0;
-    const int p0 = __builtin_amdgcn_readfirstlane(S.p[kc]);
-    const int a0 = __builtin_amdgcn_readfirstlane(S.a[kc]);
-    const int t16 = 16 * (wv + 8 * cr);  // the tile's first place in the run
+    const int e = __builtin_amdgcn_readfirstlane(c.cur.x);
+    const int n = live ? __builtin_amdgcn_readfirstlane(c.cur.y) : 0;
+    const int p0 = __builtin_amdgcn_readfirstlane(c.cur.z);
+    const int a0 = __builtin_amdgcn_readfirstlane(c.cur.w);
+    const int t16 = 16 * (wv + 8 * cr);       // the tile's first place in the run
     const int nt = max(0, min(16, n - t16));  // tokens in the tile
+    st.k = live ? ck : m;
+    st.n = n;
+    st.t16 = t16;
     // down block: contiguous WN uint4
     const auto rw = rows_rsrc(P.Wd + ((size_t)e * (P.d / 16) + (size_t)rb * MT) * 256 * 8,
                               live ? WN * 16u : 0u);
@@ -236,19 +245,19 @@ __device__ __forceinline__ void rows_issue(RowStep &st, const DNParams &P, const
     st.tok = __builtin_amdgcn_raw_buffer_load_b32(rt, (unsigned)(lane & 15) * 4u, 0, 0);
 }
 
-// Runs step c: its down block to LDS, then the wavefront's tile.
+// Runs step st: its down block to LDS, then the wavefront's tile.
 template <int R>
-__device__ __forceinline__ void rows_run(DownRowsLds<R> &S, const RowStep &st, RowCursor c, int m,
-                                         int t0, int tid) {
+__device__ __forceinline__ void rows_run(DownRowsLds<R> &S, const RowStep &st, int m, int t0,
+                                         int tid) {
     constexpr int MT = R / 16, YS = R + 4, WN = MT * 4 * 64;
-    const int lane = tid & 63, wv = tid >> 6;
+    const int lane = tid & 63;
     __syncthreads();  // the previous step's block and rows are done with
     if (WN >= 512 || tid < WN) S.w[tid] = st.w0;
     if (WN > 512) S.w[512 + tid] = st.w1;
     __syncthreads();
-    if (c.k >= m) return;
-    const int n = S.n[c.k], t16 = 16 * (wv + 8 * c.r);
-    if (t16 >= n) return;
+    const int k = __builtin_amdgcn_readfirstlane(st.k), n = __builtin_amdgcn_readfirstlane(st.n);
+    const int t16 = __builtin_amdgcn_readfirstlane(st.t16);
+    if (k >= m || t16 >= n) return;
     // lane: rows 4 (lane / 16) + i of each row tile, its slot's token.  The
     // rows and all of the down block's fragments are read from LDS first (the
     // barrier ordered the reads after the previous step's adds), then the
@@ -314,13 +323,9 @@ __global__ __launch_bounds__(512, 1) void down_rows_k(DNParams P) {
                     b = P.cut[(size_t)e * P.ncut + c + 1];
                 }
                 const unsigned long long bal = __ballot(b > a);
-                if (b > a) {
-                    const int k = m + __popcll(bal & ((1ull << lane) - 1ull));
-                    S.e[k] = e;
-                    S.a[k] = a;
-                    S.n[k] = b - a;
-                    S.p[k] = P.ebase[e] + a;
-                }
+                if (b > a)
+                    S.ent[m + __popcll(bal & ((1ull << lane) - 1ull))] =
+                        make_int4(e, b - a, P.ebase[e] + a, a);
                 m += __popcll(bal);
                 const int rounds = b > a ? (b - a + 127) / 128 : 0;
                 steps += __builtin_amdgcn_readlane(wave_scan_i32(rounds), 63);
@@ -340,18 +345,17 @@ __global__ __launch_bounds__(512, 1) void down_rows_k(DNParams P) {
         const int m = S.m, steps = S.steps;
         if (m > 0) {
             RowStep st[kRowAhead];
-            RowCursor ci = {0, 0}, cr = {0, 0};  // next step to issue / to run
+            RowCursor ci = {0, 0, S.ent[0], S.ent[min(1, m - 1)]};  // next step to issue
 #pragma unroll
             for (int i = 0; i < kRowAhead; ++i) {
-                rows_issue<R>(st[i], P, S, ci, m, rb, tid);
+                rows_issue<R>(st[i], P, ci, m, rb, tid);
                 rows_next<R>(ci, S, m);
             }
             for (int s0 = 0; s0 < steps; s0 += kRowAhead) {
 #pragma unroll
                 for (int i = 0; i < kRowAhead; ++i) {
-                    rows_run<R>(S, st[i], cr, m, t0, tid);
-                    rows_next<R>(cr, S, m);
-                    rows_issue<R>(st[i], P, S, ci, m, rb, tid);
+                    rows_run<R>(S, st[i], m, t0, tid);
+                    rows_issue<R>(st[i], P, ci, m, rb, tid);
                     rows_next<R>(ci, S, m);
                 }
             }
