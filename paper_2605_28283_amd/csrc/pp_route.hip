@@ -6,13 +6,15 @@
 //            operands; wavefront w takes expert tile w (16 experts) for all
 //            four token tiles and accumulates the slice's 16 K-steps in order
 //            in the MFMA accumulators (bf16 MFMA 16x16x32, fp32), storing the
-//            slice's partial logits.  select_k sums the slices in slice order.
+//            slice's partial logits, staged in LDS and written as whole rows.
+//            select_k sums the slices in slice order.
 //            Every logit is formed in an order that depends on d only, never on
 //            T or on the other tokens, so a token's logits are the same bits in
 //            any batch: routing is batch-invariant.  Batches of up to 64 tokens
 //            use logits_small_k (one wavefront per token tile x expert tile x
 //            slice, the same MFMA chain).
-// select_k : one workgroup per token.  pi orders experts by descending g,
+// select_k : one token per workgroup (four per workgroup for batches past 64
+//            tokens with E <= 128; the same sums).  pi orders experts by descending g,
 //            equal g by ascending expert index (ordering g orders p: softmax is
 //            monotone).  With e_i = exp(g_i - g_max), S = sum e and
 //            C_i = (e_pi1 + ... + e_pii) / S:
