@@ -413,38 +413,45 @@ struct DnRow {
     float yacc[kDnThreads / 64][TB][16 * R + 4];
 };
 
-// This wavefront's 16 x 128 block of group u's down weights.
+// This wavefront's 16 x 128 block of group u's down weights (row tile rt,
+// clamped into d: a wavefront past d loads the last tile and discards it).
 __device__ __forceinline__ void sh_load_w(const DNParams &P, int u, int rt, int RT, int lane,
                                           uint4 (&w)[4]) {
-    const uint16_t *wp = P.Wd + (((size_t)P.plan.grp_e[u] * RT + rt) * 4 * 64 + lane) * 8;
+    const uint16_t *wp =
+        P.Wd + (((size_t)P.plan.grp_e[u] * RT + min(rt, RT - 1)) * 4 * 64 + lane) * 8;
 #pragma unroll
     for (int s = 0; s < 4; ++s) w[s] = ldg16(wp + s * 512);
 }
 
 // Piece wv (hi/lo x K-step) of group u's h B fragments and the tokens of
-// this lane's slot, for every 16-token tile.
+// this lane's slot, for every 16-token tile.  Bounds-checked buffer loads:
+// every load is issued, slots past the group read zeros (their outputs are
+// never stored), so the waits for a group's data count only later loads.
 __device__ __forceinline__ void sh_load_h(const DNParams &P, int u, int wv, int lane,
-                                          uint4 (&hp)[kShTiles], int (&tp)[kShTiles]) {
+                                          uint4 (&hp)[kShTiles], unsigned (&tp)[kShTiles]) {
     const int n = P.plan.grp_n[u], p0 = P.plan.grp_pair[u], tk = P.plan.grp_tok[u];
-    const uint16_t *src = (wv < 4) ? P.h_hi : P.h_lo;
-    const int col = (wv & 3) * kKStep + 8 * (lane >> 4);
+    const uint16_t *src = (__builtin_amdgcn_readfirstlane(wv) < 4) ? P.h_hi : P.h_lo;
+    const auto rh = buf_rsrc(src + (size_t)p0 * kExpertWidth, (unsigned)n * kExpertWidth * 2u);
+    const auto rt = buf_rsrc(P.plan.toklist + tk, (unsigned)n * 4u);
+    const unsigned col = ((wv & 3) * kKStep + 8 * (lane >> 4)) * 2u;
 #pragma unroll
     for (int j = 0; j < kShTiles; ++j) {
-        const int slot = 16 * j + (lane & 15);
-        const bool ok = slot < n;
-        hp[j] = ok ? ldg16(src + (size_t)(p0 + slot) * kExpertWidth + col) : make_uint4(0, 0, 0, 0);
-        tp[j] = ok ? P.plan.toklist[tk + slot] : -1;
+        const unsigned slot = 16 * j + (lane & 15);
+        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rh, slot * kExpertWidth * 2u + col, 0, 0);
+        hp[j] = make_uint4(v.x, v.y, v.z, v.w);
+        tp[j] = __builtin_amdgcn_raw_buffer_load_b32(rt, slot * 4u, 0, 0);
     }
 }
 
 // One group of a dense unit: stage its h in LDS, reuse hp for group u + 2's
-// h, multiply, reuse wc for group u + 2's weights (both two groups ahead).
+// h, multiply, reuse wc for group u + 2's weights (both two groups ahead,
+// clamped to the chunk's last group so that every group issues the same loads).
 __device__ __forceinline__ void sh_group(const DNParams &P, DnShared &S, int u, int u1, int rt,
                                          int RT, bool rows_ok, int wv, int lane,
-                                         uint4 (&hp)[kShTiles], int (&tp)[kShTiles],
+                                         uint4 (&hp)[kShTiles], unsigned (&tp)[kShTiles],
                                          uint4 (&wc)[4]) {
-    const int nt = (P.plan.grp_n[u] + 15) >> 4;
-    int tok[kShTiles];
+    const int n = P.plan.grp_n[u], nt = (n + 15) >> 4;
+    unsigned tok[kShTiles];
     __syncthreads();  // every wavefront is done with the previous group's h
 #pragma unroll
     for (int j = 0; j < kShTiles; ++j) {
@@ -452,31 +459,33 @@ __device__ __forceinline__ void sh_group(const DNParams &P, DnShared &S, int u, 
         tok[j] = tp[j];
     }
     __syncthreads();
-    if (u + 2 < u1) sh_load_h(P, u + 2, wv, lane, hp, tp);
-    if (!rows_ok) return;
-    for (int j = 0; j < nt; ++j) {
-        f32x4 a = {0.f, 0.f, 0.f, 0.f};
+    const int un = min(u + 2, u1 - 1);
+    sh_load_h(P, un, wv, lane, hp, tp);
+    if (rows_ok) {
+        for (int j = 0; j < nt; ++j) {
+            f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            a = mfma16(wc[s], S.hb[j][s][lane], a);
-            a = mfma16(wc[s], S.hb[j][4 + s][lane], a);
-        }
-        int t = tok[0];
+            for (int s = 0; s < 4; ++s) {
+                a = mfma16(wc[s], S.hb[j][s][lane], a);
+                a = mfma16(wc[s], S.hb[j][4 + s][lane], a);
+            }
+            unsigned t = tok[0];
 #pragma unroll
-        for (int q = 1; q < kShTiles; ++q)
-            if (j == q) t = tok[q];
-        // lane holds rows 4 (lane / 16) + i of the wavefront's tile, token slot lane % 16
-        if (t >= 0) {
-            float4 *dst = reinterpret_cast<float4 *>(&S.yacc[t][wv * 16 + 4 * (lane >> 4)]);
-            float4 v = *dst;
-            v.x += a[0];
-            v.y += a[1];
-            v.z += a[2];
-            v.w += a[3];
-            *dst = v;
+            for (int q = 1; q < kShTiles; ++q)
+                if (j == q) t = tok[q];
+            // lane holds rows 4 (lane / 16) + i of the wavefront's tile, token slot lane % 16
+            if (16 * j + (lane & 15) < n) {
+                float4 *dst = reinterpret_cast<float4 *>(&S.yacc[t][wv * 16 + 4 * (lane >> 4)]);
+                float4 v = *dst;
+                v.x += a[0];
+                v.y += a[1];
+                v.z += a[2];
+                v.w += a[3];
+                *dst = v;
+            }
         }
     }
-    if (u + 2 < u1) sh_load_w(P, u + 2, rt, RT, lane, wc);
+    sh_load_w(P, un, rt, RT, lane, wc);
 }
 
 // Dense unit = (chunk c of Uc groups, 128 rows of d): the 8 wavefronts own 16
@@ -492,13 +501,12 @@ __device__ void sh_unit(const DNParams &P, DnShared &S, int c, int rb, int Uc, i
     for (int i = tid; i < T * kShYS; i += blockDim.x) S.yacc[i / kShYS][i % kShYS] = 0.0f;
     const int u0 = c * Uc, u1 = min(nU, u0 + Uc);
     uint4 w0[4], w1[4], hp0[kShTiles], hp1[kShTiles];
-    int tp0[kShTiles], tp1[kShTiles];
-    if (rows_ok) {
-        sh_load_w(P, u0, rt, RT, lane, w0);
-        if (u0 + 1 < u1) sh_load_w(P, u0 + 1, rt, RT, lane, w1);
-    }
+    unsigned tp0[kShTiles], tp1[kShTiles];
+    const int u0n = min(u0 + 1, u1 - 1);
+    sh_load_w(P, u0, rt, RT, lane, w0);
     sh_load_h(P, u0, wv, lane, hp0, tp0);
-    if (u0 + 1 < u1) sh_load_h(P, u0 + 1, wv, lane, hp1, tp1);
+    sh_load_w(P, u0n, rt, RT, lane, w1);
+    sh_load_h(P, u0n, wv, lane, hp1, tp1);
     for (int u = u0; u < u1; u += 2) {
         sh_group(P, S, u, u1, rt, RT, rows_ok, wv, lane, hp0, tp0, w0);
         if (u + 1 >= u1) break;

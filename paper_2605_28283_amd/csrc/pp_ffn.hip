@@ -154,7 +154,6 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
 // down blocks in L2.
 constexpr int kRowAhead = 3;  // steps whose loads are in flight
 
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 template <int R>
 struct DownRowsLds {
@@ -196,17 +195,6 @@ __device__ __forceinline__ void rows_next(RowCursor &c, const DownRowsLds<R> &S,
     }
 }
 
-// A raw buffer over [base, base + bytes): loads past it read zeros without a
-// memory access.  base and bytes are wavefront-uniform (scalar registers).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const void *base, unsigned bytes) {
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-    const uint32_t nb = __builtin_amdgcn_readfirstlane(bytes);
-    return __builtin_amdgcn_make_buffer_rsrc(
-        reinterpret_cast<void *>(((uint64_t)hi << 32) | lo), (short)0, (int)nb, 0x00020000);
-}
-
 // Issues step c's loads (past the list: all out of range, zeros).
 template <int R>
 __device__ __forceinline__ void rows_issue(RowStep &st, const DNParams &P, const RowCursor &c,
@@ -227,21 +215,21 @@ __device__ __forceinline__ void rows_issue(RowStep &st, const DNParams &P, const
     st.n = n;
     st.t16 = t16;
     // down block: contiguous WN uint4
-    const auto rw = rows_rsrc(P.Wd + ((size_t)e * (P.d / 16) + (size_t)rb * MT) * 256 * 8,
+    const auto rw = buf_rsrc(P.Wd + ((size_t)e * (P.d / 16) + (size_t)rb * MT) * 256 * 8,
                               live ? WN * 16u : 0u);
     st.w0 = __builtin_amdgcn_raw_buffer_load_b128(rw, (unsigned)tid * 16u, 0, 0);
     if (WN > 512) st.w1 = __builtin_amdgcn_raw_buffer_load_b128(rw, (unsigned)(512 + tid) * 16u, 0, 0);
     // the tile's h rows and tokens
     const size_t q0 = (size_t)p0 + t16;
-    const auto rh = rows_rsrc(P.h_hi + q0 * kExpertWidth, (unsigned)nt * kExpertWidth * 2u);
-    const auto rl = rows_rsrc(P.h_lo + q0 * kExpertWidth, (unsigned)nt * kExpertWidth * 2u);
+    const auto rh = buf_rsrc(P.h_hi + q0 * kExpertWidth, (unsigned)nt * kExpertWidth * 2u);
+    const auto rl = buf_rsrc(P.h_lo + q0 * kExpertWidth, (unsigned)nt * kExpertWidth * 2u);
     const unsigned o = ((unsigned)(lane & 15) * kExpertWidth + 8u * (lane >> 4)) * 2u;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
         st.bh[s] = __builtin_amdgcn_raw_buffer_load_b128(rh, o + s * kKStep * 2u, 0, 0);
         st.bl[s] = __builtin_amdgcn_raw_buffer_load_b128(rl, o + s * kKStep * 2u, 0, 0);
     }
-    const auto rt = rows_rsrc(P.plan.toklist + (size_t)e * P.tstride + a0 + t16, (unsigned)nt * 4u);
+    const auto rt = buf_rsrc(P.plan.toklist + (size_t)e * P.tstride + a0 + t16, (unsigned)nt * 4u);
     st.tok = __builtin_amdgcn_raw_buffer_load_b32(rt, (unsigned)(lane & 15) * 4u, 0, 0);
 }
 

@@ -171,6 +171,20 @@ __device__ __forceinline__ uint4 ldg16(const void *p) {
     return *reinterpret_cast<const uint4 *>(p);
 }
 
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// A raw buffer over [base, base + bytes): loads past it read zeros without a
+// memory access, so a load can be issued whether or not its lane has data.
+// base and bytes must be wavefront-uniform; they are moved to scalar registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *base, unsigned bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    const uint32_t nb = __builtin_amdgcn_readfirstlane(bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void *>(((uint64_t)hi << 32) | lo), (short)0, (int)nb, 0x00020000);
+}
+
 __device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
 
 // ------------------------------------------------ hand-off between workgroups
