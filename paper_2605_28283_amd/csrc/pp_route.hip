@@ -65,19 +65,20 @@ __global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
     // stage the block's token rows of this slice as MFMA A fragments; every
     // load is issued (addresses clamped into the operands), then rows past T
     // and K-steps past the slice are zeroed
-    const uint4 z = make_uint4(0, 0, 0, 0);
     {
         const int s = wv, sc = min(s, s_end - 1);  // thread (wv, lane) stages K-step wv of every tile
-        uint4 v[kLgTiles];
+        u32x4_t v[kLgTiles];  // native vectors: the selects below stay in registers
 #pragma unroll
         for (int j = 0; j < kLgTiles; ++j) {
             const int t = min(tb * 16 * kLgTiles + 16 * j + (lane & 15), P.T - 1);
-            v[j] = ldg16(P.x + (size_t)t * P.d + (ks * kRouteWaves + sc) * kKStep + 8 * (lane >> 4));
+            v[j] = *reinterpret_cast<const u32x4_t *>(P.x + (size_t)t * P.d +
+                                                      (ks * kRouteWaves + sc) * kKStep + 8 * (lane >> 4));
         }
 #pragma unroll
         for (int j = 0; j < kLgTiles; ++j) {
             const int t = tb * 16 * kLgTiles + 16 * j + (lane & 15);
-            xs[j][s][lane] = (t < P.T && s < s_end) ? v[j] : z;
+            const u32x4_t w = (t < P.T && s < s_end) ? v[j] : u32x4_t{0u, 0u, 0u, 0u};
+            xs[j][s][lane] = make_uint4(w.x, w.y, w.z, w.w);
         }
     }
     __syncthreads();
@@ -90,21 +91,32 @@ __global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
 #pragma unroll
     for (int j = 0; j < kLgTiles; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (wv < P.nEt) {
-        uint4 b[kRouteWaves];
+        // (native vectors: an array of uint4 would not stay in registers; an
+        // expert column past E reads a clamped row, and its products land only
+        // in outputs that are never stored)
+        u32x4_t b[kRouteWaves];
+        const u32x4_t *wr = reinterpret_cast<const u32x4_t *>(
+            P.Wr + (size_t)min(ec, P.E - 1) * P.d + ks * kRouteWaves * kKStep + 8 * (lane >> 4));
+        if (s_end == kRouteWaves) {  // a whole slice: one base, immediate offsets
 #pragma unroll
-        for (int s = 0; s < kRouteWaves; ++s) {
-            const int sc = min(s, s_end - 1);
-            const uint4 v = ldg16(P.Wr + (size_t)min(ec, P.E - 1) * P.d +
-                                  (ks * kRouteWaves + sc) * kKStep + 8 * (lane >> 4));
-            b[s] = ve ? v : z;
+            for (int s = 0; s < kRouteWaves; ++s) b[s] = wr[s * (kKStep / 8)];
+        } else {
+#pragma unroll
+            for (int s = 0; s < kRouteWaves; ++s) b[s] = wr[min(s, s_end - 1) * (kKStep / 8)];
         }
         const int ntile = min(kLgTiles, (P.T - tb * 16 * kLgTiles + 15) / 16);
+        // two token tiles at a time (register budget), K-steps in order
 #pragma unroll
-        for (int s = 0; s < kRouteWaves; ++s) {
-            if (s < s_end) {
+        for (int j0 = 0; j0 < kLgTiles; j0 += 2) {
+            if (j0 < ntile) {
 #pragma unroll
-                for (int j = 0; j < kLgTiles; ++j)
-                    if (j < ntile) acc[j] = mfma16(xs[j][s][lane], b[s], acc[j]);
+                for (int s = 0; s < kRouteWaves; ++s) {
+                    if (s < s_end) {
+                        const uint4 bs = make_uint4(b[s].x, b[s].y, b[s].z, b[s].w);
+                        acc[j0] = mfma16(xs[j0][s][lane], bs, acc[j0]);
+                        if (j0 + 1 < ntile) acc[j0 + 1] = mfma16(xs[j0 + 1][s][lane], bs, acc[j0 + 1]);
+                    }
+                }
             }
         }
     }
