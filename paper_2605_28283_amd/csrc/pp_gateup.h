@@ -48,36 +48,40 @@ __device__ __forceinline__ void split_bf16(float h, uint16_t &hi, uint16_t &lo) 
 
 // Stage token rows of a K sub-chunk into LDS in B-operand order:
 // xf[(j * nsc + step) * 64 + lane] holds token slot 16 j + lane % 16,
-// columns 32 (sc + step) + 8 (lane / 16) .. +7.  All loads are issued first.
+// columns 32 (sc + step) + 8 (lane / 16) .. +7.  Loads go out in batches,
+// every lane of a batch loading unconditionally from an element index clamped
+// into the group (native vectors, so the zeroing selects stay in registers);
+// the batch loop ends on a wavefront-uniform bound.
 template <int NT>
 __device__ __forceinline__ void stage_x(const GUParams &P, const int *stok, int n, int sc, int nsc,
                                         uint4 *xf) {
     constexpr int kPerThread = kXBufBytes / 16 / kGuThreads;
-    constexpr int kBatch = 4;  // loads in flight per thread (register budget)
+    constexpr int kBatch = NT >= 4 ? 2 : 4;  // loads in flight per thread (register budget)
     const int per_tok = nsc * 4;
     const int total = NT * 16 * per_tok;
-    const uint4 z = make_uint4(0, 0, 0, 0);
+    const int wave0 = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63);
 #pragma unroll
     for (int i0 = 0; i0 < kPerThread; i0 += kBatch) {
-        if (threadIdx.x + kGuThreads * i0 >= total) break;
-        uint4 v[kBatch];
+        if (wave0 + kGuThreads * i0 >= total) break;
+        u32x4_t v[kBatch];
 #pragma unroll
         for (int i = 0; i < kBatch; ++i) {
-            const int c = threadIdx.x + kGuThreads * (i0 + i);
-            v[i] = z;
-            if (c < total) {
-                const int q = c / per_tok, r = c - q * per_tok;
-                if (q < n)
-                    v[i] = ldg16(P.x + (size_t)stok[q] * P.d + (sc + (r >> 2)) * kKStep + 8 * (r & 3));
-            }
+            const int c = min((int)threadIdx.x + kGuThreads * (i0 + i), total - 1);
+            const int q = c / per_tok, r = c - q * per_tok;
+            v[i] = *reinterpret_cast<const u32x4_t *>(P.x + (size_t)stok[min(q, n - 1)] * P.d +
+                                                      (sc + (r >> 2)) * kKStep + 8 * (r & 3));
         }
+        // A lane past the end stores the last element again, the same value
+        // its own thread stores, so the stores need no branch either.
 #pragma unroll
         for (int i = 0; i < kBatch; ++i) {
-            const int c = threadIdx.x + kGuThreads * (i0 + i);
-            if (c < total) {
-                const int q = c / per_tok, r = c - q * per_tok;
-                xf[((q >> 4) * nsc + (r >> 2)) * 64 + (q & 15) + 16 * (r & 3)] = v[i];
-            }
+            const int c = min((int)threadIdx.x + kGuThreads * (i0 + i), total - 1);
+            const int q = c / per_tok, r = c - q * per_tok;
+            // The empty asm consumes the loaded value on every lane, so the
+            // compiler cannot turn the zeroing select into a guarded load.
+            asm volatile("" : "+v"(v[i]));
+            const u32x4_t w = q < n ? v[i] : u32x4_t{0u, 0u, 0u, 0u};
+            xf[((q >> 4) * nsc + (r >> 2)) * 64 + (q & 15) + 16 * (r & 3)] = make_uint4(w.x, w.y, w.z, w.w);
         }
     }
 }
