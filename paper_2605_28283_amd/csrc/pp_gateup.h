@@ -71,8 +71,8 @@ __device__ __forceinline__ void stage_x(const GUParams &P, const int *stok, int 
             v[i] = *reinterpret_cast<const u32x4_t *>(P.x + (size_t)stok[min(q, n - 1)] * P.d +
                                                       (sc + (r >> 2)) * kKStep + 8 * (r & 3));
         }
-        // A lane past the end stores the last element again, the same value
-        // its own thread stores, so the stores need no branch either.
+        // A lane past the end stores the last element again, the value that
+        // element's own thread stores, so the stores need no branch either.
 #pragma unroll
         for (int i = 0; i < kBatch; ++i) {
             const int c = min((int)threadIdx.x + kGuThreads * (i0 + i), total - 1);
