@@ -37,6 +37,9 @@ struct DNParams {
     PlanView plan;
 };
 
+// Token-row loads per thread in flight while staging a prefill group.
+constexpr int kPfStageBatch = 4;
+
 template <bool GATED>
 __global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
     __shared__ uint4 xf[kXBufBytes / 16];
@@ -59,7 +62,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
         const int p0 = P.plan.grp_pair[g];
         if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
         __syncthreads();
-        gateup_group<GATED, 4, kPF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, &s_flag);
+        gateup_group<GATED, 4, kPF, kPfStageBatch>(P, e, n, p0, g, ks, KS, npairs, stok, xf, &s_flag);
         __syncthreads();
     }
 }

@@ -51,12 +51,14 @@ __device__ __forceinline__ void split_bf16(float h, uint16_t &hi, uint16_t &lo) 
 // columns 32 (sc + step) + 8 (lane / 16) .. +7.  Loads go out in batches,
 // every lane of a batch loading unconditionally from an element index clamped
 // into the group (native vectors, so the zeroing selects stay in registers);
-// the batch loop ends on a wavefront-uniform bound.
-template <int NT>
+// the batch loop ends on a wavefront-uniform bound.  XB: loads per thread
+// in a batch (0: chosen by NT for the register budget of the decode kernels).
+template <int NT, int XB>
 __device__ __forceinline__ void stage_x(const GUParams &P, const int *stok, int n, int sc, int nsc,
                                         uint4 *xf) {
     constexpr int kPerThread = kXBufBytes / 16 / kGuThreads;
-    constexpr int kBatch = NT >= 4 ? 2 : 4;  // loads in flight per thread (register budget)
+    constexpr int kBatch = XB > 0 ? XB : (NT >= 4 ? 2 : 4);  // loads in flight per thread
+    static_assert(kPerThread % kBatch == 0, "whole batches");
     const int per_tok = nsc * 4;
     const int total = NT * 16 * per_tok;
     const int wave0 = __builtin_amdgcn_readfirstlane(threadIdx.x & ~63);
@@ -134,7 +136,7 @@ __device__ __forceinline__ float act(const GUParams &P, int e, int r, float a, f
 
 // PF: K-steps per register buffer; two buffers alternate, so PF steps of
 // weights are in flight while the other PF are multiplied.
-template <int NT, bool GATED, int PF>
+template <int NT, bool GATED, int PF, int XB>
 __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int ks, int KS,
                             int npairs, const int *stok, uint4 *xf, int *flag) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -151,7 +153,7 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
         const int nsc = min(nsc_max, s1 - sc), last = sc + nsc - 1;
         uint4 G0[PF], U0[PF], G1[PF], U1[PF];
         load_wgu<GATED, PF>(wb, sc, last, G0, U0);  // weights do not wait for the token staging
-        stage_x<NT>(P, stok, n, sc, nsc, xf);
+        stage_x<NT, XB>(P, stok, n, sc, nsc, xf);
         __syncthreads();
         for (int b = 0; b < nsc; b += 2 * PF) {
             if (b + PF < nsc) load_wgu<GATED, PF>(wb, sc + b + PF, last, G1, U1);
@@ -303,19 +305,19 @@ __device__ void decode_plan(const GUParams &P, DecodePlan &D, unsigned long long
 // One group's gate/up unit, dispatched on its number of 16-token tiles (at
 // most NTMAX: a kernel whose groups are known to be small is compiled without
 // the larger tiles' registers and spends them on a deeper weight prefetch PF).
-template <bool GATED, int NTMAX, int PF>
+template <bool GATED, int NTMAX, int PF, int XB = 0>
 __device__ __forceinline__ void gateup_group(const GUParams &P, int e, int n, int p0, int g,
                                              int ks, int KS, int npairs, const int *stok,
                                              uint4 *xf, int *flag) {
     const int nt = (n + 15) >> 4;
     if (NTMAX >= 4 && nt >= 4)
-        gateup_unit<(NTMAX >= 4 ? 4 : 1), GATED, PF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+        gateup_unit<(NTMAX >= 4 ? 4 : 1), GATED, PF, XB>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
     else if (NTMAX >= 3 && nt == 3)
-        gateup_unit<(NTMAX >= 3 ? 3 : 1), GATED, PF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+        gateup_unit<(NTMAX >= 3 ? 3 : 1), GATED, PF, XB>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
     else if (NTMAX >= 2 && nt == 2)
-        gateup_unit<(NTMAX >= 2 ? 2 : 1), GATED, PF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+        gateup_unit<(NTMAX >= 2 ? 2 : 1), GATED, PF, XB>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
     else
-        gateup_unit<1, GATED, PF>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+        gateup_unit<1, GATED, PF, XB>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
 }
 
 // K-slices per group: as many as keep all nG * KS units within `slots`
