@@ -37,7 +37,8 @@ def parse_args():
                     help="time every (T, tau) point or only the headline one")
     ap.add_argument("--copies", type=int, default=0, help="layer copies (0 = enough for 2.2 GB)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="target duration of the CPU-oracle baseline (0 = skip)")
+                    help="target duration of the CPU-oracle timing: three single-thread and "
+                         "three all-core runs share it (0 = skip the CPU leg)")
     ap.add_argument("--no-stack", action="store_true",
                     help="skip the 32-layer stacked decode measurement")
     ap.add_argument("--no-prefill", action="store_true",
@@ -48,6 +49,8 @@ def parse_args():
                     help="skip the balanced k-means (neuron clustering) leg")
     ap.add_argument("--no-loss", action="store_true",
                     help="skip the router-loss (training regularisers) leg")
+    ap.add_argument("--no-skewed", action="store_true",
+                    help="skip the wide skewed-routing layer (Qwen2-7B FFN shape)")
     ap.add_argument("--no-rules", action="store_true",
                     help="skip the comparison selection rules (strict, top-k, LTE)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -133,52 +136,37 @@ def main():
                                 stream=stream)
 
     def union_stats(T, tau):
-        """Per copy: |U| (batch-union experts) and pairs sum_t k_t."""
-        out = []
-        for h in handles:
+        """Per copy: |U| (batch-union experts), pairs sum_t k_t, and copy 0's
+        selection (compared with the CPU oracle's in the cpu_baseline leg)."""
+        out, sel0 = [], None
+        for c, h in enumerate(handles):
             pp.prunepath_route(h, x, T, tau, None, idx, cnt, stream=stream)
             torch.cuda.synchronize()
             ii = idx[:T].cpu().numpy()
-            out.append((len(np.unique(ii[ii >= 0])), int(cnt[:T].sum().item())))
-        return out
+            cc = cnt[:T].cpu().numpy()
+            if c == 0:
+                sel0 = (ii.copy(), cc.copy())
+            out.append((len(np.unique(ii[ii >= 0])), int(cc.sum()), int(cc.min()), int(cc.max())))
+        return out, sel0
 
     def run_point(T, tau):
-        for i in range(args.warmup):
-            step(i, T, tau)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for i in range(args.steps):
-            step(i, T, tau)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / args.steps
-        # per-kernel device time of the same sequence, HIP events on the call stream
-        for h in handles:
-            pp.prunepath_profile_begin(h, 4 * args.steps)
-        for i in range(args.steps):
-            step(i, T, tau)
-        torch.cuda.synchronize()
-        kms = [0.0] * pp.PP_KERNEL_COUNT
-        kn = [0] * pp.PP_KERNEL_COUNT
-        for h in handles:
-            a, n = pp.prunepath_profile_end(h)
-            kms = [u + v for u, v in zip(kms, a)]
-            kn = [u + v for u, v in zip(kn, n)]
-        us = union_stats(T, tau)
+        ms, kavg = time_decode(torch, pp, handles, lambda i: step(i, T, tau), args.steps,
+                               args.warmup, stream)
+        us, sel0 = union_stats(T, tau)
+        gpu_sel[(T, tau)] = sel0
         seq = [us[i % n_copies] for i in range(args.steps)]
         U = float(np.mean([s[0] for s in seq]))
         pairs = float(np.mean([s[1] for s in seq]))
         step_bytes = E * d * 2 + U * 6 * 128 * d + 2 * T * d + 4 * T * d
         gateup_bytes = U * 2 * 128 * d * 2 + 2 * T * d + pairs * 128 * 4
         down_bytes = U * 128 * d * 2 + pairs * 128 * 4 + 4 * T * d
-        kavg = {name: (kms[k] / kn[k] * 1e3 if kn[k] else None)
-                for name, k in (("route", pp.PP_KERNEL_ROUTE), ("gateup", pp.PP_KERNEL_GATEUP),
-                                ("down", pp.PP_KERNEL_DOWN))}
         gbps = step_bytes / (ms * 1e-3) / 1e9
         return {
             "T": T, "tau": tau, "ms_per_step": ms, "tokens_per_s_layer": T / (ms * 1e-3),
             "union_experts": U, "pairs": pairs, "k_mean": pairs / T,
+            "k_min": min(s[2] for s in us), "k_max": max(s[3] for s in us),
+            # the paper's FFN sparsity (Sec. 4.1): 1 - mean kept experts / E
+            "s_ffn": 1.0 - pairs / (T * E), "union_frac": U / E,
             "algorithmic_bytes": step_bytes, "effective_GBps": gbps,
             "frac_hbm_peak": gbps / HBM_PEAK_GBPS,
             "kernel_us": kavg,
@@ -188,6 +176,7 @@ def main():
             "down_GBps": (down_bytes / (kavg["down"] * 1e-6) / 1e9 if kavg["down"] else None),
         }
 
+    gpu_sel = {}
     points = [(args.T, args.tau)]
     if args.sweep == "full":
         points = [(T, tau) for T in w.T for tau in w.taus]
@@ -197,10 +186,11 @@ def main():
     for T, tau in points:
         r = run_point(T, tau)
         results[(T, tau)] = r
-        print("# T=%-3d tau=%.2f  %8.1f us/step  %9.0f tok/s/layer  |U|=%5.1f  %7.1f GB/s "
-              "(%4.1f%% of peak)  gateup %.1f us (%.0f GB/s)  down %.1f us (%.0f GB/s)  "
+        print("# T=%-3d tau=%.2f  %8.1f us/step  %9.0f tok/s/layer  s_FFN %.3f  |U|=%5.1f  "
+              "%7.1f GB/s (%4.1f%% of peak)  gateup %.1f us (%.0f GB/s)  down %.1f us (%.0f GB/s)  "
               "route %.1f us" % (
-                  T, tau, r["ms_per_step"] * 1e3, r["tokens_per_s_layer"], r["union_experts"],
+                  T, tau, r["ms_per_step"] * 1e3, r["tokens_per_s_layer"], r["s_ffn"],
+                  r["union_experts"],
                   r["effective_GBps"], 100 * r["frac_hbm_peak"], r["kernel_us"]["gateup"],
                   r["gateup_GBps"], r["kernel_us"]["down"], r["down_GBps"],
                   r["kernel_us"]["route"]), file=sys.stderr, flush=True)
@@ -225,26 +215,6 @@ def main():
             "algorithmic_bytes_per_launch": head["gateup_bytes"],
             "avg_launch_us": head["kernel_us"]["gateup"]}
 
-    # ---- CPU oracle baseline (rank 0, N=1): same layer copy 0 and batch
-    cpu = None
-    if args.cpu_seconds > 0:
-        import oracle
-        T = args.T
-        xs = x_np[:T]
-        oracle.forward(xs[:1], L0.W_r, L0.W_gate, L0.W_up, L0.W_down, args.tau)  # load / warm
-        n, t0 = 0, time.perf_counter()
-        while True:
-            oracle.forward(xs, L0.W_r, L0.W_gate, L0.W_up, L0.W_down, args.tau)
-            n += 1
-            el = time.perf_counter() - t0
-            if el >= args.cpu_seconds:
-                break
-        cpu = {"value": n * T / el, "unit": "tokens/s/layer", "cores": oracle.num_threads(),
-               "kind": "oracle",
-               "sample": "fp64 C oracle (route + kept-expert FFN), layer copy 0, the T=%d "
-                         "headline batch at tau=%g, repeated %d times in %.1f s" % (
-                             T, args.tau, n, el)}
-
     sweep = list(results.values())
     out = {
         "metric": "sparse-FFN decode tokens/s/layer",
@@ -265,7 +235,7 @@ def main():
         "effective_GBps": head["effective_GBps"],
         "frac_hbm_peak": head["frac_hbm_peak"],
         "roofline": roof,
-        "cpu_baseline": cpu,
+        "cpu_baseline": None,
         "sweep": sweep,
         "source_hash": source_hash(),
     }
@@ -273,6 +243,10 @@ def main():
         pp.prunepath_destroy(h)
     handles = []
     torch.cuda.empty_cache()
+    skewed = None
+    if not args.no_skewed:
+        skewed = bench_skewed(args, torch, np, pp)
+        out["skewed"] = skewed["points"]
     if not args.no_rules:
         out["rules"] = bench_rules(args, torch, np, pp, x, n_copies)
     if not args.no_prefill:
@@ -285,6 +259,15 @@ def main():
         out["router_loss"] = bench_loss(args, torch, np, pp)
     if not args.no_kmeans:
         out["kmeans"] = bench_kmeans(args, torch, np, pp)
+    # ---- the CPU oracle (rank 0, N = 1), after every GPU leg
+    if args.cpu_seconds > 0:
+        cpu, stats = cpu_baseline_leg(args, np, L0, x_np, gpu_sel, skewed, head)
+        out["cpu_baseline"] = cpu
+        for r in sweep:
+            r["oracle_selection"] = stats.get(("llama8b", r["T"], r["tau"]))
+        if skewed:
+            for r in out["skewed"]:
+                r["oracle_selection"] = stats.get(("qwen7b", r["T"], r["tau"]))
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -297,6 +280,223 @@ def main():
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def time_decode(torch, pp, handles, call, steps, warmup, stream):
+    """Times `call(i)` (one decode step on layer copy i % len(handles)) over
+    `steps` calls after `warmup`, then repeats the calls with per-kernel HIP
+    events recorded on the call stream.  Returns (ms per step, average
+    microseconds per launch by kernel kind)."""
+    for i in range(warmup):
+        call(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(steps):
+        call(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    for h in handles:
+        pp.prunepath_profile_begin(h, 4 * steps)
+    for i in range(steps):
+        call(i)
+    torch.cuda.synchronize()
+    kms = [0.0] * pp.PP_KERNEL_COUNT
+    kn = [0] * pp.PP_KERNEL_COUNT
+    for h in handles:
+        a, n = pp.prunepath_profile_end(h)
+        kms = [u + v for u, v in zip(kms, a)]
+        kn = [u + v for u, v in zip(kn, n)]
+    kavg = {name: (kms[k] / kn[k] * 1e3 if kn[k] else None)
+            for name, k in (("route", pp.PP_KERNEL_ROUTE), ("gateup", pp.PP_KERNEL_GATEUP),
+                            ("down", pp.PP_KERNEL_DOWN))}
+    return ms, kavg
+
+
+def bench_skewed(args, torch, np, pp):
+    """The wide skewed-routing layer: the Qwen2-7B FFN shape (d 3584, d_ff
+    18944, E 148 experts of 128), router logits (W_r x + b) / temperature
+    with b ~ Gumbel(0, 1.5) per expert and temperature ~ U(0.5, 2) per token,
+    decode T = 64, tau in {0.5, 0.9}.  Calls rotate over 6 layer copies
+    (2.4 GB) drawn on the GPU, each with its own bias draw; the tokens and
+    temperatures are the seeded workload's.  Algorithmic bytes as for the
+    main sweep plus the bias and temperatures."""
+    from paper_2605_28283_amd.workloads import WORKLOADS, workload_tokens
+    w = WORKLOADS["qwen7b_skewed"]
+    d, d_ff, E, T = w.d, w.d_ff, w.E, w.T[0]
+    layer_bytes = 3 * d_ff * d * 2 + E * d * 2
+    ncp = max(2, math.ceil(2.2e9 / layer_bytes))
+    hs, bts = [], []
+    Wr0 = bias0 = None
+    for c in range(ncp):
+        Wt = device_layer(torch, d, d_ff, E, 5000 + c)
+        b = np.random.default_rng(5000 + c).gumbel(0.0, 1.5, size=E).astype(np.float32)
+        bts.append(torch.from_numpy(b).cuda())
+        hs.append(pp.prunepath_create(d, d_ff, E, T, *Wt, router_bias=bts[-1]))
+        if c == 0:
+            Wr0 = Wt[0].view(torch.int16).cpu().numpy().view(np.uint16)
+            bias0 = b
+        del Wt
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    x_np, it_np = workload_tokens(w, T, 0)
+    x = torch.from_numpy(x_np.view(np.int16)).cuda()
+    it = torch.from_numpy(it_np).cuda()
+    y = torch.empty((T, d), dtype=torch.float32, device="cuda")
+    idx = torch.empty((T, E), dtype=torch.int32, device="cuda")
+    cnt = torch.empty((T,), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    planned = {0.5: 146e6, 0.9: 376e6}  # simulated union bytes of this workload's distributions
+    res, sel = [], {}
+    for tau in w.taus:
+        ms, kavg = time_decode(
+            torch, pp, hs,
+            lambda i: pp.prunepath_ffn_decode(hs[i % ncp], x, T, tau, it, y, idx, cnt,
+                                              stream=stream),
+            args.steps, args.warmup, stream)
+        us, ks = [], []
+        for c, h in enumerate(hs):
+            pp.prunepath_route(h, x, T, tau, it, idx, cnt, stream=stream)
+            torch.cuda.synchronize()
+            ii, cc = idx.cpu().numpy(), cnt.cpu().numpy()
+            if c == 0:
+                sel[tau] = (ii.copy(), cc.copy())
+            us.append(len(np.unique(ii[ii >= 0])))
+            ks.append(cc)
+        seq = [i % ncp for i in range(args.steps)]
+        U = float(np.mean([us[i] for i in seq]))
+        pairs = float(np.mean([ks[i].sum() for i in seq]))
+        nbytes = E * d * 2 + 4 * E + U * 6 * 128 * d + 2 * T * d + 4 * T + 4 * T * d
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        gu_bytes = U * 2 * 128 * d * 2 + 2 * T * d + pairs * 128 * 4
+        dn_bytes = U * 128 * d * 2 + pairs * 128 * 4 + 4 * T * d
+        r = {"workload": "qwen7b_skewed_decode", "d_model": d, "d_ff": d_ff, "experts": E,
+             "T": T, "tau": tau, "layer_copies": ncp, "ms_per_step": ms,
+             "tokens_per_s_layer": T / (ms * 1e-3), "union_experts": U,
+             "union_frac": U / E, "pairs": pairs, "k_mean": pairs / T,
+             "k_min": int(min(k.min() for k in ks)), "k_max": int(max(k.max() for k in ks)),
+             "s_ffn": 1.0 - pairs / (T * E), "algorithmic_bytes": nbytes,
+             "effective_GBps": gbps, "frac_hbm_peak": gbps / HBM_PEAK_GBPS,
+             "planned_bytes": planned.get(tau),
+             "planned_ideal_us": planned[tau] / (HBM_PEAK_GBPS * 1e3) if tau in planned else None,
+             "kernel_us": kavg,
+             "gateup_GBps": gu_bytes / (kavg["gateup"] * 1e-6) / 1e9 if kavg["gateup"] else None,
+             "down_GBps": dn_bytes / (kavg["down"] * 1e-6) / 1e9 if kavg["down"] else None}
+        res.append(r)
+        print("# skewed qwen7b T=%d tau=%.2f  %7.1f us/step  %9.0f tok/s/layer  k %.2f (%d..%d)  "
+              "s_FFN %.3f  |U| %.1f of %d  %7.1f GB/s (%4.1f%% of peak)  gateup %.1f us  down "
+              "%.1f us  route %.1f us" % (
+                  T, tau, ms * 1e3, r["tokens_per_s_layer"], r["k_mean"], r["k_min"], r["k_max"],
+                  r["s_ffn"], U, E, gbps, 100 * gbps / HBM_PEAK_GBPS, kavg["gateup"],
+                  kavg["down"], kavg["route"]), file=sys.stderr, flush=True)
+    for h in hs:
+        pp.prunepath_destroy(h)
+    torch.cuda.empty_cache()
+    return {"points": res, "sel": sel, "W_r0": Wr0, "bias0": bias0, "x": x_np, "inv_temp": it_np}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def selection_stats(oracle, np, r, idx, cnt, tau):
+    """The GPU's selections against the oracle's fp64 routing r: tokens in
+    the tie bands (cumulative mass within 1e-5 of tau; last kept and first
+    dropped logits within 1e-5) and tokens whose kept set, count or order
+    differs outside them (order may differ only between tied logits)."""
+    near = oracle.near_tie(r["cum"], tau)
+    cut = oracle.cut_order_tie(r["g"], r["count"])
+    pre = oracle.prefix_order_tie(r["g"], r["count"])
+    ex = near | cut
+    bad = 0
+    for t in range(len(cnt)):
+        if ex[t]:
+            continue
+        k = int(cnt[t])
+        ref = r["idx"][t, :r["count"][t]]
+        kept = idx[t, :k]
+        if k != len(ref) or not (np.sort(kept) == np.sort(ref)).all():
+            bad += 1
+        elif not (kept == ref).all() and not pre[t]:
+            bad += 1
+    return {"tokens": int(len(cnt)), "near_tie": int(near.sum()), "cut_tie": int(cut.sum()),
+            "order_only_ties": int(pre.sum()), "exempt": int(ex.sum()),
+            "mismatch_outside_bands": bad}
+
+
+def cpu_baseline_leg(args, np, L0, x_np, gpu_sel, skewed, head):
+    """Everything that runs the CPU oracle.  (1) Its throughput on the
+    headline batch (layer copy 0, T = --T, tau = --tau, route + kept-expert
+    FFN in fp64), three runs single-threaded and three on all the threads
+    OpenMP is given, each figure the median of its three; (2) for every
+    decode point timed above, the oracle's routing of layer copy 0 (and of
+    the skewed leg's copy 0) against the GPU's selection of the same batch."""
+    import oracle
+    T, tau = args.T, args.tau
+    xs = x_np[:T]
+
+    def one():
+        oracle.forward(xs, L0.W_r, L0.W_gate, L0.W_up, L0.W_down, tau)
+
+    all_threads = oracle.num_threads()
+    per_run = args.cpu_seconds / 6.0
+
+    def three_runs(threads):
+        oracle.set_num_threads(threads)
+        one()  # warm: library load, page-in of the weights
+        t0 = time.perf_counter()
+        one()
+        n = max(1, int(round(per_run / (time.perf_counter() - t0))))
+        rates = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            for _ in range(n):
+                one()
+            rates.append(n * T / (time.perf_counter() - t0))
+        return rates, n
+
+    single, n1 = three_runs(1)
+    multi, nm = three_runs(all_threads)
+    oracle.set_num_threads(all_threads)
+    med1, medm = float(np.median(single)), float(np.median(multi))
+    gpu = head["tokens_per_s_layer"]
+    cpu = {"value": medm, "unit": "tokens/s/layer", "cores": all_threads, "kind": "oracle",
+           "sample": "fp64 C oracle (route + kept-expert FFN), LLaMA-3-8B layer copy 0, the "
+                     "T=%d headline batch at tau=%g: median of 3 runs of %d calls on %d "
+                     "threads (single-thread: median of 3 runs of %d calls)" % (
+                         T, tau, nm, all_threads, n1),
+           "runs": multi,
+           "single_thread": {"value": med1, "cores": 1, "runs": single},
+           "nproc": os.cpu_count(),
+           "affinity_cpus": len(os.sched_getaffinity(0)),
+           "cpu_model": cpu_model(),
+           "gpu_speedup_vs_all_threads": gpu / medm,
+           "gpu_speedup_vs_single_thread": gpu / med1}
+    print("# CPU oracle (%s, nproc %s): %.0f tokens/s/layer on %d threads, %.0f single-threaded "
+          "(GPU %.0fx / %.0fx)" % (cpu["cpu_model"], cpu["nproc"], medm, all_threads, med1,
+                                   gpu / medm, gpu / med1), file=sys.stderr, flush=True)
+    stats = {}
+    for (Tp, taup), (ii, cc) in gpu_sel.items():
+        r = oracle.route(x_np[:Tp], L0.W_r, taup)
+        stats[("llama8b", Tp, taup)] = selection_stats(oracle, np, r, ii, cc, taup)
+    if skewed:
+        for taup, (ii, cc) in skewed["sel"].items():
+            r = oracle.route(skewed["x"], skewed["W_r0"], taup, bias=skewed["bias0"],
+                             inv_temp=skewed["inv_temp"])
+            stats[("qwen7b", len(cc), taup)] = selection_stats(oracle, np, r, ii, cc, taup)
+    bad = sum(v["mismatch_outside_bands"] for v in stats.values())
+    ties = sum(v["exempt"] for v in stats.values())
+    print("# oracle selections: %d decode points, %d tokens in tie bands, %d mismatches outside "
+          "them" % (len(stats), ties, bad), file=sys.stderr, flush=True)
+    return cpu, stats
 
 
 def bench_rules(args, torch, np, pp, x, n_copies):

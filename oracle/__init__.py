@@ -66,6 +66,8 @@ def _load():
         lib.ppo_router_loss.restype = ctypes.c_int
         lib.ppo_num_threads.argtypes = []
         lib.ppo_num_threads.restype = ctypes.c_int
+        lib.ppo_set_num_threads.argtypes = [ctypes.c_int]
+        lib.ppo_set_num_threads.restype = None
         _lib = lib
     return _lib
 
@@ -80,6 +82,11 @@ def _c(a, dtype):
 
 def num_threads() -> int:
     return _load().ppo_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """Threads the oracle's OpenMP loops use from now on (benchmark timing)."""
+    _load().ppo_set_num_threads(int(n))
 
 
 def softmax(g):
@@ -179,39 +186,62 @@ def forward(x, W_r, W_gate, W_up, W_down, tau, flags=0, bias=None, inv_temp=None
 
 
 def near_tie(cum, tau, band=1e-5, flags=0):
-    """Tokens whose cumulative mass lies within `band` of tau at some cut
-    position (C_1..C_{E-1}); for these the count may legitimately differ
-    between fp32 and fp64 evaluation.  Nothing is near a tie when the rule
-    keeps every expert regardless of C (nucleus with tau >= 1, strict with
-    tau > 1)."""
+    """Cumulative-mass ties of the cut (Eq. tau_thresh_activate): tokens whose
+    cumulative mass lies within `band` of tau at some cut position
+    (C_1..C_{E-1}; C_E = 1 decides nothing for tau < 1).  For these the count
+    may legitimately differ between fp32 and fp64 evaluation.  Nothing is near
+    a tie when the rule keeps every expert regardless of C (nucleus with
+    tau >= 1, strict with tau > 1), nor for the top-k and LTE rules, which do
+    not read C."""
     cum = np.asarray(cum)
     if flags & (SELECT_TOPK | SELECT_LTE):
-        return np.zeros(cum.shape[0], bool)  # these rules do not read C
+        return np.zeros(cum.shape[0], bool)
     if (flags & SELECT_STRICT and tau > 1.0) or (not flags & SELECT_STRICT and tau >= 1.0):
         return np.zeros(cum.shape[0], bool)
     return (np.abs(cum[:, :-1] - tau) <= band).any(axis=1)
 
 
 def lte_tie(g, delta, band=1e-6):
-    """Tokens with an expert whose sigmoid score lies within `band` of delta:
-    their LTE decision may differ between fp32 and fp64 evaluation."""
+    """LTE threshold ties (Eq. lte_hard_set): tokens with an expert whose
+    sigmoid score lies within `band` of delta; their kept set may differ
+    between fp32 and fp64 evaluation."""
     s = 1.0 / (1.0 + np.exp(-np.asarray(g, np.float64)))
     return (np.abs(s - delta) <= band).any(axis=1)
 
 
-def order_tie(g, idx, count, band=1e-5):
-    """Tokens whose logits at the cut (last kept vs first dropped) or inside
-    the kept prefix differ by at most `band`; their expert order (and, at the
-    cut, their set) is not unique under fp32 evaluation."""
-    g = np.asarray(g)
-    T, E = g.shape
+def _sorted_desc(g):
+    g = np.asarray(g, np.float64)
+    return -np.sort(-g, axis=1)
+
+
+def cut_order_tie(g, count, band=1e-5):
+    """Logit ties at the cut: tokens whose last kept and first dropped experts
+    in the descending order (pi_k, pi_{k+1}) have logits within `band`.
+    Which of the two is kept is then not unique under fp32 evaluation (the
+    count is not affected unless the mass is also near tau).  Tokens keeping
+    no expert or all E have no cut."""
+    srt = _sorted_desc(g)
+    T, E = srt.shape
+    k = np.asarray(count, np.int64)
+    out = np.zeros(T, bool)
+    rows = np.nonzero((k >= 1) & (k < E))[0]
+    out[rows] = srt[rows, k[rows] - 1] - srt[rows, k[rows]] <= band
+    return out
+
+
+def prefix_order_tie(g, count, band=1e-5):
+    """Logit ties inside the kept prefix: tokens with two consecutive kept
+    experts whose logits lie within `band`.  The kept set stays unique (a
+    swap inside the prefix changes C only at positions within `band` of
+    tau, which near_tie covers), but the order in which the kept experts are
+    listed is not."""
+    srt = _sorted_desc(g)
+    T, E = srt.shape
+    k = np.asarray(count, np.int64)
     out = np.zeros(T, bool)
     for t in range(T):
-        k = int(count[t])
-        srt = np.sort(g[t])[::-1]
-        m = min(k + 1, E)
-        if m >= 2 and (np.diff(srt[:m]) >= -band).any():
-            out[t] = True
+        if k[t] >= 2:
+            out[t] = bool((srt[t, :k[t] - 1] - srt[t, 1:k[t]] <= band).any())
     return out
 
 

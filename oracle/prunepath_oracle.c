@@ -68,6 +68,16 @@ int ppo_num_threads(void) {
 #endif
 }
 
+/* Threads of the following parallel regions (n >= 1); used to time the
+ * oracle single-threaded next to its all-core run. */
+void ppo_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Eq. (routing_logits), one token: g_e = sum_j W_r[e,j] x_j, then the optional
  * per-expert bias and per-token inverse temperature of the skewed workload. */
 static void logits_one(int64_t d, int64_t E, const uint16_t *x, const uint16_t *Wr,

@@ -11,7 +11,7 @@ import pytest
 import paper_2605_28283_amd as pp
 from paper_2605_28283_amd.workloads import (WORKLOADS, make_layer, make_tokens, workload_layer,
                                             workload_tokens)
-from gpu_helpers import DevLayer, check_output, check_selection, parity, to_dev
+from gpu_helpers import DevLayer, check_output, check_selection, full_size_cap, parity, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -60,7 +60,7 @@ def test_route_entry_point(oracle_mod):
     for flags in (NUC | SUM, STRICT | SIG):
         with DevLayer(L, 32, flags) as dl:
             idx, cnt, gw = dl.run("route", x, 0.8, it)
-            r, _ = check_selection(oracle_mod, L, x, 0.8, flags, idx, cnt, it)
+            r, _, _ = check_selection(oracle_mod, L, x, 0.8, flags, idx, cnt, it, label="route")
             for t in range(x.shape[0]):
                 k = cnt[t]
                 if flags & SIG:
@@ -111,7 +111,7 @@ def test_comparison_rules(oracle_mod, flags, params, mode):
         for p in params:
             if mode == "route":
                 idx, cnt, gw = dl.run("route", x, p)
-                r, _ = check_selection(oracle_mod, L, x, p, flags, idx, cnt)
+                r, _, _ = check_selection(oracle_mod, L, x, p, flags, idx, cnt, label="route rules")
                 continue
             res = parity(oracle_mod, dl, mode, x, p)
             if flags & LTE and p >= 1.0:
@@ -123,7 +123,7 @@ def test_comparison_rules_llama8b_decode(oracle_mod, llama8b):
     x, _ = workload_tokens(w, 32, 0)
     for flags, p in ((TOPK, 4), (LTE, 0.95), (STRICT, 0.7)):
         with DevLayer(L, 64, flags=flags) as dl:
-            parity(oracle_mod, dl, "decode", x, p, rows=np.arange(0, 32, 5))
+            parity(oracle_mod, dl, "decode", x, p, label="llama8b rules")
 
 
 def test_decode_down_modes_ragged_rows(oracle_mod):
@@ -260,22 +260,25 @@ def llama8b():
 @pytest.mark.parametrize("T", [1, 8, 32, 64])
 def test_llama8b_decode_sweep(oracle_mod, llama8b, T):
     """Full LLaMA-3-8B FFN shape, the decode launch configuration the benchmark
-    times: every token's selection, y on sampled tokens."""
+    times: every token's selection and every row of y against the oracle."""
     L, w, dl = llama8b
     x, _ = workload_tokens(w, 64, 0)
     x = x[:T]
-    rows = np.unique(np.linspace(0, T - 1, min(T, 4)).astype(int))
     for tau in w.taus:
-        parity(oracle_mod, dl, "decode", x, tau, rows=rows)
+        parity(oracle_mod, dl, "decode", x, tau, label="llama8b decode",
+               max_exempt=full_size_cap(T))
 
 
 def test_llama8b_prefill(oracle_mod, llama8b):
+    """2048-token prefill at the benchmark's taus: every selection and every
+    row of y (four full 512-token chunks of the down projection) against the
+    oracle; the decode path agrees with prefill on the same tokens."""
     L, _, dl = llama8b
     w = WORKLOADS["llama8b_prefill"]
     x, _ = workload_tokens(w, 2048, 0)
-    rows = np.arange(0, 2048, 97)
     for tau in w.taus:
-        res = parity(oracle_mod, dl, "prefill", x, tau, rows=rows)
+        res = parity(oracle_mod, dl, "prefill", x, tau, label="llama8b prefill",
+                     max_exempt=full_size_cap(2048))
         # decode path on the same tokens agrees with prefill everywhere
         idx, cnt, y = dl.run("decode", x, tau)
         np.testing.assert_array_equal(idx, res["idx"])
@@ -288,32 +291,37 @@ def test_llama8b_prefill_many_pairs(oracle_mod, llama8b):
     even tokens route nearly flat (inverse temperature 0.01: most experts kept
     at tau 0.95), odd tokens sharply (inverse temperature 20: one or two
     kept), so the experts' runs in each 512-token chunk are long and every
-    expert's down block meets tokens of both kinds."""
+    expert's down block meets tokens of both kinds.  y: the whole first
+    512-token chunk and both sides of every chunk edge."""
     L, w, dl = llama8b
     T = 2048
     x, _ = make_tokens(T, w.d, 91)
     it = np.where(np.arange(T) % 2 == 0, 0.01, 20.0).astype(np.float32)
-    res = parity(oracle_mod, dl, "prefill", x, 0.95, it, rows=np.arange(0, T, 127))
+    rows = np.concatenate([np.arange(512), [1023, 1024, 1535, 1536, 2046, 2047]])
+    res = parity(oracle_mod, dl, "prefill", x, 0.95, it, rows=rows, label="prefill many pairs")
     assert int(res["cnt"].sum()) > 65536
     assert res["cnt"][1::2].max() <= 8
 
 
 def test_llama8b_prefill_ragged_chunks(oracle_mod, llama8b):
     """700 tokens: one full 512-token chunk of the down projection and a ragged
-    one (the 32-row units); rows on both sides of the chunk edge and the last
-    token checked against the oracle."""
+    one (the 32-row units); every row of y against the oracle."""
     L, w, dl = llama8b
     x, _ = make_tokens(700, w.d, 93, row_lognormal_sigma=0.5)
-    parity(oracle_mod, dl, "prefill", x, 0.8, rows=np.array([0, 255, 510, 511, 512, 513, 650, 699]))
+    parity(oracle_mod, dl, "prefill", x, 0.8, label="prefill 700 tokens",
+           max_exempt=full_size_cap(700))
 
 
 def test_qwen_skewed(oracle_mod):
+    """The wide skewed-routing layer (d 3584, E 148, Gumbel router bias,
+    per-token temperature), T = 64: every selection and every row of y."""
     w = WORKLOADS["qwen7b_skewed"]
     L = workload_layer(w, 0)
     x, it = workload_tokens(w, 64, 0)
     with DevLayer(L, 64) as dl:
         for tau in w.taus:
-            res = parity(oracle_mod, dl, "decode", x, tau, it, rows=np.array([0, 21, 42, 63]))
+            res = parity(oracle_mod, dl, "decode", x, tau, it, label="qwen7b skewed",
+                         max_exempt=full_size_cap(64))
             assert res["cnt"].min() >= 1
 
 

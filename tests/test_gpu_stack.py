@@ -13,7 +13,7 @@ import paper_2605_28283_amd as pp
 from paper_2605_28283_amd.stack import DecodeStack
 from paper_2605_28283_amd.workloads import (WORKLOADS, Layer, bf16_to_f32, make_layer_device,
                                             stack_layer_seed, workload_tokens)
-from gpu_helpers import check_output, check_selection
+from gpu_helpers import check_output, check_selection, full_size_cap
 
 pytestmark = pytest.mark.gpu
 
@@ -141,7 +141,8 @@ def test_stack32_teacher_forced(oracle_mod):
     for l in (0, 1, 13, 30, 31):
         L = host_layer(w, l)
         u_bits = us[l].view(np.uint16)
-        r, exempt = check_selection(oracle_mod, L, u_bits, tau, 0, idx[l], cnt[l])
+        r, _, _ = check_selection(oracle_mod, L, u_bits, tau, 0, idx[l], cnt[l],
+                                  label="stack32 layer %d" % l, max_exempt=full_size_cap(w.T[0]))
         check_output(oracle_mod, L, u_bits, 0, idx[l], cnt[l], ys[l], r["g"])
         ks.append(cnt[l].mean())
     union = [len(np.unique(idx[l][idx[l] >= 0])) for l in range(w.layers)]

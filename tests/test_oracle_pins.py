@@ -315,10 +315,78 @@ def test_scalar_closed_form(oracle_mod):
     assert abs(y[0, 9] - s1 * (-2.0) * h[200]) < 1e-14
 
 
-def test_near_tie_helper(oracle_mod):
-    cum = np.array([[0.5, 0.899995, 1.0], [0.5, 0.95, 1.0]])
-    assert list(oracle_mod.near_tie(cum, 0.9)) == [True, False]
-    assert not oracle_mod.near_tie(cum, 1.0).any()
+def test_near_tie_nucleus_branch(oracle_mod):
+    """Cumulative-mass ties: C_1..C_{E-1} within the band of tau (inclusive),
+    C_E ignored (it is 1 and decides nothing for tau < 1), nothing at tau >= 1."""
+    b = 2.0 ** -17  # exact in binary, so the band edge is exact
+    cum = np.array([[0.5, 0.9 - b, 1.0],         # at the band edge: tie
+                    [0.5, 0.9 - 2 * b, 1.0],     # twice the band away: no tie
+                    [0.9 + b / 2, 0.95, 1.0],    # first position inside the band
+                    [0.5, 0.95, 1.0]])
+    assert list(oracle_mod.near_tie(cum, 0.9, band=b)) == [True, False, True, False]
+    # C_E = 1 lies within the band of tau = 1 - b/2, but it is not a cut position
+    cum2 = np.array([[0.5, 0.9, 1.0], [0.5, 1.0 - b, 1.0]])
+    assert list(oracle_mod.near_tie(cum2, 1.0 - b / 2, band=b)) == [False, True]
+    assert not oracle_mod.near_tie(cum, 1.0, band=b).any()
+    assert not oracle_mod.near_tie(cum2, 1.05, band=b).any()
+
+
+def test_near_tie_strict_and_rule_branches(oracle_mod):
+    """Strict: tau = 1 is a cut (E - 1 kept in exact arithmetic), so masses
+    within the band of 1 are ties; tau > 1 keeps all (no ties).  Top-k and
+    LTE do not read C."""
+    S = oracle_mod.SELECT_STRICT
+    cum = np.array([[0.6, 0.999995, 1.0], [0.6, 0.99, 1.0]])
+    assert list(oracle_mod.near_tie(cum, 1.0, flags=S)) == [True, False]
+    assert list(oracle_mod.near_tie(cum, 0.6, flags=S)) == [True, True]
+    assert not oracle_mod.near_tie(cum, 1.05, flags=S).any()
+    for rule in (oracle_mod.SELECT_TOPK, oracle_mod.SELECT_LTE):
+        assert not oracle_mod.near_tie(cum, 0.6, flags=rule).any()
+        assert not oracle_mod.near_tie(cum, 1.0, flags=rule).any()
+
+
+def test_cut_and_prefix_order_ties(oracle_mod):
+    """Logit ties by position in the descending order, hand cases: a gap at
+    the cut (pi_k vs pi_{k+1}), a gap inside the kept prefix, no gap, the
+    band edge, nothing to cut (k = E) and logits given in expert order (the
+    helpers sort them)."""
+    b = 2.0 ** -17
+    g = np.array([[3.0, 2.0, 2.0 - b, 0.0]])   # the tie is between ranks 2 and 3
+    cases = [  # (count, tie at the cut, tie inside the prefix)
+        (1, False, False), (2, True, False), (3, False, True), (4, False, True)]
+    for k, cut, pre in cases:
+        c = np.array([k])
+        assert oracle_mod.cut_order_tie(g, c, band=b)[0] == cut, k
+        assert oracle_mod.prefix_order_tie(g, c, band=b)[0] == pre, k
+    # twice the band apart: no tie anywhere
+    g2 = np.array([[3.0, 2.0, 2.0 - 2 * b, 0.0]])
+    for k in (1, 2, 3, 4):
+        assert not oracle_mod.cut_order_tie(g2, np.array([k]), band=b)[0]
+        assert not oracle_mod.prefix_order_tie(g2, np.array([k]), band=b)[0]
+    # the same logits in shuffled expert order, several tokens at once
+    gs = np.array([[0.0, 2.0 - b, 3.0, 2.0], [2.0, 0.0, 3.0, 2.0 - b], [3.0, 2.0, 1.0, 0.0]])
+    cnt = np.array([2, 3, 2])
+    assert list(oracle_mod.cut_order_tie(gs, cnt, band=b)) == [True, False, False]
+    assert list(oracle_mod.prefix_order_tie(gs, cnt, band=b)) == [False, True, False]
+    # LTE may keep nothing: no cut, no prefix
+    assert not oracle_mod.cut_order_tie(g, np.array([0]), band=b)[0]
+    assert not oracle_mod.prefix_order_tie(g, np.array([0]), band=b)[0]
+    # default band is the benchmark's 1e-5
+    g3 = np.array([[1.0, 1.0 - 9e-6, -1.0], [1.0, 1.0 - 1.1e-5, -1.0]])
+    assert list(oracle_mod.cut_order_tie(g3, np.array([1, 1]))) == [True, False]
+
+
+def test_lte_tie(oracle_mod):
+    """Sigmoid scores within the band of delta: logit(delta) exactly, just
+    inside and just outside the band (sigmoid'(0) = 1/4), and any expert of
+    the token counts."""
+    d = 0.5
+    inside, outside = 4 * 0.9e-6, 4 * 1.1e-6  # sigmoid(z) - 1/2 ~ z / 4
+    g = np.array([[0.0, 3.0], [3.0, inside], [3.0, outside], [-outside, 5.0], [-3.0, 3.0]])
+    assert list(oracle_mod.lte_tie(g, d)) == [True, True, False, False, False]
+    # another delta: logit(0.9) = log 9
+    g9 = np.array([[math.log(9.0), -1.0], [math.log(9.0) + 1e-3, -1.0]])
+    assert list(oracle_mod.lte_tie(g9, 0.9)) == [True, False]
 
 
 # ------------------------------------------- stacked-workload wiring (RMSNorm)
