@@ -50,12 +50,20 @@ _lib = None
 
 
 def load():
-    """Load the HIP library (raises OSError if it has not been built)."""
+    """Load the HIP library (raises OSError if it has not been built).
+
+    torch is imported first: its wheel carries its own HIP runtime, which the
+    process must share with the library.  Both runtimes have the soname
+    libamdhip64.so.7, but torch asks for it by the unversioned name, so a
+    library loaded before torch would bind to the system runtime and torch
+    would then map its own: device memory from one runtime and kernel launches
+    on the other fail."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise OSError("libprunepath.so not built: run __graft_entry__.build() "
                           "or python paper_2605_28283_amd/build.py")
+        import torch  # noqa: F401  (maps torch's HIP runtime before the library's dependency)
         lib = ctypes.CDLL(LIB_PATH)
         P, I32, U32, F32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_float
         lib.prunepath_create.argtypes = [ctypes.POINTER(ctypes.c_void_p), I32, I32, I32, I32,

@@ -196,3 +196,18 @@ def test_kmeans_workspace_and_rejections():
                                            a["ws"], None)
         assert st == pp.PP_EINVAL, b
     assert pp.prunepath_status_string(pp.PP_ENOTCONVERGED) == "did not converge"
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Loading the library before torch must not map a second HIP runtime
+    (torch's wheel carries its own; both would serve the same GPU with
+    separate state, and launches on pointers from the other one fail)."""
+    import subprocess
+    import sys
+    code = ("import paper_2605_28283_amd as pp; pp.load(); import torch; "
+            "print(len(set(l.split()[-1] for l in open('/proc/self/maps') "
+            "if 'libamdhip64' in l)))")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip().splitlines()[-1] == "1"
