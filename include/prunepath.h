@@ -206,6 +206,27 @@ pp_status prunepath_router_loss(const float *g, int32_t B, int32_t E, float eps,
                                 float lambda, float gamma, float *losses, float *dg,
                                 void *workspace, void *hip_stream);
 
+/* prunepath_router_loss_noalloc -- prunepath_router_loss for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight training
+ * or serving loops, harnesses that forbid hipMalloc.  Same arguments, results
+ * and bits as prunepath_router_loss, minus `workspace`: the partial sums live
+ * in a device array inside the library, PP_ROUTER_LOSS_NOALLOC_SCRATCH_BYTES
+ * (4 MiB) per GPU, held until the process ends.  Calls no allocator.
+ *  - Sizes: prunepath_router_loss_workspace(B, E) must not exceed the array
+ *    (ceil(B / 64) * (E + 2) * 4 bytes: B up to 588672 rows at E = 112,
+ *    260096 at E = 256); larger sizes return PP_EUNSUPPORTED, enqueue nothing.
+ *  - The first call on each device looks up that device's copy of the array
+ *    (hipGetSymbolAddress); make it outside any graph capture.
+ *  - Every call on one GPU shares its array: calls that can overlap on one GPU
+ *    (two streams, two threads, two captured graphs replayed concurrently)
+ *    race and give undefined results.  The array needs no clearing: each call
+ *    overwrites the partials it reads.
+ * Other errors as for prunepath_router_loss. */
+#define PP_ROUTER_LOSS_NOALLOC_SCRATCH_BYTES (4u << 20)
+pp_status prunepath_router_loss_noalloc(const float *g, int32_t B, int32_t E, float eps,
+                                        float eta, float lambda, float gamma, float *losses,
+                                        float *dg, void *hip_stream);
+
 /* prunepath_balanced_kmeans -- MoEfication's neuron clustering (Sec. 2.2):
  * balanced k-means of the n rows of F into k clusters of exactly m = n / k
  * rows (the constrained k-means the paper cites), which gives the

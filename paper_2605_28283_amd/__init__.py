@@ -12,5 +12,6 @@ from ._lib import (EXPORTED, PP_AGG_SIGMOID, PP_AGG_SUM, PP_EHIP, PP_EINVAL, PP_
                    prunepath_create_mlp,
                    prunepath_destroy, prunepath_ffn_decode, prunepath_ffn_prefill,
                    prunepath_profile_begin, prunepath_profile_end, prunepath_residual_rmsnorm,
-                   prunepath_route, prunepath_router_loss, prunepath_router_loss_workspace,
+                   prunepath_route, prunepath_router_loss, prunepath_router_loss_noalloc,
+                   prunepath_router_loss_workspace,
                    prunepath_status_string)

@@ -37,6 +37,7 @@ EXPORTED = ("prunepath_create", "prunepath_create_mlp", "prunepath_route", "prun
             "prunepath_ffn_prefill", "prunepath_destroy", "prunepath_status_string",
             "prunepath_profile_begin", "prunepath_profile_end", "prunepath_residual_rmsnorm",
             "prunepath_router_loss_workspace", "prunepath_router_loss",
+            "prunepath_router_loss_noalloc",
             "prunepath_kmeans_workspace", "prunepath_balanced_kmeans")
 
 
@@ -90,6 +91,8 @@ def load():
         lib.prunepath_router_loss_workspace.restype = ctypes.c_size_t
         lib.prunepath_router_loss.argtypes = [P, I32, I32, F32, F32, F32, F32, P, P, P, P]
         lib.prunepath_router_loss.restype = ctypes.c_int
+        lib.prunepath_router_loss_noalloc.argtypes = [P, I32, I32, F32, F32, F32, F32, P, P, P]
+        lib.prunepath_router_loss_noalloc.restype = ctypes.c_int
         lib.prunepath_kmeans_workspace.argtypes = [I32, I32, I32]
         lib.prunepath_kmeans_workspace.restype = ctypes.c_size_t
         lib.prunepath_balanced_kmeans.argtypes = [P, I32, I32, I32, P, I32, P, P, P, P, P, P, P,
@@ -213,6 +216,15 @@ def prunepath_router_loss(g, B, E, eps, eta, lam, gamma, losses, dg, workspace, 
                                       _ptr(losses, "f32"), _ptr(dg, "f32"), _ptr(workspace),
                                       _stream(stream))
     _check(st, "prunepath_router_loss")
+
+
+def prunepath_router_loss_noalloc(g, B, E, eps, eta, lam, gamma, losses, dg, stream=None):
+    """prunepath_router_loss with the library's own device scratch (no
+    workspace argument, nothing allocated)."""
+    st = load().prunepath_router_loss_noalloc(_ptr(g, "f32"), B, E, eps, eta, lam, gamma,
+                                              _ptr(losses, "f32"), _ptr(dg, "f32"),
+                                              _stream(stream))
+    _check(st, "prunepath_router_loss_noalloc")
 
 
 def prunepath_kmeans_workspace(n, D, k):

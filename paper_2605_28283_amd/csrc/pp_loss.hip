@@ -24,6 +24,8 @@
 // exp, log and reciprocal use the hardware instructions (1 ulp); kernels are
 // instantiated for each ceil(E / 16).
 #include <array>
+#include <atomic>
+#include <mutex>
 #include <utility>
 
 #include "pp_internal.h"
@@ -308,6 +310,56 @@ constexpr auto kLaunchers = make_launchers(std::make_integer_sequence<int, kMaxE
 }  // namespace
 }  // namespace pp
 
+// ---------------------------------------------- allocation-free variant
+// The partials of prunepath_router_loss_noalloc live in this file-scope
+// device array (one copy per GPU, held until the process ends).  In host code
+// the name `scratch` is a host-side stand-in, not a device address: kernels
+// take the address hipGetSymbolAddress returns on each device, kept in
+// g_scratch_dev.
+constexpr size_t kLossScratchBytes = PP_ROUTER_LOSS_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) float scratch[kLossScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<float *> g_scratch_dev[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of `scratch` on the current device, resolved on the first
+// call on each device and kept.
+pp_status loss_scratch_address(float **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return PP_EHIP;
+    if (dev < 0 || dev >= kMaxDevices) return PP_EUNSUPPORTED;
+    float *p = g_scratch_dev[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_dev[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            void *a = nullptr;
+            if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || !a) return PP_EHIP;
+            p = static_cast<float *>(a);
+            g_scratch_dev[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return PP_OK;
+}
+
+// Argument checks shared by both entry points (workspace aside).
+pp_status check_loss_args(const float *g, int32_t B, int32_t E, float eps, float eta,
+                          float lambda, float gamma, const float *losses, const float *dg) {
+    if (!g || !losses || dg == g) return PP_EINVAL;
+    if (B < 1 || B > pp::kMaxLossRows || E < 1 || E > pp::kMaxExperts) return PP_EINVAL;
+    if (!(eps >= 0.0f && eps <= 3.0e38f) || !(fabsf(eta) <= 3.0e38f) ||
+        !(fabsf(lambda) <= 3.0e38f) || !(fabsf(gamma) <= 3.0e38f))
+        return PP_EINVAL;
+    if (((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(dg)) & 15) ||
+        (reinterpret_cast<uintptr_t>(losses) & 3))
+        return PP_EINVAL;
+    return PP_OK;
+}
+}  // namespace
+
 extern "C" size_t prunepath_router_loss_workspace(int32_t B, int32_t E) {
     if (B < 1 || B > pp::kMaxLossRows || E < 1 || E > pp::kMaxExperts) return 0;
     return sizeof(float) * (size_t)pp::rows_blocks(B) * ((size_t)E + 2);
@@ -316,16 +368,27 @@ extern "C" size_t prunepath_router_loss_workspace(int32_t B, int32_t E) {
 extern "C" pp_status prunepath_router_loss(const float *g, int32_t B, int32_t E, float eps,
                                            float eta, float lambda, float gamma, float *losses,
                                            float *dg, void *workspace, void *hip_stream) {
-    if (!g || !losses || !workspace || dg == g) return PP_EINVAL;
-    if (B < 1 || B > pp::kMaxLossRows || E < 1 || E > pp::kMaxExperts) return PP_EINVAL;
-    if (!(eps >= 0.0f && eps <= 3.0e38f) || !(fabsf(eta) <= 3.0e38f) ||
-        !(fabsf(lambda) <= 3.0e38f) || !(fabsf(gamma) <= 3.0e38f))
-        return PP_EINVAL;
-    if (((reinterpret_cast<uintptr_t>(g) | reinterpret_cast<uintptr_t>(dg)) & 15) ||
-        ((reinterpret_cast<uintptr_t>(losses) | reinterpret_cast<uintptr_t>(workspace)) & 3))
-        return PP_EINVAL;
+    pp_status st = check_loss_args(g, B, E, eps, eta, lambda, gamma, losses, dg);
+    if (st != PP_OK) return st;
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 3)) return PP_EINVAL;
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     pp::kLaunchers[(E + 15) / 16 - 1](g, B, E, eps, eta, lambda, gamma, losses, dg,
                                       static_cast<float *>(workspace), s);
+    return hipGetLastError() == hipSuccess ? PP_OK : PP_EHIP;
+}
+
+extern "C" pp_status prunepath_router_loss_noalloc(const float *g, int32_t B, int32_t E,
+                                                   float eps, float eta, float lambda,
+                                                   float gamma, float *losses, float *dg,
+                                                   void *hip_stream) {
+    pp_status st = check_loss_args(g, B, E, eps, eta, lambda, gamma, losses, dg);
+    if (st != PP_OK) return st;
+    if (prunepath_router_loss_workspace(B, E) > kLossScratchBytes) return PP_EUNSUPPORTED;
+    float *ws = nullptr;
+    st = loss_scratch_address(&ws);
+    if (st != PP_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    // the kernels overwrite every partial they read: nothing to clear
+    pp::kLaunchers[(E + 15) / 16 - 1](g, B, E, eps, eta, lambda, gamma, losses, dg, ws, s);
     return hipGetLastError() == hipSuccess ? PP_OK : PP_EHIP;
 }
