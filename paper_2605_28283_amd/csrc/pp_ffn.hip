@@ -1,9 +1,9 @@
 // Prefill expert evaluation: Eq. (ffn) restricted to the kept experts and
 // summed per token, Eqs. (moefication_decomp) and (moe_output), for large T.
 //
-// Work is organised in "groups" listed by a plan: one expert with up to 64 of
-// the tokens that kept it.  dispatch_k buckets the tokens per expert and
-// splits each bucket into groups of 64; each (token, expert) pair owns one
+// Work is organised in "groups" listed by a plan: one expert with up to 128
+// of the tokens that kept it.  dispatch_k buckets the tokens per expert and
+// splits each bucket into groups of 128; each (token, expert) pair owns one
 // row of the h scratch, rows numbered group by group, tokens ascending inside
 // a group.
 //
@@ -11,13 +11,14 @@
 //                 (ballot prefix over blocks of 256 tokens + scatter), where
 //                 each chunk of kPfChunk tokens starts in it, and the plan,
 //                 written by the last expert to finish.
-//   gateup_pf_k : unit = (group, K-slice); the gate/up projections and the
-//                 SiLU product of one group (shared with the decode kernel).
+//   gateup_pf_k : unit = one group, all of K, one workgroup per CU; the
+//                 gate/up projections and the SiLU product (bf16 MFMA, each
+//                 weight fragment read once per group).
 //   down_rows_k : unit = (R rows of d, chunk of kPfChunk tokens); the chunk's
 //                 y rows are summed in LDS over the experts in ascending
 //                 order and written once -- no float atomics, deterministic.
-// Units sharing weights (an expert's K-slices and groups; a row block's token
-// chunks) are placed on one XCD, where they meet in L2.
+// Units sharing weights (an expert's groups; a row block's token chunks) are
+// placed on one XCD, where they meet in L2.
 #include "pp_gateup.h"
 
 namespace pp {
@@ -37,33 +38,146 @@ struct DNParams {
     PlanView plan;
 };
 
-// Token-row loads per thread in flight while staging a prefill group.
-constexpr int kPfStageBatch = 4;
+// Gate/up of one group (one expert, up to kPfGroupTokens of its tokens) in
+// one workgroup, all 256 gate/up columns and all of K: wavefront w owns the
+// expert's neuron tile w (16 neurons, gate and up) for every token tile of
+// the group, so each weight fragment is read once per group, by one
+// wavefront, straight from HBM into registers kPfPF K-steps ahead.  The
+// group's token rows are staged in LDS in B-fragment order, kPfXC K-steps at
+// a time: wavefront w loads token tile w's fragments of the next sub-chunk
+// into registers while the current one is multiplied, and stores them after
+// it (two LDS buffers, one barrier per sub-chunk).  One workgroup per CU;
+// the groups of one expert are neighbouring units on one XCD, where they
+// share the expert's weights in L2.
+constexpr int kPfXC = 8;                         // K-steps per staged token sub-chunk
+constexpr int kPfPF = 8;                         // K-steps of weights in flight per wavefront
+constexpr int kPfNT = kPfGroupTokens / 16;       // token tiles per group
+static_assert(kPfXC % kPfPF == 0, "the weight ring restarts at every sub-chunk");
+static_assert(kPfNT == kGuThreads / 64, "wavefront w stages token tile w");
+
+// SiLU(a) * b with the hardware exp2 and reciprocal (about 1 ulp each):
+// a / (1 + e^-a) = a * rcp(1 + 2^(-a log2 e)); a -> -inf gives 0, a -> +inf a.
+__device__ __forceinline__ float silu_mul_fast(float a, float b) {
+    const float t = __builtin_amdgcn_exp2f(-a * 1.44269504088896341f);
+    return a * __builtin_amdgcn_rcpf(1.0f + t) * b;
+}
 
 template <bool GATED>
-__global__ __launch_bounds__(kGuThreads, 4) void gateup_pf_k(GUParams P) {
-    __shared__ uint4 xf[kXBufBytes / 16];
-    __shared__ int stok[kGroupTokens];
-    __shared__ int s_flag;
-    const int tid = threadIdx.x;
+__device__ __forceinline__ float pf_act(const GUParams &P, int e, int r, float a, float b) {
+    if (GATED) return silu_mul_fast(a, b);
+    return act<false>(P, e, r, a, b);
+}
+
+template <bool GATED>
+__device__ __forceinline__ void pf_load_w(const uint16_t *wb, int s, uint4 &g, uint4 &u) {
+    const uint16_t *p = wb + (size_t)s * kStepElems<GATED>;
+    g = ldg16(p);
+    if (GATED) u = ldg16(p + 512);
+}
+
+template <bool GATED>
+__global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
+    __shared__ uint4 xs[2][kPfXC][kPfNT][64];
+    __shared__ int stok[kPfGroupTokens];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int nG = P.plan.head[0];
-    const int npairs = P.plan.head[1];
-    const int KS = choose_ks(P, nG, npairs, (int)gridDim.x);
-    const int units = nG * KS;
-    // consecutive units (K-slices of a group, then the groups of one expert)
-    // go to the same XCD, where they share the expert's weights in L2
-    const int slots = 8 * ((units + 7) / 8);
+    const int NS = P.NS, last = NS - 1;
+    const bool sig = (P.flags & PP_AGG_SIGMOID) != 0;
+    const int slots = 8 * ((nG + 7) / 8);
     for (int slot = blockIdx.x; slot < slots; slot += gridDim.x) {
-        const int unit = xcd_order(slot, units);
-        if (unit >= units) continue;
-        const int g = unit / KS, ks = unit - g * KS;
-        const int e = P.plan.grp_e[g];
-        const int n = P.plan.grp_n[g];
-        const int p0 = P.plan.grp_pair[g];
+        const int g = xcd_order(slot, nG);
+        if (g >= nG) continue;
+        const int e = P.plan.grp_e[g], n = P.plan.grp_n[g], p0 = P.plan.grp_pair[g];
+        __syncthreads();  // the previous group is done with stok and xs
         if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
         __syncthreads();
-        gateup_group<GATED, 4, kPF, kPfStageBatch>(P, e, n, p0, g, ks, KS, npairs, stok, xf, &s_flag);
+        const int nt = (n + 15) >> 4;
+        const bool stager = wv < nt;
+        // this lane's token row while staging tile wv (slots past the group
+        // read its last token: they only feed output columns never stored)
+        const uint16_t *xr =
+            P.x + (size_t)stok[min(16 * wv + (lane & 15), n - 1)] * P.d + 8 * (lane >> 4);
+        const uint16_t *wb =
+            P.Wgu + (size_t)(e * 8 + wv) * NS * kStepElems<GATED> + lane * 8;
+        uint4 G[kPfPF], U[kPfPF], xv[kPfXC];
+#pragma unroll
+        for (int i = 0; i < kPfPF; ++i) pf_load_w<GATED>(wb, min(i, last), G[i], U[i]);
+        if (stager) {
+#pragma unroll
+            for (int k = 0; k < kPfXC; ++k) xv[k] = ldg16(xr + min(k, last) * kKStep);
+#pragma unroll
+            for (int k = 0; k < kPfXC; ++k) xs[0][k][wv][lane] = xv[k];
+        }
         __syncthreads();
+        f32x4 ag[kPfNT], au[kPfNT];
+#pragma unroll
+        for (int j = 0; j < kPfNT; ++j) {
+            ag[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            au[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        for (int s0 = 0, c = 0; s0 < NS; s0 += kPfXC, ++c) {
+            const bool more = s0 + kPfXC < NS;
+            if (stager && more) {
+#pragma unroll
+                for (int k = 0; k < kPfXC; ++k)
+                    xv[k] = ldg16(xr + min(s0 + kPfXC + k, last) * kKStep);
+            }
+            const uint4 *xb = &xs[c & 1][0][0][0];
+            // the token fragments of step k are read from LDS one step ahead
+            uint4 b[kPfNT];
+#pragma unroll
+            for (int j = 0; j < kPfNT; ++j) b[j] = xb[j * 64 + lane];
+#pragma unroll
+            for (int k = 0; k < kPfXC; ++k) {
+                uint4 bn[kPfNT];
+                if (k + 1 < kPfXC) {
+#pragma unroll
+                    for (int j = 0; j < kPfNT; ++j) bn[j] = xb[((k + 1) * kPfNT + j) * 64 + lane];
+                }
+                if (s0 + k < NS) {
+#pragma unroll
+                    for (int j = 0; j < kPfNT / 2; ++j) {
+                        ag[j] = mfma16(G[k % kPfPF], b[j], ag[j]);
+                        if (GATED) au[j] = mfma16(U[k % kPfPF], b[j], au[j]);
+                    }
+                    if (nt > kPfNT / 2) {
+#pragma unroll
+                        for (int j = kPfNT / 2; j < kPfNT; ++j) {
+                            ag[j] = mfma16(G[k % kPfPF], b[j], ag[j]);
+                            if (GATED) au[j] = mfma16(U[k % kPfPF], b[j], au[j]);
+                        }
+                    }
+                }
+                pf_load_w<GATED>(wb, min(s0 + k + kPfPF, last), G[k % kPfPF], U[k % kPfPF]);
+                if (k + 1 < kPfXC) {
+#pragma unroll
+                    for (int j = 0; j < kPfNT; ++j) b[j] = bn[j];
+                }
+            }
+            if (stager && more) {
+#pragma unroll
+                for (int k = 0; k < kPfXC; ++k) xs[(c + 1) & 1][k][wv][lane] = xv[k];
+            }
+            __syncthreads();
+        }
+        // lane holds neurons r0 .. r0 + 3 of token slot 16 j + lane % 16
+        const int r0 = wv * 16 + 4 * (lane >> 4);
+#pragma unroll
+        for (int j = 0; j < kPfNT; ++j) {
+            const int q = 16 * j + (lane & 15);
+            if (j < nt && q < n) {
+                const float scl = sig ? P.gsig[(size_t)stok[q] * P.E + e] : 1.0f;
+                uint16_t hi[4], lo[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    split_bf16(pf_act<GATED>(P, e, r0 + i, ag[j][i], au[j][i]) * scl, hi[i], lo[i]);
+                const size_t row = (size_t)(p0 + q) * kExpertWidth + r0;
+                *reinterpret_cast<uint2 *>(P.h_hi + row) =
+                    make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+                *reinterpret_cast<uint2 *>(P.h_lo + row) =
+                    make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+            }
+        }
     }
 }
 
@@ -116,9 +230,12 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
         st_dev_u32(reinterpret_cast<uint32_t *>(ecount + e), (uint32_t)base);
     }
     if (!arrive_last(cnt, (unsigned)E, &s_flag)) return;
-    // prefill plan: expert e's bucket becomes ceil(c_e / 64) groups
+    // prefill plan: expert e's bucket becomes ceil(c_e / kPfGroupTokens) groups
+    // of nearly equal size (the first c_e % groups one token larger), so that
+    // the groups of one expert stream its weights at the same pace and meet
+    // in L2
     const int c = (tid < E) ? (int)ld_dev_u32(reinterpret_cast<uint32_t *>(ecount + tid)) : 0;
-    const int nch = (c + kGroupTokens - 1) / kGroupTokens;
+    const int nch = (c + kPfGroupTokens - 1) / kPfGroupTokens;
     int cb, off, nG, npairs;
     block_excl_scan2(nch, c, &cb, &off, &nG, &npairs, scan);
     if (tid < E) {
@@ -126,12 +243,14 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
         ebase[tid] = off;
     }
     if (tid == 0) plan.egrp[E] = nG;
-    for (int ch = 0; ch < nch; ++ch) {
-        const int g = cb + ch;
+    const int gbase = nch > 0 ? c / nch : 0, grem = nch > 0 ? c - gbase * nch : 0;
+    for (int ch = 0, first = 0; ch < nch; ++ch) {
+        const int g = cb + ch, n = gbase + (ch < grem ? 1 : 0);
         plan.grp_e[g] = tid;
-        plan.grp_pair[g] = off + ch * kGroupTokens;
-        plan.grp_n[g] = min(kGroupTokens, c - ch * kGroupTokens);
-        plan.grp_tok[g] = tid * stride + ch * kGroupTokens;
+        plan.grp_pair[g] = off + first;
+        plan.grp_n[g] = n;
+        plan.grp_tok[g] = tid * stride + first;
+        first += n;
     }
     if (tid == 0) {
         plan.head[0] = nG;
@@ -403,14 +522,13 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     prof_mark(L, PP_KERNEL_DISPATCH, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    static const int occ_g = resident(gateup_pf_k<true>, kGuThreads);
-    static const int occ_p = resident(gateup_pf_k<false>, kGuThreads);
     const GUParams gp = gu_params(L, x, T, true);
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
+    // one workgroup per CU (the kernel's registers and LDS allow no more)
     if (L->gated)
-        hipLaunchKernelGGL(gateup_pf_k<true>, dim3(occ_g * L->num_cu), dim3(kGuThreads), 0, s, gp);
+        hipLaunchKernelGGL(gateup_pf_k<true>, dim3(L->num_cu), dim3(kGuThreads), 0, s, gp);
     else
-        hipLaunchKernelGGL(gateup_pf_k<false>, dim3(occ_p * L->num_cu), dim3(kGuThreads), 0, s, gp);
+        hipLaunchKernelGGL(gateup_pf_k<false>, dim3(L->num_cu), dim3(kGuThreads), 0, s, gp);
     prof_mark(L, PP_KERNEL_GATEUP, s, false);
     err = hipGetLastError();
     if (err != hipSuccess) return err;

@@ -18,7 +18,8 @@ constexpr int kDecodeChunks = 16;      // expert chunks of the dense-group decod
 constexpr int kRouteTile = 16;         // tokens / experts per router MFMA tile
 constexpr int kMaxWidth = 8192;        // largest supported d
 constexpr int kPfChunk = 512;          // tokens per prefill down unit (their y rows stay in LDS)
-constexpr int kGroupTokens = 64;       // tokens per prefill expert group
+constexpr int kGroupTokens = 64;       // tokens per decode expert group (one u64 token mask)
+constexpr int kPfGroupTokens = 128;    // tokens per prefill expert group
 constexpr int kMinStepsPerSlice = 8;   // K-steps each gate/up K-slice covers at least
 
 // Byte sizes of the scratch areas whose size does not follow from max_tokens.
