@@ -13,7 +13,9 @@
 //                 written by the last expert to finish.
 //   gateup_pf_k : unit = one group, all of K, one workgroup per CU; the
 //                 gate/up projections and the SiLU product (bf16 MFMA, each
-//                 weight fragment read once per group).
+//                 weight fragment read once per group).  The groups of a last,
+//                 partial round are split along K into pieces whose partial
+//                 sums the last piece adds in piece order.
 //   down_rows_k : unit = (R rows of d, chunk of kPfChunk tokens); the chunk's
 //                 y rows are summed in LDS over the experts in ascending
 //                 order and written once -- no float atomics, deterministic.
@@ -50,7 +52,7 @@ struct DNParams {
 // the groups of one expert are neighbouring units on one XCD, where they
 // share the expert's weights in L2.
 constexpr int kPfXC = 8;                         // K-steps per staged token sub-chunk
-constexpr int kPfPF = 8;                         // K-steps of weights in flight per wavefront
+constexpr int kPfPF = 4;                         // K-steps of weights in flight per wavefront
 constexpr int kPfNT = kPfGroupTokens / 16;       // token tiles per group
 static_assert(kPfXC % kPfPF == 0, "the weight ring restarts at every sub-chunk");
 static_assert(kPfNT == kGuThreads / 64, "wavefront w stages token tile w");
@@ -75,20 +77,62 @@ __device__ __forceinline__ void pf_load_w(const uint16_t *wb, int s, uint4 &g, u
     if (GATED) u = ldg16(p + 512);
 }
 
+// Work list of gateup_pf_k with nG groups on nW workgroups: full rounds of
+// whole groups (nW groups each), then the groups left over, each split into
+// KS pieces along K (at most nW pieces in all), so that the last round uses
+// every workgroup instead of leaving most of them idle.
+struct PfSchedule {
+    int full;    // groups run whole: [0, full)
+    int KS;      // pieces per leftover group (1 when nothing is left over)
+    int units;   // full + (nG - full) * KS
+};
+
+__device__ __forceinline__ PfSchedule pf_schedule(int nG, int nW, size_t part_rows) {
+    PfSchedule S;
+    S.full = nG - nG % nW;
+    const int left = nG - S.full;
+    S.KS = 1;
+    if (left > 0 && S.full > 0) {
+        S.KS = min(nW / left, 4);
+        // each piece's partial rows (up to kPfGroupTokens per group) must fit
+        while (S.KS > 1 && (size_t)left * S.KS * kPfGroupTokens > part_rows) --S.KS;
+        if (S.KS < 1) S.KS = 1;
+    }
+    if (S.KS == 1) S.full = nG;
+    S.units = S.full + (nG - S.full) * S.KS;
+    return S;
+}
+
 template <bool GATED>
 __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
     __shared__ uint4 xs[2][kPfXC][kPfNT][64];
     __shared__ int stok[kPfGroupTokens];
+    __shared__ int s_flag;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int nG = P.plan.head[0];
     const int NS = P.NS, last = NS - 1;
+    const int nsub = (NS + kPfXC - 1) / kPfXC;  // token sub-chunks over all of K
     const bool sig = (P.flags & PP_AGG_SIGMOID) != 0;
-    const int slots = 8 * ((nG + 7) / 8);
-    for (int slot = blockIdx.x; slot < slots; slot += gridDim.x) {
-        const int g = xcd_order(slot, nG);
-        if (g >= nG) continue;
+    const PfSchedule S = pf_schedule(nG, (int)gridDim.x, P.abpart_rows);
+    const int slots_full = 8 * ((S.full + 7) / 8);
+    for (int slot = blockIdx.x; slot < slots_full + (S.units - S.full); slot += gridDim.x) {
+        // unit: a whole group (xcd-ordered, so an expert's groups share an
+        // XCD), or piece `piece` of leftover group g (pieces of one group are
+        // neighbouring slots)
+        int g, piece = 0, KSg = 1;
+        if (slot < slots_full) {
+            g = xcd_order(slot, S.full);
+            if (g >= S.full) continue;
+        } else {
+            const int v = slot - slots_full;
+            g = S.full + v / S.KS;
+            piece = v - (g - S.full) * S.KS;
+            KSg = S.KS;
+        }
+        const int cA = piece * nsub / KSg, cB = (piece + 1) * nsub / KSg;
+        const int sA = cA * kPfXC, sB = min(cB * kPfXC, NS);
         const int e = P.plan.grp_e[g], n = P.plan.grp_n[g], p0 = P.plan.grp_pair[g];
-        __syncthreads();  // the previous group is done with stok and xs
+        __syncthreads();  // the previous unit is done with stok and xs
         if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
         __syncthreads();
         const int nt = (n + 15) >> 4;
@@ -101,10 +145,10 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
             P.Wgu + (size_t)(e * 8 + wv) * NS * kStepElems<GATED> + lane * 8;
         uint4 G[kPfPF], U[kPfPF], xv[kPfXC];
 #pragma unroll
-        for (int i = 0; i < kPfPF; ++i) pf_load_w<GATED>(wb, min(i, last), G[i], U[i]);
+        for (int i = 0; i < kPfPF; ++i) pf_load_w<GATED>(wb, min(sA + i, last), G[i], U[i]);
         if (stager) {
 #pragma unroll
-            for (int k = 0; k < kPfXC; ++k) xv[k] = ldg16(xr + min(k, last) * kKStep);
+            for (int k = 0; k < kPfXC; ++k) xv[k] = ldg16(xr + min(sA + k, last) * kKStep);
 #pragma unroll
             for (int k = 0; k < kPfXC; ++k) xs[0][k][wv][lane] = xv[k];
         }
@@ -115,8 +159,8 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
             ag[j] = f32x4{0.f, 0.f, 0.f, 0.f};
             au[j] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        for (int s0 = 0, c = 0; s0 < NS; s0 += kPfXC, ++c) {
-            const bool more = s0 + kPfXC < NS;
+        for (int s0 = sA, c = 0; s0 < sB; s0 += kPfXC, ++c) {
+            const bool more = s0 + kPfXC < sB;
             if (stager && more) {
 #pragma unroll
                 for (int k = 0; k < kPfXC; ++k)
@@ -134,7 +178,7 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
 #pragma unroll
                     for (int j = 0; j < kPfNT; ++j) bn[j] = xb[((k + 1) * kPfNT + j) * 64 + lane];
                 }
-                if (s0 + k < NS) {
+                if (s0 + k < sB) {
 #pragma unroll
                     for (int j = 0; j < kPfNT / 2; ++j) {
                         ag[j] = mfma16(G[k % kPfPF], b[j], ag[j]);
@@ -162,6 +206,44 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
         }
         // lane holds neurons r0 .. r0 + 3 of token slot 16 j + lane % 16
         const int r0 = wv * 16 + 4 * (lane >> 4);
+        if (KSg > 1) {
+            // a piece of a split group: its partial (a, b) in fragment order,
+            // [piece][token tile][wavefront][a, b][lane] float4 (one KiB per
+            // wavefront store); the last piece to arrive adds the pieces in
+            // piece order at its own fragments and goes on to the epilogue
+            constexpr unsigned kPieceBytes = kPfNT * 8 * 2 * 64 * 16;
+            const auto pr = buf_rsrc(P.abpart + (size_t)(g - S.full) * KSg * (kPieceBytes / 4),
+                                     (unsigned)KSg * kPieceBytes);
+            const unsigned lo = ((unsigned)wv * 2 * 64 + lane) * 16;
+#pragma unroll
+            for (int j = 0; j < kPfNT; ++j) {
+                if (j < nt) {
+                    const unsigned o = (unsigned)piece * kPieceBytes + j * (8 * 2 * 64 * 16) + lo;
+                    st_dev16(pr, o, ag[j]);
+                    if (GATED) st_dev16(pr, o + 64 * 16, au[j]);
+                }
+            }
+            if (!arrive_last(&P.cnt[g], (unsigned)KSg, &s_flag)) continue;
+            f32x4 sa[kPfNT], su[kPfNT];
+            for (int k = 0; k < KSg; ++k) {
+#pragma unroll
+                for (int j = 0; j < kPfNT; ++j) {
+                    f32x4 va = ag[j], vu = au[j];
+                    if (k != piece && j < nt) {
+                        const unsigned o = (unsigned)k * kPieceBytes + j * (8 * 2 * 64 * 16) + lo;
+                        va = ld_dev16(pr, o);
+                        if (GATED) vu = ld_dev16(pr, o + 64 * 16);
+                    }
+                    sa[j] = k == 0 ? va : sa[j] + va;
+                    su[j] = k == 0 ? vu : su[j] + vu;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kPfNT; ++j) {
+                ag[j] = sa[j];
+                au[j] = su[j];
+            }
+        }
 #pragma unroll
         for (int j = 0; j < kPfNT; ++j) {
             const int q = 16 * j + (lane & 15);
@@ -170,12 +252,13 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
                 uint16_t hi[4], lo[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    split_bf16(pf_act<GATED>(P, e, r0 + i, ag[j][i], au[j][i]) * scl, hi[i], lo[i]);
+                    split_bf16(pf_act<GATED>(P, e, r0 + i, ag[j][i], au[j][i]) * scl, hi[i],
+                               lo[i]);
                 const size_t row = (size_t)(p0 + q) * kExpertWidth + r0;
-                *reinterpret_cast<uint2 *>(P.h_hi + row) =
-                    make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
-                *reinterpret_cast<uint2 *>(P.h_lo + row) =
-                    make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+                *reinterpret_cast<uint2 *>(P.h_hi + row) = make_uint2(
+                    hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+                *reinterpret_cast<uint2 *>(P.h_lo + row) = make_uint2(
+                    lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
             }
         }
     }

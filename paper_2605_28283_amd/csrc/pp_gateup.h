@@ -187,16 +187,17 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
         }
         return;
     }
+    {
+        // each lane's four neurons as one 16-byte store (the lanes of a token
+        // slot fill 64 contiguous bytes of its row)
+        const auto pr = buf_rsrc(P.abpart, (unsigned)(P.abpart_rows * 256 * sizeof(float)));
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-        const int q = 16 * j + (lane & 15);
-        if (q < n) {
-            float *row = P.abpart + ((size_t)ks * npairs + p0 + q) * 256 + r0;
-            st_dev2(row, ag[j][0], ag[j][1]);
-            st_dev2(row + 2, ag[j][2], ag[j][3]);
-            if (GATED) {
-                st_dev2(row + 128, au[j][0], au[j][1]);
-                st_dev2(row + 130, au[j][2], au[j][3]);
+        for (int j = 0; j < NT; ++j) {
+            const int q = 16 * j + (lane & 15);
+            if (q < n) {
+                const unsigned o = (unsigned)(((size_t)ks * npairs + p0 + q) * 256 + r0) * 4u;
+                st_dev16(pr, o, ag[j]);
+                if (GATED) st_dev16(pr, o + 128 * 4u, au[j]);
             }
         }
     }

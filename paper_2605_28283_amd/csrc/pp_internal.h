@@ -220,6 +220,19 @@ __device__ __forceinline__ float2 ld_dev2(const float *p) {
         __HIP_MEMORY_SCOPE_AGENT);
     return make_float2(__uint_as_float((uint32_t)u), __uint_as_float((uint32_t)(u >> 32)));
 }
+// 16-byte stores and loads at the device coherence point through a raw
+// buffer (cache policy sc1, what the agent-scope atomic stores and loads
+// above compile to), for partial results laid out in MFMA fragment order:
+// one wavefront instruction then moves one contiguous KiB instead of
+// scattered 8-byte pieces.
+constexpr int kCpolDevice = 16;  // sc1
+__device__ __forceinline__ void st_dev16(__amdgpu_buffer_rsrc_t r, unsigned off, f32x4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, off, 0, kCpolDevice);
+}
+__device__ __forceinline__ f32x4 ld_dev16(__amdgpu_buffer_rsrc_t r, unsigned off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolDevice));
+}
+
 // Wait until this thread's outstanding vector-memory operations completed
 // (s_waitcnt vmcnt(0); the expcnt and lgkmcnt fields are left at their maxima).
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
