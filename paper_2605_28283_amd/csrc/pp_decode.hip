@@ -514,6 +514,7 @@ __device__ void sh_unit(const DNParams &P, DnShared &S, int c, int rb, int Uc, i
     }
     __syncthreads();
     const int nq = nrows / 4;
+    const auto pr = buf_rsrc(P.ypart, (unsigned)((size_t)kDecodeChunks * T * d * 4u));
     for (int i = tid; i < T * nq; i += blockDim.x) {
         const int t = i / nq, r = 4 * (i - t * nq);
         float4 v = *reinterpret_cast<const float4 *>(&S.yacc[t][r]);
@@ -528,53 +529,52 @@ __device__ void sh_unit(const DNParams &P, DnShared &S, int c, int rb, int Uc, i
             }
             *reinterpret_cast<float4 *>(P.y + (size_t)t * d + col) = v;
         } else {
-            float *dst = P.ypart + ((size_t)c * T + t) * d + col;
-            st_dev2(dst, v.x, v.y);
-            st_dev2(dst + 2, v.z, v.w);
+            st_dev16(pr, (unsigned)(((size_t)c * T + t) * d + col) * 4u, f32x4{v.x, v.y, v.z, v.w});
         }
     }
     if (ES == 1 || !arrive_last(&P.dn_cnt[rb], (unsigned)ES, flag)) return;
     // last chunk to arrive: y = sum of the chunk partials in chunk order, all
-    // of a thread's loads for kRedChunks chunks issued at once
-    constexpr int kRedPer = kDecodeTile * (kShRows / 2) / kDnThreads;
+    // of a thread's 16-byte loads for kRedChunks chunks issued at once
+    constexpr int kRedPer = kDecodeTile * (kShRows / 4) / kDnThreads;
     constexpr int kRedChunks = 4;
-    const int nh = nrows / 2, nel = T * nh;
+    const int nq4 = nrows / 4, nel = T * nq4;
     int off[kRedPer];
-    float2 acc[kRedPer];
+    f32x4 acc[kRedPer];
 #pragma unroll
     for (int q = 0; q < kRedPer; ++q) {
-        const int i = min(tid + kDnThreads * q, nel - 1), t = i / nh;
-        off[q] = t * d + rb * kShRows + 2 * (i - t * nh);
-        acc[q] = make_float2(0.f, 0.f);
+        const int i = min(tid + kDnThreads * q, nel - 1), t = i / nq4;
+        off[q] = t * d + rb * kShRows + 4 * (i - t * nq4);
+        acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     const int nown = (nel - tid + kDnThreads - 1) / kDnThreads;
     for (int k0 = 0; k0 < ES; k0 += kRedChunks) {
-        float2 v[kRedChunks][kRedPer];
+        f32x4 v[kRedChunks][kRedPer];
 #pragma unroll
         for (int k = 0; k < kRedChunks; ++k) {
-            const float *base = P.ypart + (size_t)min(k0 + k, ES - 1) * T * d;
+            const size_t base = (size_t)min(k0 + k, ES - 1) * T * d;
 #pragma unroll
             for (int q = 0; q < kRedPer; ++q)
-                v[k][q] = q < nown ? ld_dev2(base + off[q]) : make_float2(0.f, 0.f);
+                v[k][q] = q < nown ? ld_dev16(pr, (unsigned)(base + off[q]) * 4u)
+                                   : f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
         for (int k = 0; k < kRedChunks; ++k)
             if (k0 + k < ES)
 #pragma unroll
-                for (int q = 0; q < kRedPer; ++q) {
-                    acc[q].x += v[k][q].x;
-                    acc[q].y += v[k][q].y;
-                }
+                for (int q = 0; q < kRedPer; ++q) acc[q] += v[k][q];
     }
 #pragma unroll
     for (int q = 0; q < kRedPer; ++q) {
         if (q < nown) {
+            float4 o = make_float4(acc[q][0], acc[q][1], acc[q][2], acc[q][3]);
             if (P.bproj) {
-                const float2 b = *reinterpret_cast<const float2 *>(P.bproj + off[q] % d);
-                acc[q].x += b.x;
-                acc[q].y += b.y;
+                const float4 b = *reinterpret_cast<const float4 *>(P.bproj + off[q] % d);
+                o.x += b.x;
+                o.y += b.y;
+                o.z += b.z;
+                o.w += b.w;
             }
-            *reinterpret_cast<float2 *>(P.y + off[q]) = acc[q];
+            *reinterpret_cast<float4 *>(P.y + off[q]) = o;
         }
     }
 }
