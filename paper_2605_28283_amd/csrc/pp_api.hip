@@ -87,6 +87,13 @@ pp_status run_ffn(pp_layer *L, const uint16_t *x, int32_t T, float tau, const fl
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     const int E = L->dm.E, d = L->dm.d;
     const int slice = prefill ? T : kDecodeTile;
+    // every token keeps every expert (nucleus with tau >= 1, strict with
+    // tau > 1, top-k with k >= E): a decode slice of at least 16 tokens then
+    // runs its gate/up as grouped work (below 16 the K-split units are faster)
+    const uint32_t sel = L->flags & (PP_SELECT_STRICT | PP_SELECT_TOPK | PP_SELECT_LTE);
+    const bool all_kept = (sel == PP_SELECT_NUCLEUS && tau >= 1.0f) ||
+                          (sel == PP_SELECT_STRICT && tau > 1.0f) ||
+                          (sel == PP_SELECT_TOPK && floorf(tau + 0.5f) >= (float)E);
     for (int t0 = 0; t0 < T; t0 += slice) {
         const int n = (T - t0 < slice) ? T - t0 : slice;
         int32_t *idx = expert_idx ? expert_idx + (size_t)t0 * E : L->idx_tmp;
@@ -96,7 +103,8 @@ pp_status run_ffn(pp_layer *L, const uint16_t *x, int32_t T, float tau, const fl
         const float *it = inv_temp ? inv_temp + t0 : nullptr;
         hipError_t e = launch_route(L, xs, n, tau, it, idx, cnt, nullptr, !prefill, s);
         if (e == hipSuccess)
-            e = prefill ? launch_prefill_ffn(L, xs, n, ys, s) : launch_decode_ffn(L, xs, n, ys, s);
+            e = prefill ? launch_prefill_ffn(L, xs, n, ys, s)
+                        : launch_decode_ffn(L, xs, n, ys, all_kept && n >= 16, s);
         if (e != hipSuccess) return hip_status(e);
     }
     return PP_OK;

@@ -680,10 +680,13 @@ void launch_gateup_dec_t(const GUParams &gp, int T, int num_cu, hipStream_t s) {
         launch_gateup_dec<GATED, 4, kPF>(gp, num_cu, s);
 }
 
-hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s) {
+hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, bool dense,
+                             hipStream_t s) {
     const GUParams gp = gu_params(L, x, T, false);
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
-    if (L->gated)
+    if (dense)
+        launch_gateup_dense_dec(L, x, T, s);
+    else if (L->gated)
         launch_gateup_dec_t<true>(gp, T, L->num_cu, s);
     else
         launch_gateup_dec_t<false>(gp, T, L->num_cu, s);

@@ -79,8 +79,9 @@ __device__ __forceinline__ void pf_load_w(const uint16_t *wb, int s, uint4 &g, u
 
 // Work list of gateup_pf_k with nG groups on nW workgroups: full rounds of
 // whole groups (nW groups each), then the groups left over, each split into
-// KS pieces along K (at most nW pieces in all), so that the last round uses
-// every workgroup instead of leaving most of them idle.
+// KS pieces along K (at most nW pieces in all, at most four per group), so
+// that the last (or only) round uses more of the workgroups instead of
+// leaving them idle.
 struct PfSchedule {
     int full;    // groups run whole: [0, full)
     int KS;      // pieces per leftover group (1 when nothing is left over)
@@ -92,7 +93,7 @@ __device__ __forceinline__ PfSchedule pf_schedule(int nG, int nW, size_t part_ro
     S.full = nG - nG % nW;
     const int left = nG - S.full;
     S.KS = 1;
-    if (left > 0 && S.full > 0) {
+    if (left > 0) {
         S.KS = min(nW / left, 4);
         // each piece's partial rows (up to kPfGroupTokens per group) must fit
         while (S.KS > 1 && (size_t)left * S.KS * kPfGroupTokens > part_rows) --S.KS;
@@ -103,13 +104,18 @@ __device__ __forceinline__ PfSchedule pf_schedule(int nG, int nW, size_t part_ro
     return S;
 }
 
-template <bool GATED>
+// DEC: a decode batch whose groups come from the router's per-expert token
+// masks (the decode plan, derived here in LDS as the decode gate/up kernel
+// does; workgroup 0 stores it for the down projection).
+template <bool GATED, bool DEC>
 __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
     __shared__ uint4 xs[2][kPfXC][kPfNT][64];
     __shared__ int stok[kPfGroupTokens];
     __shared__ int s_flag;
+    __shared__ DecodePlan D;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int nG = P.plan.head[0];
+    if (DEC) decode_plan<true>(P, D, tid < P.E ? P.emask[tid] : 0ull);
+    const int nG = DEC ? D.nG : P.plan.head[0];
     const int NS = P.NS, last = NS - 1;
     const int nsub = (NS + kPfXC - 1) / kPfXC;  // token sub-chunks over all of K
     const bool sig = (P.flags & PP_AGG_SIGMOID) != 0;
@@ -131,9 +137,20 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
         }
         const int cA = piece * nsub / KSg, cB = (piece + 1) * nsub / KSg;
         const int sA = cA * kPfXC, sB = min(cB * kPfXC, NS);
-        const int e = P.plan.grp_e[g], n = P.plan.grp_n[g], p0 = P.plan.grp_pair[g];
+        int e, n, p0;
         __syncthreads();  // the previous unit is done with stok and xs
-        if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
+        if (DEC) {
+            const unsigned long long m = D.mask[g];
+            e = D.e[g];
+            n = __popcll(m);
+            p0 = D.pair[g];
+            if (tid < 64 && ((m >> tid) & 1ull)) stok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
+        } else {
+            e = P.plan.grp_e[g];
+            n = P.plan.grp_n[g];
+            p0 = P.plan.grp_pair[g];
+            if (tid < n) stok[tid] = P.plan.toklist[P.plan.grp_tok[g] + tid];
+        }
         __syncthreads();
         const int nt = (n + 15) >> 4;
         const bool stager = wv < nt;
@@ -585,6 +602,16 @@ DNParams dn_params(pp_layer *L, int T, float *y) {
 
 }  // namespace
 
+// Gate/up of a decode batch in which every token keeps every expert (dense):
+// the grouped kernel above, its groups from the decode plan.
+void launch_gateup_dense_dec(pp_layer *L, const uint16_t *x, int T, hipStream_t s) {
+    const GUParams gp = gu_params(L, x, T, false);
+    if (L->gated)
+        hipLaunchKernelGGL((gateup_pf_k<true, true>), dim3(L->num_cu), dim3(kGuThreads), 0, s, gp);
+    else
+        hipLaunchKernelGGL((gateup_pf_k<false, true>), dim3(L->num_cu), dim3(kGuThreads), 0, s, gp);
+}
+
 counter_layout counters_for(const pp_dims &dm, int max_tokens) {
     counter_layout c;
     c.route = 0;
@@ -609,9 +636,9 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
     // one workgroup per CU (the kernel's registers and LDS allow no more)
     if (L->gated)
-        hipLaunchKernelGGL(gateup_pf_k<true>, dim3(L->num_cu), dim3(kGuThreads), 0, s, gp);
+        hipLaunchKernelGGL((gateup_pf_k<true, false>), dim3(L->num_cu), dim3(kGuThreads), 0, s, gp);
     else
-        hipLaunchKernelGGL(gateup_pf_k<false>, dim3(L->num_cu), dim3(kGuThreads), 0, s, gp);
+        hipLaunchKernelGGL((gateup_pf_k<false, false>), dim3(L->num_cu), dim3(kGuThreads), 0, s, gp);
     prof_mark(L, PP_KERNEL_GATEUP, s, false);
     err = hipGetLastError();
     if (err != hipSuccess) return err;

@@ -131,7 +131,11 @@ hipError_t launch_repack(pp_layer *L, const uint16_t *W_gate, const uint16_t *W_
 hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const float *inv_temp,
                         int32_t *idx, int32_t *count, float *gate_w, bool build_plan,
                         hipStream_t s);
-hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
+// dense: every token keeps every expert (the gate/up then runs as grouped
+// MFMA work like prefill).
+hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, bool dense,
+                             hipStream_t s);
+void launch_gateup_dense_dec(pp_layer *L, const uint16_t *x, int T, hipStream_t s);
 hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
 
 inline PlanView plan_view(pp_layer *L, bool prefill) {
