@@ -74,8 +74,8 @@ __device__ __forceinline__ void tile_load(const uint16_t *wb, const uint16_t *co
     for (int i = 0; i < PF; ++i) {
         const int s = min(step + i, last);
         const uint16_t *p = wb + (size_t)s * kStepElems<GATED>;
-        G[i] = ldg16(p);
-        if (GATED) U[i] = ldg16(p + 512);
+        G[i] = ldw16(p);
+        if (GATED) U[i] = ldw16(p + 512);
 #pragma unroll
         for (int j = 0; j < NT; ++j) B[i][j] = ldg16(xr[j] + s * kKStep);
     }
@@ -293,6 +293,10 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         extra = min(nG, max(0, slots - nG * KS));
     const int big = extra * (KS + 1);
     const int units = nG * KS + extra;
+    // streaming weight loads for large unions (the K-slice units of non-gated
+    // layers keep plain loads: their kernel for batches past 32 tokens has no
+    // registers left for a second copy of the unit loop)
+    const bool stream = GATED && __builtin_amdgcn_readfirstlane(nG) >= kStreamGroups;
     for (int unit = (int)blockIdx.x; unit < units; unit += slots) {
         int g, ks, ksg;
         if (unit < big) {
@@ -308,8 +312,12 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         const unsigned long long m = D.mask[g];
         if (tid < 64 && ((m >> tid) & 1ull)) stok[__popcll(m & ((1ull << tid) - 1ull))] = tid;
         __syncthreads();
-        gateup_group<GATED, NTMAX, PF>(P, D.e[g], __popcll(m), D.pair[g], g, ks, ksg, npairs, stok,
-                                       xf, &s_flag);
+        if (stream)
+            gateup_group<GATED, NTMAX, PF, true>(P, D.e[g], __popcll(m), D.pair[g], g, ks, ksg,
+                                                 npairs, stok, xf, &s_flag);
+        else
+            gateup_group<GATED, NTMAX, PF, false>(P, D.e[g], __popcll(m), D.pair[g], g, ks, ksg,
+                                                  npairs, stok, xf, &s_flag);
         __syncthreads();
     }
 }
@@ -349,7 +357,7 @@ struct RowCursor {
     }
 };
 
-template <int R>
+template <int R, bool STREAM>
 __device__ __forceinline__ void load_row_item(const DNParams &P, RowCursor &c, int rt, int RT,
                                               int lane, RowItem<R> &it) {
     const uint4 z = make_uint4(0, 0, 0, 0);
@@ -359,7 +367,7 @@ __device__ __forceinline__ void load_row_item(const DNParams &P, RowCursor &c, i
     for (int m = 0; m < R; ++m) {
         const uint16_t *wp = P.Wd + (((size_t)c.e * RT + rt + m) * 4 * 64 + lane) * 8;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) it.w[m][s] = ldg16(wp + s * 512);
+        for (int s = 0; s < 4; ++s) it.w[m][s] = ldw16_if<STREAM>(wp + s * 512);
     }
     const int slot = 16 * c.j + (lane & 15);
     const bool ok = slot < c.n;
@@ -420,7 +428,7 @@ __device__ __forceinline__ void sh_load_w(const DNParams &P, int u, int rt, int 
     const uint16_t *wp =
         P.Wd + (((size_t)P.plan.grp_e[u] * RT + min(rt, RT - 1)) * 4 * 64 + lane) * 8;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) w[s] = ldg16(wp + s * 512);
+    for (int s = 0; s < 4; ++s) w[s] = ldw16(wp + s * 512);
 }
 
 // Piece wv (hi/lo x K-step) of group u's h B fragments and the tokens of
@@ -579,18 +587,61 @@ __device__ void sh_unit(const DNParams &P, DnShared &S, int c, int rb, int Uc, i
     }
 }
 
+// Sparse groups: unit = R 16-row tiles of d over every group of the plan,
+// the wavefronts' LDS accumulators summed in wavefront order and y written
+// once.  STREAM: the down weights come by streaming (nontemporal) loads.
+template <int TB, int R, bool STREAM>
+__device__ void rows_sparse(const DNParams &P, DnRow<TB, R> &rw, int nU) {
+    constexpr int YS = 16 * R + 4;
+    constexpr int NW = kDnThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int RT = P.d / 16;
+    float(*acc)[YS] = rw.yacc[wv];
+    for (int rt = blockIdx.x * R; rt < RT; rt += gridDim.x * R) {
+        for (int i = lane; i < P.T * YS; i += 64) acc[i / YS][i % YS] = 0.0f;
+        RowCursor c;
+        c.u = __builtin_amdgcn_readfirstlane(wv);
+        c.j = 0;
+        c.n = 0;
+        c.stride = NW;
+        c.nU = nU;
+        c.enter(P.plan);
+        // ring of kDnRing items: the next item's loads go out before each apply
+        RowItem<R> it[kDnRing];
+#pragma unroll
+        for (int q = 0; q < kDnRing - 1; ++q) load_row_item<R, STREAM>(P, c, rt, RT, lane, it[q]);
+        for (bool more = true; more;) {
+#pragma unroll
+            for (int q = 0; q < kDnRing; ++q) {
+                if (!it[q].live) {
+                    more = false;
+                    break;
+                }
+                load_row_item<R, STREAM>(P, c, rt, RT, lane, it[(q + kDnRing - 1) % kDnRing]);
+                apply_row_item<R, YS>(it[q], lane, acc);
+            }
+        }
+        __syncthreads();
+        for (int i = tid; i < P.T * 16 * R; i += blockDim.x) {
+            const int t = i / (16 * R), r = i - t * 16 * R;
+            float v = rw.yacc[0][t][r];
+#pragma unroll
+            for (int w = 1; w < NW; ++w) v += rw.yacc[w][t][r];
+            if (P.bproj) v += P.bproj[rt * 16 + r];
+            P.y[(size_t)t * P.d + rt * 16 + r] = v;
+        }
+        __syncthreads();
+    }
+}
+
 template <int TB, int R>
 __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
-    constexpr int YS = 16 * R + 4;  // padded accumulator row (floats)
-    constexpr int NW = kDnThreads / 64;
     __shared__ union {
         DnShared sh;
         DnRow<TB, R> rw;
     } S;
     __shared__ int s_flag;
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int nU = P.plan.head[0], npairs = P.plan.head[1];
-    const int RT = P.d / 16;
     // Dense groups (more than 8 tokens per group on average): reading h once
     // per 16-row tile would cost more than the weights, so share it through
     // LDS across 128-row units, with the groups split into chunks.
@@ -609,42 +660,10 @@ __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
         }
         return;
     }
-    float(*acc)[YS] = S.rw.yacc[wv];
-    for (int rt = blockIdx.x * R; rt < RT; rt += gridDim.x * R) {
-        for (int i = lane; i < P.T * YS; i += 64) acc[i / YS][i % YS] = 0.0f;
-        RowCursor c;
-        c.u = __builtin_amdgcn_readfirstlane(wv);
-        c.j = 0;
-        c.n = 0;
-        c.stride = NW;
-        c.nU = nU;
-        c.enter(P.plan);
-        // ring of kDnRing items: the next item's loads go out before each apply
-        RowItem<R> it[kDnRing];
-#pragma unroll
-        for (int q = 0; q < kDnRing - 1; ++q) load_row_item<R>(P, c, rt, RT, lane, it[q]);
-        for (bool more = true; more;) {
-#pragma unroll
-            for (int q = 0; q < kDnRing; ++q) {
-                if (!it[q].live) {
-                    more = false;
-                    break;
-                }
-                load_row_item<R>(P, c, rt, RT, lane, it[(q + kDnRing - 1) % kDnRing]);
-                apply_row_item<R, YS>(it[q], lane, acc);
-            }
-        }
-        __syncthreads();
-        for (int i = tid; i < P.T * 16 * R; i += blockDim.x) {
-            const int t = i / (16 * R), r = i - t * 16 * R;
-            float v = S.rw.yacc[0][t][r];
-#pragma unroll
-            for (int w = 1; w < NW; ++w) v += S.rw.yacc[w][t][r];
-            if (P.bproj) v += P.bproj[rt * 16 + r];
-            P.y[(size_t)t * P.d + rt * 16 + r] = v;
-        }
-        __syncthreads();
-    }
+    if (__builtin_amdgcn_readfirstlane(nU) >= kStreamGroups)
+        rows_sparse<TB, R, true>(P, S.rw, nU);
+    else
+        rows_sparse<TB, R, false>(P, S.rw, nU);
 }
 
 // ------------------------------------------------------------------ launchers

@@ -70,11 +70,14 @@ __device__ __forceinline__ float pf_act(const GUParams &P, int e, int r, float a
     return act<false>(P, e, r, a, b);
 }
 
-template <bool GATED>
+// STREAM: a dense decode batch (every expert kept) streams the weights; a
+// prefill group's weights are shared with the other groups of its expert in
+// L2 and are read with plain loads.
+template <bool GATED, bool STREAM>
 __device__ __forceinline__ void pf_load_w(const uint16_t *wb, int s, uint4 &g, uint4 &u) {
     const uint16_t *p = wb + (size_t)s * kStepElems<GATED>;
-    g = ldg16(p);
-    if (GATED) u = ldg16(p + 512);
+    g = ldw16_if<STREAM>(p);
+    if (GATED) u = ldw16_if<STREAM>(p + 512);
 }
 
 // Work list of gateup_pf_k with nG groups on nW workgroups: full rounds of
@@ -162,7 +165,7 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
             P.Wgu + (size_t)(e * 8 + wv) * NS * kStepElems<GATED> + lane * 8;
         uint4 G[kPfPF], U[kPfPF], xv[kPfXC];
 #pragma unroll
-        for (int i = 0; i < kPfPF; ++i) pf_load_w<GATED>(wb, min(sA + i, last), G[i], U[i]);
+        for (int i = 0; i < kPfPF; ++i) pf_load_w<GATED, DEC>(wb, min(sA + i, last), G[i], U[i]);
         if (stager) {
 #pragma unroll
             for (int k = 0; k < kPfXC; ++k) xv[k] = ldg16(xr + min(sA + k, last) * kKStep);
@@ -209,7 +212,7 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
                         }
                     }
                 }
-                pf_load_w<GATED>(wb, min(s0 + k + kPfPF, last), G[k % kPfPF], U[k % kPfPF]);
+                pf_load_w<GATED, DEC>(wb, min(s0 + k + kPfPF, last), G[k % kPfPF], U[k % kPfPF]);
                 if (k + 1 < kPfXC) {
 #pragma unroll
                     for (int j = 0; j < kPfNT; ++j) b[j] = bn[j];

@@ -93,14 +93,14 @@ __device__ __forceinline__ void stage_x(const GUParams &P, const int *stok, int 
 template <bool GATED>
 constexpr int kStepElems = GATED ? 1024 : 512;
 
-template <bool GATED, int PF>
+template <bool GATED, int PF, bool STREAM>
 __device__ __forceinline__ void load_wgu(const uint16_t *wb, int step, int last, uint4 (&G)[PF],
                                          uint4 (&U)[PF]) {
 #pragma unroll
     for (int i = 0; i < PF; ++i) {
         const uint16_t *p = wb + (size_t)min(step + i, last) * kStepElems<GATED>;
-        G[i] = ldg16(p);
-        if (GATED) U[i] = ldg16(p + 512);
+        G[i] = ldw16_if<STREAM>(p);
+        if (GATED) U[i] = ldw16_if<STREAM>(p + 512);
     }
 }
 
@@ -136,8 +136,8 @@ __device__ __forceinline__ float act(const GUParams &P, int e, int r, float a, f
 
 // PF: K-steps per register buffer; two buffers alternate, so PF steps of
 // weights are in flight while the other PF are multiplied.
-template <int NT, bool GATED, int PF, int XB>
-__device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int ks, int KS,
+template <int NT, bool GATED, int PF, int XB, bool STREAM>
+__device__ __forceinline__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int ks, int KS,
                             int npairs, const int *stok, uint4 *xf, int *flag) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int s0 = (int)((long)ks * P.NS / KS), s1 = (int)((long)(ks + 1) * P.NS / KS);
@@ -152,13 +152,13 @@ __device__ void gateup_unit(const GUParams &P, int e, int n, int p0, int g, int 
     for (int sc = s0; sc < s1; sc += nsc_max) {
         const int nsc = min(nsc_max, s1 - sc), last = sc + nsc - 1;
         uint4 G0[PF], U0[PF], G1[PF], U1[PF];
-        load_wgu<GATED, PF>(wb, sc, last, G0, U0);  // weights do not wait for the token staging
+        load_wgu<GATED, PF, STREAM>(wb, sc, last, G0, U0);  // weights do not wait for the token staging
         stage_x<NT, XB>(P, stok, n, sc, nsc, xf);
         __syncthreads();
         for (int b = 0; b < nsc; b += 2 * PF) {
-            if (b + PF < nsc) load_wgu<GATED, PF>(wb, sc + b + PF, last, G1, U1);
+            if (b + PF < nsc) load_wgu<GATED, PF, STREAM>(wb, sc + b + PF, last, G1, U1);
             mfma_wgu<NT, GATED, PF>(xf, nsc, b, min(PF, nsc - b), G0, U0, ag, au, lane);
-            if (b + 2 * PF < nsc) load_wgu<GATED, PF>(wb, sc + b + 2 * PF, last, G0, U0);
+            if (b + 2 * PF < nsc) load_wgu<GATED, PF, STREAM>(wb, sc + b + 2 * PF, last, G0, U0);
             if (b + PF < nsc)
                 mfma_wgu<NT, GATED, PF>(xf, nsc, b + PF, min(PF, nsc - b - PF), G1, U1, ag, au,
                                         lane);
@@ -273,7 +273,7 @@ struct DecodePlan {
 
 // m: this thread's expert's token mask (P.emask[threadIdx.x], 0 past E).
 template <bool GLOBAL>
-__device__ void decode_plan(const GUParams &P, DecodePlan &D, unsigned long long m) {
+__device__ __forceinline__ void decode_plan(const GUParams &P, DecodePlan &D, unsigned long long m) {
     const int tid = threadIdx.x, e = tid;
     const int act = m != 0ull ? 1 : 0, pc = __popcll(m);
     int slot, poff, nG, npairs;
@@ -306,19 +306,19 @@ __device__ void decode_plan(const GUParams &P, DecodePlan &D, unsigned long long
 // One group's gate/up unit, dispatched on its number of 16-token tiles (at
 // most NTMAX: a kernel whose groups are known to be small is compiled without
 // the larger tiles' registers and spends them on a deeper weight prefetch PF).
-template <bool GATED, int NTMAX, int PF, int XB = 0>
+template <bool GATED, int NTMAX, int PF, bool STREAM, int XB = 0>
 __device__ __forceinline__ void gateup_group(const GUParams &P, int e, int n, int p0, int g,
                                              int ks, int KS, int npairs, const int *stok,
                                              uint4 *xf, int *flag) {
     const int nt = (n + 15) >> 4;
     if (NTMAX >= 4 && nt >= 4)
-        gateup_unit<(NTMAX >= 4 ? 4 : 1), GATED, PF, XB>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+        gateup_unit<(NTMAX >= 4 ? 4 : 1), GATED, PF, XB, STREAM>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
     else if (NTMAX >= 3 && nt == 3)
-        gateup_unit<(NTMAX >= 3 ? 3 : 1), GATED, PF, XB>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+        gateup_unit<(NTMAX >= 3 ? 3 : 1), GATED, PF, XB, STREAM>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
     else if (NTMAX >= 2 && nt == 2)
-        gateup_unit<(NTMAX >= 2 ? 2 : 1), GATED, PF, XB>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+        gateup_unit<(NTMAX >= 2 ? 2 : 1), GATED, PF, XB, STREAM>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
     else
-        gateup_unit<1, GATED, PF, XB>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
+        gateup_unit<1, GATED, PF, XB, STREAM>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
 }
 
 // K-slices per group: as many as keep all nG * KS units within `slots`

@@ -176,6 +176,21 @@ __device__ __forceinline__ uint4 ldg16(const void *p) {
     return *reinterpret_cast<const uint4 *>(p);
 }
 
+// A weight fragment read once per call: a nontemporal load (streamed past the
+// caches).  When a call touches only a few experts, their weights can stay in
+// the Infinity Cache between calls, so plain loads are kept for small unions
+// (fewer than kStreamGroups kept experts, decided per call on the device).
+__device__ __forceinline__ uint4 ldw16(const void *p) {
+    typedef unsigned int v4 __attribute__((ext_vector_type(4)));
+    const v4 v = __builtin_nontemporal_load(reinterpret_cast<const v4 *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+template <bool STREAM>
+__device__ __forceinline__ uint4 ldw16_if(const void *p) {
+    return STREAM ? ldw16(p) : ldg16(p);
+}
+constexpr int kStreamGroups = 16;
+
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 // A raw buffer over [base, base + bytes): loads past it read zeros without a
