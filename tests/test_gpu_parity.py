@@ -95,6 +95,20 @@ def test_single_and_max_experts(oracle_mod):
                         assert (res["cnt"] == 1).all()
 
 
+def test_max_width(oracle_mod):
+    """The widest supported d (8192): 16 router K-slices of partial logits and
+    256 gate/up K-steps per expert, decode (one token; 70 tokens = a 64-token
+    slice plus a ragged 6) and prefill, sparse and dense (tau 1)."""
+    d = 8192
+    L = make_layer(d, 8 * 128, 8, 31)
+    with DevLayer(L, 128) as dl:
+        for T in (1, 70):
+            x, _ = make_tokens(T, d, 32 + T)
+            for mode in ("decode", "prefill"):
+                for tau in (0.5, 1.0):
+                    parity(oracle_mod, dl, mode, x, tau, label="d=8192 %s" % mode)
+
+
 @pytest.mark.parametrize("flags,params", [
     (TOPK | SUM, (1, 2, 5, 16, 40)),
     (TOPK | SIG, (3,)),
