@@ -289,6 +289,10 @@ __global__ __launch_bounds__(kSelThreads) void select_k(RouteParams P) {
                     uint4 o[4];
 #pragma unroll
                     for (int w = 0; w < 4; ++w) o[w] = kk[u][j + w];
+                    // keep the masses unconditional loads, issued with the
+                    // keys: left to itself the compiler reloads one under its
+                    // comparison (a branch and a second LDS round trip)
+                    asm volatile("" : "+v"(o[0].z), "+v"(o[1].z), "+v"(o[2].z), "+v"(o[3].z));
 #pragma unroll
                     for (int w = 0; w < 4; ++w) {
                         const bool bef = (((unsigned long long)o[w].y << 32) | o[w].x) > ki;
