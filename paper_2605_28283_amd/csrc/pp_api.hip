@@ -101,10 +101,16 @@ pp_status run_ffn(pp_layer *L, const uint16_t *x, int32_t T, float tau, const fl
         const uint16_t *xs = x + (size_t)t0 * d;
         float *ys = y + (size_t)t0 * d;
         const float *it = inv_temp ? inv_temp + t0 : nullptr;
-        hipError_t e = launch_route(L, xs, n, tau, it, idx, cnt, nullptr, !prefill, s);
+        // a single decode token: the gate/up kernel selects its experts itself
+        // (one launch and one round trip fewer)
+        const bool fuse = !prefill && n == 1;
+        const DecodeSelect dsel = {tau, it, idx, cnt};
+        hipError_t e = launch_route(L, xs, n, tau, it, idx, cnt, nullptr, !prefill && !fuse, s,
+                                    !fuse);
         if (e == hipSuccess)
             e = prefill ? launch_prefill_ffn(L, xs, n, ys, s)
-                        : launch_decode_ffn(L, xs, n, ys, all_kept && n >= 16, s);
+                        : launch_decode_ffn(L, xs, n, ys, all_kept && n >= 16, s,
+                                            fuse ? &dsel : nullptr);
         if (e != hipSuccess) return hip_status(e);
     }
     return PP_OK;

@@ -246,15 +246,38 @@ __device__ void tile_units_bits(const GUParams &P, DecodePlan &D, unsigned long 
 
 template <bool GATED, int NTMAX, int PF>
 __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
-    __shared__ uint4 xf[kXBufBytes / 16];
+    static_assert(kGuThreads == kSelThreads, "the selection runs on the whole workgroup");
+    __shared__ union {
+        uint4 xf[kXBufBytes / 16];
+        SelLds<1> sel;  // the single-token selection, before any token is staged
+    } U;
+    uint4 *const xf = U.xf;
     __shared__ int stok[kTileHalves * kGroupTokens];
     __shared__ int s_flag;
     __shared__ DecodePlan D;
     __shared__ unsigned long long s_mask[kMaxExperts];
     __shared__ unsigned long long s_kept[kMaxExperts / 64];
     __shared__ __align__(16) int s_sum[kGuThreads / 64];
+    __shared__ float s_gsig[kMaxExperts];
     const int tid = threadIdx.x;
-    const unsigned long long m_own = tid < P.E ? P.emask[tid] : 0ull;
+    unsigned long long m_own;
+    if (P.select_here) {
+        // single-token decode: every workgroup selects the token's experts
+        // from the partial logits (the same arithmetic as the router's
+        // selection kernel, so the same bits); workgroup 0 stores the
+        // selection outputs, and the gate weights the epilogues scale by
+        // come from LDS
+        const SelOut r = select_tokens<1>(P.rp, 0, U.sel);
+        if (blockIdx.x == 0) select_store<1>(P.rp, U.sel, r);
+        const bool kept = tid < P.E && r.rank < r.k;
+        m_own = kept ? 1ull : 0ull;
+        if (tid < P.E)
+            s_gsig[tid] = (P.flags & PP_AGG_SIGMOID) ? r.sg : 1.0f;
+        P.gsig = s_gsig;
+        __syncthreads();  // the selection's scratch is done with
+    } else {
+        m_own = tid < P.E ? P.emask[tid] : 0ull;
+    }
     if (tid < kMaxExperts) s_mask[tid] = m_own;
     {
         const unsigned long long kb = __ballot(m_own != 0ull);
@@ -700,8 +723,14 @@ void launch_gateup_dec_t(const GUParams &gp, int T, int num_cu, hipStream_t s) {
 }
 
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, bool dense,
-                             hipStream_t s) {
-    const GUParams gp = gu_params(L, x, T, false);
+                             hipStream_t s, const DecodeSelect *sel) {
+    GUParams gp = gu_params(L, x, T, false);
+    if (sel) {
+        if (T != 1 || dense) return hipErrorInvalidValue;
+        gp.select_here = 1;
+        gp.rp = route_params(L, x, T, sel->tau, sel->inv_temp, sel->idx, sel->count, nullptr,
+                             false);
+    }
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
     if (dense)
         launch_gateup_dense_dec(L, x, T, s);

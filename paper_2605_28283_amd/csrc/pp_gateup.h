@@ -14,7 +14,7 @@
 // h is stored as two bf16 numbers, hi = bf16(h) and lo = bf16(h - hi), so the
 // down projection keeps ~16 significant bits of h.
 #pragma once
-#include "pp_internal.h"
+#include "pp_select.h"
 
 namespace pp {
 namespace {
@@ -37,6 +37,10 @@ struct GUParams {
     uint32_t *cnt;
     uint16_t *h_hi;
     uint16_t *h_lo;
+    // single-token decode: the kernel selects the token's experts itself from
+    // the router's partial logits (rp), instead of reading the token masks
+    int select_here;
+    RouteParams rp;
 };
 
 __device__ __forceinline__ void split_bf16(float h, uint16_t &hi, uint16_t &lo) {
@@ -361,6 +365,7 @@ inline GUParams gu_params(pp_layer *L, const uint16_t *x, int T, bool prefill) {
     P.cnt = L->counters + cl.gateup_base();
     P.h_hi = L->h_hi;
     P.h_lo = L->h_lo;
+    P.select_here = 0;
     return P;
 }
 

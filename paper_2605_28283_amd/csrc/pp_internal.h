@@ -128,13 +128,23 @@ inline PlanView plan_view(pp_layer *L, bool prefill);
 hipError_t launch_repack(pp_layer *L, const uint16_t *W_gate, const uint16_t *W_up,
                          const uint16_t *W_down, const int32_t *perm, const float *b_fc,
                          hipStream_t s);
+// select = false launches the router logits only (the single-token decode
+// gate/up kernel then selects the token's experts itself).
 hipError_t launch_route(pp_layer *L, const uint16_t *x, int T, float tau, const float *inv_temp,
                         int32_t *idx, int32_t *count, float *gate_w, bool build_plan,
-                        hipStream_t s);
+                        hipStream_t s, bool select = true);
 // dense: every token keeps every expert (the gate/up then runs as grouped
 // MFMA work like prefill).
+// The selection arguments of a single-token decode call whose gate/up
+// kernel selects the experts itself (after launch_route with select = false).
+struct DecodeSelect {
+    float tau;
+    const float *inv_temp;
+    int32_t *idx;
+    int32_t *count;
+};
 hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, bool dense,
-                             hipStream_t s);
+                             hipStream_t s, const DecodeSelect *sel = nullptr);
 void launch_gateup_dense_dec(pp_layer *L, const uint16_t *x, int T, hipStream_t s);
 hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, hipStream_t s);
 

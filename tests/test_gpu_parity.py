@@ -245,6 +245,24 @@ def test_routing_is_batch_invariant(oracle_mod):
             np.testing.assert_array_equal(part[2].view(np.uint32), full[2][a:b].view(np.uint32))
 
 
+@pytest.mark.parametrize("flags,tau", [(NUC | SIG, 0.8), (STRICT | SUM, 0.8), (TOPK | SIG, 3.0),
+                                       (LTE | SUM, 0.9)])
+def test_single_token_decode_selects_as_router(oracle_mod, flags, tau):
+    """A one-token decode call selects its experts inside the gate/up kernel
+    (every workgroup from the partial logits); the selection must equal the
+    router's for the same token routed in a batch, and y must pass the oracle
+    check."""
+    L = make_layer(1024, 24 * 128, 24, 19)
+    x, _ = make_tokens(40, 1024, 20)
+    with DevLayer(L, 64, flags=flags) as dl:
+        full = dl.run("route", x, tau)
+        for t in (0, 7, 39):
+            idx, cnt, _ = dl.run("decode", x[t:t + 1], tau)
+            np.testing.assert_array_equal(idx[0], full[0][t])
+            assert cnt[0] == full[1][t]
+            parity(oracle_mod, dl, "decode", x[t:t + 1], tau, label="single-token decode")
+
+
 def test_decode_deterministic_and_matches_prefill(tiny):
     L, _ = tiny
     x, _ = make_tokens(48, L.d, 15)
