@@ -63,7 +63,8 @@ def parse_args():
 # projection) are built from: the committed byte counters stay valid while
 # these are unchanged.
 DECODE_SOURCES = ("include/prunepath.h", "paper_2605_28283_amd/csrc/pp_internal.h",
-                  "paper_2605_28283_amd/csrc/pp_gateup.h", "paper_2605_28283_amd/csrc/pp_decode.hip")
+                  "paper_2605_28283_amd/csrc/pp_select.h", "paper_2605_28283_amd/csrc/pp_gateup.h",
+                  "paper_2605_28283_amd/csrc/pp_decode.hip")
 
 
 def source_hash():
