@@ -310,7 +310,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     // hold one unit fewer finish early and the rest form a tail)
     const int slots = (int)gridDim.x;
     const int KS = choose_ks(P, nG, npairs, slots);
-    const int max_ks = P.NS / kMinStepsPerSlice > 0 ? P.NS / kMinStepsPerSlice : 1;
+    const int max_ks = max_slices(P, nG);
     int extra = 0;
     if (KS < max_ks && (size_t)(KS + 1) * npairs <= P.abpart_rows)
         extra = min(nG, max(0, slots - nG * KS));

@@ -325,12 +325,24 @@ __device__ __forceinline__ void gateup_group(const GUParams &P, int e, int n, in
         gateup_unit<1, GATED, PF, XB, STREAM>(P, e, n, p0, g, ks, KS, npairs, stok, xf, flag);
 }
 
+// Most K-slices a group is split into: each slice covers at least
+// kMinStepsPerSlice K-steps, and a small union (at most kSmallUnion kept
+// experts) takes at most kMaxSlicesSmallUnion slices per group: there the
+// hand-off of more, shorter slices costs more than their streaming gains
+// (d = 4096: T = 1, tau 0.9 and T = 8, tau 0.5 / 0.7 gain 1.2-1.8 us per
+// step with 8 slices of 16 K-steps instead of 16 of 8).
+__device__ __forceinline__ int max_slices(const GUParams &P, int nG) {
+    int m = P.NS / kMinStepsPerSlice > 0 ? P.NS / kMinStepsPerSlice : 1;
+    if (nG <= kSmallUnion && m > kMaxSlicesSmallUnion) m = kMaxSlicesSmallUnion;
+    return m;
+}
+
 // K-slices per group: as many as keep all nG * KS units within `slots`
-// workgroups, each slice at least kMinStepsPerSlice K-steps, and the partial
-// rows within the abpart scratch.
+// workgroups, at most max_slices, and the partial rows within the abpart
+// scratch.
 __device__ __forceinline__ int choose_ks(const GUParams &P, int nG, int npairs, int slots) {
     int KS = nG > 0 ? slots / nG : 1;
-    const int max_ks = P.NS / kMinStepsPerSlice > 0 ? P.NS / kMinStepsPerSlice : 1;
+    const int max_ks = max_slices(P, nG);
     if (KS > max_ks) KS = max_ks;
     if (KS > 1 && (size_t)KS * npairs > P.abpart_rows) KS = (int)(P.abpart_rows / npairs);
     return KS < 1 ? 1 : KS;

@@ -21,6 +21,8 @@ constexpr int kPfChunk = 512;          // tokens per prefill down unit (their y 
 constexpr int kGroupTokens = 64;       // tokens per decode expert group (one u64 token mask)
 constexpr int kPfGroupTokens = 128;    // tokens per prefill expert group
 constexpr int kMinStepsPerSlice = 8;   // K-steps each gate/up K-slice covers at least
+constexpr int kMaxSlicesSmallUnion = 8;  // K-slices per group when at most kSmallUnion experts are kept
+constexpr int kSmallUnion = 32;
 
 // Byte sizes of the scratch areas whose size does not follow from max_tokens.
 constexpr size_t kAbPartRows = 65536;  // K-split partial (a,b) rows of 256 floats
