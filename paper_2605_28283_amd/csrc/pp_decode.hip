@@ -52,21 +52,22 @@ struct DNParams {
 // ------------------------------------------------------------------ gate/up
 
 // Neuron-tile units (sparse groups): unit = one 16-neuron tile of one group's
-// expert over all of K, taken by one half of the workgroup; wavefront q of
-// the half takes K quarter q, its token B fragments straight from x (a few
-// tokens, cache resident), the weights PF steps ahead in two register
-// buffers.  The four quarters' (a, b) are added in LDS in quarter order and
-// the half writes h for its 16 neurons: no partial sums leave the workgroup,
-// so no hand-off between workgroups.
-constexpr int kTileHalves = 2;      // units per workgroup at a time
-constexpr int kTileQuarters = 4;    // wavefronts per unit (K split)
+// expert over all of K, taken by PARTS wavefronts of the workgroup --
+// four (half a workgroup) when the union fills the chip, all eight for a
+// small union; wavefront q of the unit takes K part q, its token B
+// fragments straight from x (a few tokens, cache resident), the weights PF
+// steps ahead in two register buffers.  The parts' (a, b) are added in LDS
+// in part order and the unit writes h for its 16 neurons: no partial sums
+// leave the workgroup, so no hand-off between workgroups.
+constexpr int kTileHalves = 2;      // units per workgroup at a time (four-part units)
+constexpr int kTileQuarters = 4;    // wavefronts per unit (K parts) when the union fills the chip
 constexpr int kTilePF = 2;          // K-steps per register buffer (two buffers)
 constexpr int kTileMaxNT = 2;       // token tiles per unit (batches of up to 32 tokens)
 static_assert(kTileHalves * kTileQuarters * 64 == kGuThreads, "two halves of four wavefronts");
 static_assert(kTileHalves * kTileMaxNT * 2 * kTileQuarters * 64 * 16 <= kXBufBytes,
               "the quarters' (a, b) of both halves fit in the token staging buffer");
 
-template <int NT, bool GATED, int PF>
+template <int NT, bool GATED, int PF, bool STREAM>
 __device__ __forceinline__ void tile_load(const uint16_t *wb, const uint16_t *const (&xr)[NT],
                                           int step, int last, uint4 (&G)[PF], uint4 (&U)[PF],
                                           uint4 (&B)[PF][NT]) {
@@ -74,8 +75,8 @@ __device__ __forceinline__ void tile_load(const uint16_t *wb, const uint16_t *co
     for (int i = 0; i < PF; ++i) {
         const int s = min(step + i, last);
         const uint16_t *p = wb + (size_t)s * kStepElems<GATED>;
-        G[i] = ldw16(p);
-        if (GATED) U[i] = ldw16(p + 512);
+        G[i] = ldw16_if<STREAM>(p);
+        if (GATED) U[i] = ldw16_if<STREAM>(p + 512);
 #pragma unroll
         for (int j = 0; j < NT; ++j) B[i][j] = ldg16(xr[j] + s * kKStep);
     }
@@ -97,11 +98,11 @@ __device__ __forceinline__ void tile_mfma(int nvalid, const uint4 (&G)[PF], cons
     }
 }
 
-// One wavefront's K quarter of a tile unit; leaves its (a, b) in red.
-template <int NT, bool GATED, int PF>
-__device__ __forceinline__ void tile_quarter(const GUParams &P, int e, int nt, int n,
-                                             const int *tok, int q, int lane, float4 *red) {
-    const int sA = q * P.NS / kTileQuarters, sB = (q + 1) * P.NS / kTileQuarters;
+// One wavefront's K part q (of PARTS) of a tile unit; leaves its (a, b) in red.
+template <int NT, bool GATED, int PF, int PARTS, bool STREAM>
+__device__ __forceinline__ void tile_part(const GUParams &P, int e, int nt, int n,
+                                          const int *tok, int q, int lane, float4 *red) {
+    const int sA = q * P.NS / PARTS, sB = (q + 1) * P.NS / PARTS;
     const uint16_t *wb = P.Wgu + (size_t)(e * 8 + nt) * P.NS * kStepElems<GATED> + lane * 8;
     const uint16_t *xr[NT];
 #pragma unroll
@@ -119,34 +120,34 @@ __device__ __forceinline__ void tile_quarter(const GUParams &P, int e, int nt, i
     }
     const int last = sB - 1;
     uint4 G0[PF], U0[PF], G1[PF], U1[PF], B0[PF][NT], B1[PF][NT];
-    if (sA < sB) tile_load<NT, GATED, PF>(wb, xr, sA, last, G0, U0, B0);  // d < 128: a quarter may be empty
+    if (sA < sB) tile_load<NT, GATED, PF, STREAM>(wb, xr, sA, last, G0, U0, B0);  // small d: a part may be empty
     for (int s = sA; s < sB; s += 2 * PF) {
-        if (s + PF < sB) tile_load<NT, GATED, PF>(wb, xr, s + PF, last, G1, U1, B1);
+        if (s + PF < sB) tile_load<NT, GATED, PF, STREAM>(wb, xr, s + PF, last, G1, U1, B1);
         tile_mfma<NT, GATED, PF>(min(PF, sB - s), G0, U0, B0, ag, au);
-        if (s + 2 * PF < sB) tile_load<NT, GATED, PF>(wb, xr, s + 2 * PF, last, G0, U0, B0);
+        if (s + 2 * PF < sB) tile_load<NT, GATED, PF, STREAM>(wb, xr, s + 2 * PF, last, G0, U0, B0);
         if (s + PF < sB) tile_mfma<NT, GATED, PF>(min(PF, sB - s - PF), G1, U1, B1, ag, au);
     }
-    // red[(j * 2 + {a, b}) * kTileQuarters + q][lane]
+    // red[(j * 2 + {a, b}) * PARTS + q][lane]
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-        red[((j * 2 + 0) * kTileQuarters + q) * 64 + lane] = make_float4(ag[j][0], ag[j][1], ag[j][2], ag[j][3]);
-        red[((j * 2 + 1) * kTileQuarters + q) * 64 + lane] = make_float4(au[j][0], au[j][1], au[j][2], au[j][3]);
+        red[((j * 2 + 0) * PARTS + q) * 64 + lane] = make_float4(ag[j][0], ag[j][1], ag[j][2], ag[j][3]);
+        red[((j * 2 + 1) * PARTS + q) * 64 + lane] = make_float4(au[j][0], au[j][1], au[j][2], au[j][3]);
     }
 }
 
-// h of a tile unit from the four quarters, summed in quarter order; wavefront
-// j of the half takes token tile j.
-template <int NT, bool GATED>
+// h of a tile unit from its PARTS K parts, summed in part order; wavefront j
+// of the unit takes token tile j.
+template <int NT, bool GATED, int PARTS>
 __device__ __forceinline__ void tile_epilogue(const GUParams &P, int e, int nt, int n, int p0,
                                               const int *tok, int j, int lane, const float4 *red) {
     const int qs = 16 * j + (lane & 15);
     if (j >= NT || qs >= n) return;
-    float4 a = red[((j * 2 + 0) * kTileQuarters + 0) * 64 + lane];
-    float4 b = red[((j * 2 + 1) * kTileQuarters + 0) * 64 + lane];
+    float4 a = red[((j * 2 + 0) * PARTS + 0) * 64 + lane];
+    float4 b = red[((j * 2 + 1) * PARTS + 0) * 64 + lane];
 #pragma unroll
-    for (int q = 1; q < kTileQuarters; ++q) {
-        const float4 pa = red[((j * 2 + 0) * kTileQuarters + q) * 64 + lane];
-        const float4 pb = red[((j * 2 + 1) * kTileQuarters + q) * 64 + lane];
+    for (int q = 1; q < PARTS; ++q) {
+        const float4 pa = red[((j * 2 + 0) * PARTS + q) * 64 + lane];
+        const float4 pb = red[((j * 2 + 1) * PARTS + q) * 64 + lane];
         a.x += pa.x; a.y += pa.y; a.z += pa.z; a.w += pa.w;
         b.x += pb.x; b.y += pb.y; b.z += pb.z; b.w += pb.w;
     }
@@ -198,22 +199,25 @@ __device__ __forceinline__ int nth_set_bit(unsigned long long w, int n) {
 // stream once it has the words; the unit's first pair row (tokens of the
 // kept experts before it) is a wavefront sum of mask popcounts at the end,
 // and workgroup 0 stores the batch plan for the down projection after its
-// units.  Half h of workgroup b takes units b + h * grid, then the next
-// 2 * grid, ... (every workgroup one unit before any takes two); barriers
-// stay outside the per-half work, so both halves meet them whether or not
-// they hold a unit.  A unit of a group with more than 16 tokens takes two
-// token tiles (and one K-step per register buffer, which keeps the kernel
-// within its registers).
-template <bool GATED>
+// units.  A unit takes PARTS wavefronts (K parts), so a workgroup holds
+// 8 / PARTS units at a time: part h of workgroup b takes units b + h * grid,
+// then the next (8 / PARTS) * grid, ... (every workgroup one unit before any
+// takes two); barriers stay outside the per-unit work, so every part meets
+// them whether or not it holds a unit.  A unit of a group with more than 16
+// tokens takes two token tiles (and one K-step per register buffer, which
+// keeps the kernel within its registers).
+template <bool GATED, int PARTS, bool STREAM>
 __device__ void tile_units_bits(const GUParams &P, DecodePlan &D, unsigned long long m_own,
                                 const unsigned long long *s_mask,
                                 const unsigned long long *kept, int nG, int *tokh, float4 *red) {
+    constexpr int HALVES = (kGuThreads / 64) / PARTS;  // units per workgroup at a time
+    static_assert(HALVES * PARTS == kGuThreads / 64 && HALVES <= kTileHalves, "whole wavefronts");
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int half = wv / kTileQuarters, q = wv % kTileQuarters;
+    const int half = wv / PARTS, q = wv % PARTS;
     const int units = nG * 8, grid = (int)gridDim.x;
     int *tok = tokh + half * kGroupTokens;
-    float4 *rh = red + half * (kTileMaxNT * 2 * kTileQuarters * 64);
-    for (int base = 0; base < units; base += kTileHalves * grid) {
+    float4 *rh = red + half * (kTileMaxNT * 2 * PARTS * 64);
+    for (int base = 0; base < units; base += HALVES * grid) {
         const int u = base + half * grid + (int)blockIdx.x;
         const bool act = u < units;
         int g = act ? u >> 3 : 0, wi = 0;
@@ -225,9 +229,9 @@ __device__ void tile_units_bits(const GUParams &P, DecodePlan &D, unsigned long 
         __syncthreads();
         if (act) {
             if (n <= 16)
-                tile_quarter<1, GATED, kTilePF>(P, e, nt, n, tok, q, lane, rh);
+                tile_part<1, GATED, kTilePF, PARTS, STREAM>(P, e, nt, n, tok, q, lane, rh);
             else
-                tile_quarter<2, GATED, 1>(P, e, nt, n, tok, q, lane, rh);
+                tile_part<2, GATED, 1, PARTS, STREAM>(P, e, nt, n, tok, q, lane, rh);
         }
         __syncthreads();
         if (act && q < ((n + 15) >> 4)) {
@@ -235,9 +239,9 @@ __device__ void tile_units_bits(const GUParams &P, DecodePlan &D, unsigned long 
             for (int e2 = lane; e2 < e; e2 += 64) c += __popcll(s_mask[e2]);
             const int p0 = __builtin_amdgcn_readlane(wave_scan_i32(c), 63);
             if (n <= 16)
-                tile_epilogue<1, GATED>(P, e, nt, n, p0, tok, q, lane, rh);
+                tile_epilogue<1, GATED, PARTS>(P, e, nt, n, p0, tok, q, lane, rh);
             else
-                tile_epilogue<2, GATED>(P, e, nt, n, p0, tok, q, lane, rh);
+                tile_epilogue<2, GATED, PARTS>(P, e, nt, n, p0, tok, q, lane, rh);
         }
         __syncthreads();
     }
@@ -297,8 +301,22 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         const int nG = packed & 1023, npairs = packed >> 10;
         const int tiles = nG * 8;
         if (!over32 && tiles >= grid && 2 * tiles <= 3 * grid && npairs <= 4 * nG) {
-            tile_units_bits<GATED>(P, D, m_own, s_mask, s_kept, nG, stok,
-                                   reinterpret_cast<float4 *>(xf));
+            tile_units_bits<GATED, kTileQuarters, true>(P, D, m_own, s_mask, s_kept, nG, stok,
+                                                        reinterpret_cast<float4 *>(xf));
+            return;
+        }
+        // A small union (at most kSmallUnion kept experts, at most one tile
+        // per workgroup): whole-workgroup tile units, eight K parts summed in
+        // LDS -- as many bytes in flight per unit as a K-slice unit, without
+        // the K-slice hand-off between workgroups
+        if (!over32 && nG <= kSmallUnion && tiles <= grid && npairs <= 4 * nG) {
+            float4 *red = reinterpret_cast<float4 *>(xf);
+            if (GATED && nG >= kStreamGroups)
+                tile_units_bits<GATED, kGuThreads / 64, true>(P, D, m_own, s_mask, s_kept, nG,
+                                                              stok, red);
+            else
+                tile_units_bits<GATED, kGuThreads / 64, false>(P, D, m_own, s_mask, s_kept, nG,
+                                                               stok, red);
             return;
         }
     }
