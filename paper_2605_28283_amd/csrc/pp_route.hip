@@ -42,6 +42,25 @@ __global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
     const int tb = blockIdx.x / P.KSr, ks = blockIdx.x - tb * P.KSr;
     if (P.build_plan && blockIdx.x == 0 && tid < P.E) P.emask[tid] = 0ull;
     const int s_end = min(kRouteWaves, P.NS - ks * kRouteWaves);  // K-steps in this slice
+    // wavefront wv < nEt: the router fragments of expert tile wv for the
+    // slice, loaded first so that their round trip overlaps the token staging
+    // (native vectors: an array of uint4 would not stay in registers; an
+    // expert column past E reads a clamped row, and its products land only
+    // in outputs that are never stored)
+    const int ec = wv * kRouteTile + (lane & 15);
+    const bool ve = ec < P.E;
+    u32x4_t b[kRouteWaves];
+    if (wv < P.nEt) {
+        const u32x4_t *wr = reinterpret_cast<const u32x4_t *>(
+            P.Wr + (size_t)min(ec, P.E - 1) * P.d + ks * kRouteWaves * kKStep + 8 * (lane >> 4));
+        if (s_end == kRouteWaves) {  // a whole slice: one base, immediate offsets
+#pragma unroll
+            for (int s = 0; s < kRouteWaves; ++s) b[s] = wr[s * (kKStep / 8)];
+        } else {
+#pragma unroll
+            for (int s = 0; s < kRouteWaves; ++s) b[s] = wr[min(s, s_end - 1) * (kKStep / 8)];
+        }
+    }
     // stage the block's token rows of this slice as MFMA A fragments; every
     // load is issued (addresses clamped into the operands), then rows past T
     // and K-steps past the slice are zeroed
@@ -63,27 +82,11 @@ __global__ __launch_bounds__(1024) void logits_k(RouteParams P) {
     }
     __syncthreads();
     // wavefront wv: expert tile wv for every token tile, K-steps of the slice
-    // accumulated in order in the MFMA accumulators; the slice's router
-    // fragments are all loaded first
-    const int ec = wv * kRouteTile + (lane & 15);
-    const bool ve = ec < P.E;
+    // accumulated in order in the MFMA accumulators
     f32x4 acc[kLgTiles];
 #pragma unroll
     for (int j = 0; j < kLgTiles; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (wv < P.nEt) {
-        // (native vectors: an array of uint4 would not stay in registers; an
-        // expert column past E reads a clamped row, and its products land only
-        // in outputs that are never stored)
-        u32x4_t b[kRouteWaves];
-        const u32x4_t *wr = reinterpret_cast<const u32x4_t *>(
-            P.Wr + (size_t)min(ec, P.E - 1) * P.d + ks * kRouteWaves * kKStep + 8 * (lane >> 4));
-        if (s_end == kRouteWaves) {  // a whole slice: one base, immediate offsets
-#pragma unroll
-            for (int s = 0; s < kRouteWaves; ++s) b[s] = wr[s * (kKStep / 8)];
-        } else {
-#pragma unroll
-            for (int s = 0; s < kRouteWaves; ++s) b[s] = wr[min(s, s_end - 1) * (kKStep / 8)];
-        }
         const int ntile = min(kLgTiles, (P.T - tb * 16 * kLgTiles + 15) / 16);
         // two token tiles at a time (register budget), K-steps in order
 #pragma unroll
