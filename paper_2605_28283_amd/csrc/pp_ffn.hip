@@ -46,11 +46,14 @@ struct DNParams {
 // the group, so each weight fragment is read once per group, by one
 // wavefront, straight from HBM into registers kPfPF K-steps ahead.  The
 // group's token rows are staged in LDS in B-fragment order, kPfXC K-steps at
-// a time: wavefront w loads token tile w's fragments of the next sub-chunk
-// into registers while the current one is multiplied, and stores them after
-// it (two LDS buffers, one barrier per sub-chunk).  One workgroup per CU;
-// the groups of one expert are neighbouring units on one XCD, where they
-// share the expert's weights in L2.
+// a time: wavefront w copies token tile w's fragments of the next sub-chunk
+// straight into LDS (buffer loads to LDS, no registers) while the current
+// one is multiplied -- two LDS buffers, separate arrays so that the
+// compiler's waits for the copies into one do not hold up reads of the
+// other, and one barrier per sub-chunk.  Token tiles are multiplied in
+// pairs, the pairs past the group skipped.  One workgroup per CU; the groups
+// of one expert are neighbouring units on one XCD, where they share the
+// expert's weights in L2.
 constexpr int kPfXC = 8;                         // K-steps per staged token sub-chunk
 constexpr int kPfPF = 4;                         // K-steps of weights in flight per wavefront
 constexpr int kPfNT = kPfGroupTokens / 16;       // token tiles per group
@@ -62,6 +65,13 @@ static_assert(kPfNT == kGuThreads / 64, "wavefront w stages token tile w");
 __device__ __forceinline__ float silu_mul_fast(float a, float b) {
     const float t = __builtin_amdgcn_exp2f(-a * 1.44269504088896341f);
     return a * __builtin_amdgcn_rcpf(1.0f + t) * b;
+}
+
+// Copies 16 bytes per lane from the buffer into LDS: lane l's bytes land at
+// dst + 16 l (dst wavefront-uniform).
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint4 *dst, unsigned off) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        r, (__attribute__((address_space(3))) void *)dst, 16, off, 0, 0, 0);
 }
 
 template <bool GATED>
@@ -112,7 +122,8 @@ __device__ __forceinline__ PfSchedule pf_schedule(int nG, int nW, size_t part_ro
 // does; workgroup 0 stores it for the down projection).
 template <bool GATED, bool DEC>
 __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
-    __shared__ uint4 xs[2][kPfXC][kPfNT][64];
+    __shared__ uint4 xs0[kPfXC][kPfNT][64];
+    __shared__ uint4 xs1[kPfXC][kPfNT][64];
     __shared__ int stok[kPfGroupTokens];
     __shared__ int s_flag;
     __shared__ DecodePlan D;
@@ -159,18 +170,20 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
         const bool stager = wv < nt;
         // this lane's token row while staging tile wv (slots past the group
         // read its last token: they only feed output columns never stored)
-        const uint16_t *xr =
-            P.x + (size_t)stok[min(16 * wv + (lane & 15), n - 1)] * P.d + 8 * (lane >> 4);
+        const unsigned xoff =
+            ((unsigned)stok[min(16 * wv + (lane & 15), n - 1)] * (unsigned)P.d + 8u * (lane >> 4)) * 2u;
+        const auto rx = buf_rsrc(P.x, stager ? (unsigned)((size_t)P.T * P.d * 2u) : 0u);
         const uint16_t *wb =
             P.Wgu + (size_t)(e * 8 + wv) * NS * kStepElems<GATED> + lane * 8;
-        uint4 G[kPfPF], U[kPfPF], xv[kPfXC];
+        uint4 G[kPfPF], U[kPfPF];
 #pragma unroll
         for (int i = 0; i < kPfPF; ++i) pf_load_w<GATED, DEC>(wb, min(sA + i, last), G[i], U[i]);
-        if (stager) {
 #pragma unroll
-            for (int k = 0; k < kPfXC; ++k) xv[k] = ldg16(xr + min(sA + k, last) * kKStep);
-#pragma unroll
-            for (int k = 0; k < kPfXC; ++k) xs[0][k][wv][lane] = xv[k];
+        for (int k = 0; k < kPfXC; ++k)
+            lds_dma16(rx, &xs0[k][wv][0], xoff + (unsigned)min(sA + k, last) * kKStep * 2u);
+        {
+            const uint4 own = xs0[kPfXC - 1][wv][lane];  // waits for this wavefront's copies
+            asm volatile("" ::"v"(own.x));
         }
         __syncthreads();
         f32x4 ag[kPfNT], au[kPfNT];
@@ -179,34 +192,30 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
             ag[j] = f32x4{0.f, 0.f, 0.f, 0.f};
             au[j] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        for (int s0 = sA, c = 0; s0 < sB; s0 += kPfXC, ++c) {
+        auto sub = [&](const uint4 (&cur)[kPfXC][kPfNT][64], uint4 (&nxt)[kPfXC][kPfNT][64], int s0) {
             const bool more = s0 + kPfXC < sB;
-            if (stager && more) {
+            if (more) {
 #pragma unroll
                 for (int k = 0; k < kPfXC; ++k)
-                    xv[k] = ldg16(xr + min(s0 + kPfXC + k, last) * kKStep);
+                    lds_dma16(rx, &nxt[k][wv][0],
+                              xoff + (unsigned)min(s0 + kPfXC + k, last) * kKStep * 2u);
             }
-            const uint4 *xb = &xs[c & 1][0][0][0];
             // the token fragments of step k are read from LDS one step ahead
             uint4 b[kPfNT];
 #pragma unroll
-            for (int j = 0; j < kPfNT; ++j) b[j] = xb[j * 64 + lane];
+            for (int j = 0; j < kPfNT; ++j) b[j] = cur[0][j][lane];
 #pragma unroll
             for (int k = 0; k < kPfXC; ++k) {
                 uint4 bn[kPfNT];
                 if (k + 1 < kPfXC) {
 #pragma unroll
-                    for (int j = 0; j < kPfNT; ++j) bn[j] = xb[((k + 1) * kPfNT + j) * 64 + lane];
+                    for (int j = 0; j < kPfNT; ++j) bn[j] = cur[k + 1][j][lane];
                 }
                 if (s0 + k < sB) {
+                    // token tiles in pairs: the pairs past the group are skipped
 #pragma unroll
-                    for (int j = 0; j < kPfNT / 2; ++j) {
-                        ag[j] = mfma16(G[k % kPfPF], b[j], ag[j]);
-                        if (GATED) au[j] = mfma16(U[k % kPfPF], b[j], au[j]);
-                    }
-                    if (nt > kPfNT / 2) {
-#pragma unroll
-                        for (int j = kPfNT / 2; j < kPfNT; ++j) {
+                    for (int j = 0; j < kPfNT; ++j) {
+                        if (j < 2 || nt > (j & ~1)) {
                             ag[j] = mfma16(G[k % kPfPF], b[j], ag[j]);
                             if (GATED) au[j] = mfma16(U[k % kPfPF], b[j], au[j]);
                         }
@@ -218,11 +227,16 @@ __global__ __launch_bounds__(kGuThreads, 1) void gateup_pf_k(GUParams P) {
                     for (int j = 0; j < kPfNT; ++j) b[j] = bn[j];
                 }
             }
-            if (stager && more) {
-#pragma unroll
-                for (int k = 0; k < kPfXC; ++k) xs[(c + 1) & 1][k][wv][lane] = xv[k];
+            if (more) {
+                // this wavefront's copies into nxt have landed before the barrier
+                const uint4 own = nxt[kPfXC - 1][wv][lane];
+                asm volatile("" ::"v"(own.x));
             }
             __syncthreads();
+        };
+        for (int s0 = sA; s0 < sB; s0 += 2 * kPfXC) {
+            sub(xs0, xs1, s0);
+            if (s0 + kPfXC < sB) sub(xs1, xs0, s0 + kPfXC);
         }
         // lane holds neurons r0 .. r0 + 3 of token slot 16 j + lane % 16
         const int r0 = wv * 16 + 4 * (lane >> 4);
@@ -291,7 +305,7 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
                                                   int32_t *__restrict__ tokl, int stride,
                                                   int32_t *__restrict__ cut, int ncut,
                                                   int32_t *__restrict__ ebase, uint32_t *cnt,
-                                                  PlanView plan) {
+                                                  PlanView plan, int num_cu) {
     static_assert(kPfChunk % 256 == 0, "chunk starts fall on blocks of 256 tokens");
     constexpr int kBlocks = 8;  // blocks of 256 tokens whose flags are loaded at once
     __shared__ int scan[8];
@@ -333,12 +347,21 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
         st_dev_u32(reinterpret_cast<uint32_t *>(ecount + e), (uint32_t)base);
     }
     if (!arrive_last(cnt, (unsigned)E, &s_flag)) return;
-    // prefill plan: expert e's bucket becomes ceil(c_e / kPfGroupTokens) groups
-    // of nearly equal size (the first c_e % groups one token larger), so that
-    // the groups of one expert stream its weights at the same pace and meet
-    // in L2
+    // prefill plan: expert e's bucket becomes ceil(c_e / gs) groups of nearly
+    // equal size (the first c_e % groups one token larger), so that the groups
+    // of one expert stream its weights at the same pace and meet in L2.  The
+    // group size gs is the smallest of 64, 80, 96, 112 whose groups all fit in
+    // one round on the CUs (smaller groups stage fewer token rows and spread
+    // over more CUs), else kPfGroupTokens.
     const int c = (tid < E) ? (int)ld_dev_u32(reinterpret_cast<uint32_t *>(ecount + tid)) : 0;
-    const int nch = (c + kPfGroupTokens - 1) / kPfGroupTokens;
+    int gs = kPfGroupTokens;
+    {
+        int x0, x1, n64, n80, n96, n112;
+        block_excl_scan2((c + 63) / 64, (c + 79) / 80, &x0, &x1, &n64, &n80, scan);
+        block_excl_scan2((c + 95) / 96, (c + 111) / 112, &x0, &x1, &n96, &n112, scan);
+        gs = n64 <= num_cu ? 64 : n80 <= num_cu ? 80 : n96 <= num_cu ? 96 : n112 <= num_cu ? 112 : gs;
+    }
+    const int nch = (c + gs - 1) / gs;
     int cb, off, nG, npairs;
     block_excl_scan2(nch, c, &cb, &off, &nG, &npairs, scan);
     if (tid < E) {
@@ -631,7 +654,7 @@ hipError_t launch_prefill_ffn(pp_layer *L, const uint16_t *x, int T, float *y, h
     prof_mark(L, PP_KERNEL_DISPATCH, s, true);
     hipLaunchKernelGGL(dispatch_k, dim3(dm.E), dim3(256), 0, s, L->selmask, T, dm.E, L->ecount,
                        L->tokl, L->max_tokens, L->pf_cut, L->pf_ncut, L->pf_ebase,
-                       L->counters + cl.dispatch_base(), plan_view(L, true));
+                       L->counters + cl.dispatch_base(), plan_view(L, true), L->num_cu);
     prof_mark(L, PP_KERNEL_DISPATCH, s, false);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
