@@ -707,6 +707,179 @@ __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
         rows_sparse<TB, R, false>(P, S.rw, nU);
 }
 
+
+// ---- every token keeps every expert (dense decode, up to 32 tokens): group u
+// is expert u with all T tokens, its h rows u T .. u T + T - 1 in token order,
+// so the outputs of a unit accumulate in registers across its groups with no
+// per-group read-modify-write.  Unit = (128 rows of d, chunk of groups);
+// wavefront w owns row tiles 2 w and 2 w + 1 (each h fragment read from LDS
+// feeds both).  Group u + 2's h fragments (copied into one of three LDS
+// buffers by buffer loads to LDS) and weights (into a three-group register
+// ring) are issued together at the start of group u, so every wait is for
+// loads issued two groups earlier; one barrier per group.  Chunk partials are
+// summed in chunk order by the last chunk to arrive, as in the dense-group
+// mode above.
+constexpr int kDdThreads = 256;
+constexpr int kDdRows = 128;
+static_assert(kDdThreads / 64 * 2 * 16 == kDdRows, "four wavefronts of two row tiles");
+
+// Copies group u's h B fragments into hb: fragment f = (token tile f / 8,
+// piece f % 8 = hi K-steps 0..3, lo K-steps 0..3); wavefront w copies
+// fragments w, w + 4, ...  Token slots past T read zeros.
+template <int NTT>
+__device__ __forceinline__ void dd_copy_h(const DNParams &P, uint4 (&hb)[NTT][8][64], int u,
+                                          int wv, int lane) {
+    const unsigned bytes = (unsigned)P.T * kExpertWidth * 2u;
+    const size_t row0 = (size_t)u * P.T * kExpertWidth;
+    const auto rh = buf_rsrc(P.h_hi + row0, bytes);
+    const auto rl = buf_rsrc(P.h_lo + row0, bytes);
+#pragma unroll
+    for (int i = 0; i < 2 * NTT; ++i) {
+        const int f = wv + 4 * i, j = f >> 3, pc = f & 7;
+        const unsigned off =
+            ((unsigned)(16 * j + (lane & 15)) * kExpertWidth + kKStep * (pc & 3) + 8 * (lane >> 4)) * 2u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            pc < 4 ? rh : rl, (__attribute__((address_space(3))) void *)&hb[j][pc][0], 16, off, 0, 0,
+            0);
+    }
+}
+
+// The wavefront's two row tiles of group u's down weights (row tiles past d
+// load the last one and are discarded).  Every expert is kept, so group u is
+// expert u (no plan load, whose wait would drain the loads in flight).
+__device__ __forceinline__ void dd_load_w(const DNParams &P, int u, int rt0, int RT, int lane,
+                                          uint4 (&w)[2][4]) {
+    const int e = u;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        const uint16_t *wp =
+            P.Wd + (((size_t)e * RT + min(rt0 + t, RT - 1)) * 4 * 64 + lane) * 8;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) w[t][s] = ldw16(wp + s * 512);
+    }
+}
+
+// One group: wait for this wavefront's copies into cur (issued two groups
+// ago), meet the other wavefronts (they are then done with group u - 1's
+// buffer, which is nxt2), issue group u + 2's copies into nxt2 and weights
+// into wl (group u - 1's ring slot), multiply cur with wu.
+template <int NTT>
+__device__ __forceinline__ void dd_group(const DNParams &P, const uint4 (&cur)[NTT][8][64],
+                                         uint4 (&nxt2)[NTT][8][64], int u, int u1, int nt,
+                                         int rt0, int RT, int wv, int lane, const uint4 (&wu)[2][4],
+                                         uint4 (&wl)[2][4], f32x4 (&acc)[2][NTT]) {
+    {
+        // the last of this wavefront's copies into cur; they complete in order
+        const uint4 own = cur[NTT - 1][4 + wv][lane];
+        asm volatile("" ::"v"(own.x));
+    }
+    __syncthreads();
+    // issued for every group (past the chunk: its last group again, into a
+    // buffer and a ring slot no later group reads), so that the compiler's
+    // waits count the same loads on every path
+    const int un = min(u + 2, u1 - 1);
+    dd_copy_h<NTT>(P, nxt2, un, wv, lane);
+    dd_load_w(P, un, rt0, RT, lane, wl);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+#pragma unroll
+        for (int j = 0; j < NTT; ++j) {
+            if (j < nt) {
+                const uint4 bh = cur[j][s][lane], bl = cur[j][4 + s][lane];
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    acc[t][j] = mfma16(wu[t][s], bh, acc[t][j]);
+                    acc[t][j] = mfma16(wu[t][s], bl, acc[t][j]);
+                }
+            }
+        }
+    }
+}
+
+// NTT: token tiles the kernel holds (T <= 16 NTT).
+template <int NTT>
+__global__ __launch_bounds__(kDdThreads, 2) void down_dense_k(DNParams P) {
+    __shared__ uint4 hb0[NTT][8][64];
+    __shared__ uint4 hb1[NTT][8][64];
+    __shared__ uint4 hb2[NTT][8][64];
+    __shared__ int s_flag;
+    // the wavefront index in a scalar register: the copies' descriptors and LDS
+    // addresses derive from it and must be known uniform
+    const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int T = P.T, d = P.d, RT = d / 16, nt = (T + 15) >> 4;
+    const int nU = P.E;  // every expert is a group
+    const int n_rb = (d + kDdRows - 1) / kDdRows;
+    int ES = (int)gridDim.x / n_rb;
+    if (ES > nU / 3) ES = nU / 3;
+    if (ES > kDecodeChunks) ES = kDecodeChunks;
+    if (ES < 1) ES = 1;
+    const int Uc = (nU + ES - 1) / ES;
+    ES = (nU + Uc - 1) / Uc;
+    const auto pr = buf_rsrc(P.ypart, (unsigned)((size_t)kDecodeChunks * T * d * 4u));
+    for (int unit = blockIdx.x; unit < ES * n_rb; unit += gridDim.x) {
+        const int c = unit / n_rb, rb = unit - c * n_rb;
+        const int rt0 = rb * (kDdRows / 16) + 2 * wv;
+        const int u0 = c * Uc, u1 = min(nU, u0 + Uc);
+        f32x4 acc[2][NTT];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int j = 0; j < NTT; ++j) acc[t][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        uint4 w0[2][4], w1[2][4], w2[2][4];
+        dd_copy_h<NTT>(P, hb0, u0, wv, lane);
+        dd_load_w(P, u0, rt0, RT, lane, w0);
+        dd_copy_h<NTT>(P, hb1, min(u0 + 1, u1 - 1), wv, lane);
+        dd_load_w(P, min(u0 + 1, u1 - 1), rt0, RT, lane, w1);
+        for (int u = u0; u < u1; u += 3) {
+            dd_group<NTT>(P, hb0, hb2, u, u1, nt, rt0, RT, wv, lane, w0, w2, acc);
+            if (u + 1 >= u1) break;
+            dd_group<NTT>(P, hb1, hb0, u + 1, u1, nt, rt0, RT, wv, lane, w1, w0, acc);
+            if (u + 2 >= u1) break;
+            dd_group<NTT>(P, hb2, hb1, u + 2, u1, nt, rt0, RT, wv, lane, w2, w1, acc);
+        }
+        // lane holds rows 4 (lane / 16) + i of row tile rt0 + t, token slot 16 j + lane % 16
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+#pragma unroll
+            for (int j = 0; j < NTT; ++j) {
+                const int tok = 16 * j + (lane & 15);
+                if (rt0 + t < RT && tok < T) {
+                    const int col = (rt0 + t) * 16 + 4 * (lane >> 4);
+                    f32x4 v = acc[t][j];
+                    if (ES == 1) {
+                        if (P.bproj) v += *reinterpret_cast<const f32x4 *>(P.bproj + col);
+                        *reinterpret_cast<f32x4 *>(P.y + (size_t)tok * d + col) = v;
+                    } else {
+                        st_dev16(pr, (unsigned)(((size_t)c * T + tok) * d + col) * 4u, v);
+                    }
+                }
+            }
+        }
+        if (ES > 1 && arrive_last(&P.dn_cnt[rb], (unsigned)ES, &s_flag)) {
+            // last chunk to arrive: y = sum of the chunk partials in chunk
+            // order (+ the output bias), four chunks' loads at a time
+            const int nrows = min(kDdRows, d - rb * kDdRows), nq = nrows / 4;
+            for (int i = tid; i < T * nq; i += kDdThreads) {
+                const int tk = i / nq;
+                const size_t off = (size_t)tk * d + rb * kDdRows + 4 * (i - tk * nq);
+                f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int k0 = 0; k0 < ES; k0 += 4) {
+                    f32x4 v[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        v[k] = ld_dev16(pr, (unsigned)((size_t)min(k0 + k, ES - 1) * T * d + off) * 4u);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (k0 + k < ES) a += v[k];
+                }
+                if (P.bproj) a += *reinterpret_cast<const f32x4 *>(P.bproj + off % d);
+                *reinterpret_cast<f32x4 *>(P.y + off) = a;
+            }
+        }
+        __syncthreads();  // the unit's LDS buffers and flag are free again
+    }
+}
+
 // ------------------------------------------------------------------ launchers
 
 template <int TB>
@@ -772,7 +945,13 @@ hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, bo
     dp.dn_cnt = L->counters + counters_for(L->dm, L->max_tokens).down_base();
     dp.plan = plan_view(L, false);
     prof_mark(L, PP_KERNEL_DOWN, s, true);
-    if (T <= 16)
+    if (dense && T <= 16) {
+        static const int occ = resident(down_dense_k<1>, kDdThreads);
+        hipLaunchKernelGGL(down_dense_k<1>, dim3(occ * L->num_cu), dim3(kDdThreads), 0, s, dp);
+    } else if (dense && T <= 32) {
+        static const int occ = resident(down_dense_k<2>, kDdThreads);
+        hipLaunchKernelGGL(down_dense_k<2>, dim3(occ * L->num_cu), dim3(kDdThreads), 0, s, dp);
+    } else if (T <= 16)
         launch_down_dec_tb<16>(dp, L->num_cu, s);
     else if (T <= 32)
         launch_down_dec_tb<32>(dp, L->num_cu, s);
