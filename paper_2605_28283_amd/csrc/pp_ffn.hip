@@ -355,10 +355,12 @@ __global__ __launch_bounds__(256) void dispatch_k(const uint32_t *__restrict__ s
     // over more CUs), else kPfGroupTokens.
     const int c = (tid < E) ? (int)ld_dev_u32(reinterpret_cast<uint32_t *>(ecount + tid)) : 0;
     int gs = kPfGroupTokens;
-    {
-        int x0, x1, n64, n80, n96, n112;
-        block_excl_scan2((c + 63) / 64, (c + 79) / 80, &x0, &x1, &n64, &n80, scan);
-        block_excl_scan2((c + 95) / 96, (c + 111) / 112, &x0, &x1, &n96, &n112, scan);
+    if ((long)T * E / 64 + E < 65535) {
+        // the four sizes' group counts, two to an int (each sum below 2^16): one scan
+        int x0, x1, p0, p1;
+        block_excl_scan2(((c + 63) / 64) | (((c + 79) / 80) << 16),
+                         ((c + 95) / 96) | (((c + 111) / 112) << 16), &x0, &x1, &p0, &p1, scan);
+        const int n64 = p0 & 0xFFFF, n80 = p0 >> 16, n96 = p1 & 0xFFFF, n112 = p1 >> 16;
         gs = n64 <= num_cu ? 64 : n80 <= num_cu ? 80 : n96 <= num_cu ? 96 : n112 <= num_cu ? 112 : gs;
     }
     const int nch = (c + gs - 1) / gs;
