@@ -58,7 +58,7 @@ struct KmWork {
     float *list;         // [k][n] margins (rounded up to fp32) of each cluster's rows
     int32_t *memb;       // [k][n] the rows themselves (same order as list)
     double *lam;         // [k] cluster prices
-    double *part;        // [bid workgroups] spread sums (eps scale)
+    double *part;        // [bid workgroups] spread sums, then [bid workgroups] = the eps scale
     float *cn;           // [k] ||mu_j||^2
     uint16_t *mu3;       // [3][k][D] bf16 parts of mu
     int32_t *count;      // [k] rows whose argmax is j (this round)
@@ -87,7 +87,7 @@ size_t km_layout(int n, int D, int k, KmWork *w, char *base) {
     t.list = reinterpret_cast<float *>(take(sizeof(float) * (size_t)k * n));
     t.memb = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * (size_t)k * n));
     t.lam = reinterpret_cast<double *>(take(sizeof(double) * k));
-    t.part = reinterpret_cast<double *>(take(sizeof(double) * bid_blocks(n)));
+    t.part = reinterpret_cast<double *>(take(sizeof(double) * (bid_blocks(n) + 1)));
     t.cn = reinterpret_cast<float *>(take(sizeof(float) * k));
     t.mu3 = reinterpret_cast<uint16_t *>(take(sizeof(uint16_t) * 3 * (size_t)k * D));
     t.count = reinterpret_cast<int32_t *>(take(sizeof(int32_t) * k));
@@ -263,7 +263,7 @@ __device__ __forceinline__ Best2 shfl_best2(const Best2 &v, int st) {
 // index on ties) and its margin w1 - w2 (w2 the best over the other
 // clusters), rounded up to fp32 and appended, with the row, to cluster j1's
 // lists; counts per cluster.  kBidLanes adjacent lanes share a row, each
-// taking every kBidLanes-th cluster with its loads 8 at a time in flight, and
+// taking every kBidLanes-th cluster with its loads 32 at a time in flight, and
 // their partial results are merged.  Exits at once when the previous round
 // left no cluster over-full (the assignment then stands).
 constexpr int kBidLanes = 4;
@@ -272,7 +272,7 @@ constexpr int kBidRows = kKmBidThreads / kBidLanes;  // rows per workgroup
 __global__ __launch_bounds__(kKmBidThreads) void km_bid_k(const float *__restrict__ S, int n, int k,
                                                           int r, KmWork W,
                                                           int32_t *__restrict__ assign) {
-    constexpr int kBatch = 8;
+    constexpr int kBatch = 32;  // a lane's clusters in flight at once (k <= 128: all of them)
     __shared__ double lam[kKmMaxK];
     __shared__ int cnt[kKmMaxK];
     __shared__ int base[kKmMaxK];
@@ -347,16 +347,22 @@ __global__ __launch_bounds__(kKmBidThreads) void km_bid_k(const float *__restric
 // (m+1)-th largest margin in its list by a 4-pass radix select on the fp32
 // bits (margins are >= 0, so bit order is value order; the list order does
 // not matter) and raises its price by that margin plus eps_r; it also counts
-// itself in flags[r & 1].  Every workgroup clears its count for the next
-// round.
+// itself in flags[r & 1].  A list of up to kKmPriceLds margins is copied into
+// LDS once and the passes read it there.  The eps scale (the round-0 spread
+// sums, added in workgroup order) is formed in round 0 and kept in
+// part[nbid].  Every workgroup clears its count for the next round.
+constexpr int kKmPriceLds = 16384;
+
 __global__ __launch_bounds__(kKmPriceThreads) void km_price_k(int n, int k, int m, int r,
                                                               int nbid, KmWork W) {
     constexpr int kBatch = 4;
+    constexpr int kCopy = 8;
     static_assert(kKmPriceThreads == 256, "one thread per radix digit");
     __shared__ int hist[256];
     __shared__ int scan[8];
     __shared__ uint32_t s_pref;
     __shared__ int s_rank;
+    __shared__ uint32_t sl[kKmPriceLds];
     const int j = blockIdx.x, tid = threadIdx.x;
     if (W.flags[2]) return;
     const int c = W.count[j];
@@ -368,6 +374,18 @@ __global__ __launch_bounds__(kKmPriceThreads) void km_price_k(int n, int k, int 
         s_rank = m;  // 0-based rank from the top
     }
     const float *lst = W.list + (size_t)j * n;
+    const bool inl = c <= kKmPriceLds;  // workgroup-uniform
+    if (inl) {
+        for (int i0 = 0; i0 < c; i0 += kCopy * kKmPriceThreads) {
+            uint32_t v[kCopy];
+#pragma unroll
+            for (int u = 0; u < kCopy; ++u)
+                v[u] = __float_as_uint(lst[min(i0 + u * kKmPriceThreads + tid, c - 1)]);
+#pragma unroll
+            for (int u = 0; u < kCopy; ++u)
+                if (i0 + u * kKmPriceThreads + tid < c) sl[i0 + u * kKmPriceThreads + tid] = v[u];
+        }
+    }
     {
         uint32_t mask = 0u;
         for (int pass = 0; pass < 4; ++pass) {
@@ -378,8 +396,10 @@ __global__ __launch_bounds__(kKmPriceThreads) void km_price_k(int n, int k, int 
             for (int i0 = 0; i0 < c; i0 += kBatch * kKmPriceThreads) {
                 uint32_t v[kBatch];
     #pragma unroll
-                for (int u = 0; u < kBatch; ++u)
-                    v[u] = __float_as_uint(lst[min(i0 + u * kKmPriceThreads + tid, c - 1)]);
+                for (int u = 0; u < kBatch; ++u) {
+                    const int ix = min(i0 + u * kKmPriceThreads + tid, c - 1);
+                    v[u] = inl ? sl[ix] : __float_as_uint(lst[ix]);
+                }
     #pragma unroll
                 for (int u = 0; u < kBatch; ++u)
                     if (i0 + u * kKmPriceThreads + tid < c && (v[u] & mask) == pref)
@@ -403,8 +423,13 @@ __global__ __launch_bounds__(kKmPriceThreads) void km_price_k(int n, int k, int 
     }
     if (tid == 0) {
         double scale = 0.0;
-        for (int b = 0; b < nbid; ++b) scale += W.part[b];
-        scale /= (double)n;
+        if (r == 0) {  // every over-full cluster forms the same value
+            for (int b = 0; b < nbid; ++b) scale += W.part[b];
+            scale /= (double)n;
+            W.part[nbid] = scale;
+        } else {
+            scale = W.part[nbid];
+        }
         double e = 0.3 * pow(0.9, (double)r);
         if (e < 0x1p-22) e = 0x1p-22;
         W.lam[j] += (double)__uint_as_float(s_pref) + e * scale;
