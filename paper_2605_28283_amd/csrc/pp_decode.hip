@@ -857,23 +857,44 @@ __global__ __launch_bounds__(kDdThreads, 2) void down_dense_k(DNParams P) {
         }
         if (ES > 1 && arrive_last(&P.dn_cnt[rb], (unsigned)ES, &s_flag)) {
             // last chunk to arrive: y = sum of the chunk partials in chunk
-            // order (+ the output bias), four chunks' loads at a time
-            const int nrows = min(kDdRows, d - rb * kDdRows), nq = nrows / 4;
-            for (int i = tid; i < T * nq; i += kDdThreads) {
-                const int tk = i / nq;
-                const size_t off = (size_t)tk * d + rb * kDdRows + 4 * (i - tk * nq);
-                f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
-                for (int k0 = 0; k0 < ES; k0 += 4) {
-                    f32x4 v[4];
+            // order (+ the output bias).  A thread owns kRedPer 16-byte
+            // pieces of the row block; its loads of kRedChunks chunks of all
+            // of them are in flight at once (loads past the block or the
+            // chunks read in-range elements and are not added), so the sum
+            // takes ES / kRedChunks round trips instead of one per piece and
+            // chunk batch.
+            constexpr int kRedPer = 2 * NTT;                  // 16 NTT tokens x 32 pieces / 256 threads
+            constexpr int kRedChunks = kDecodeChunks / NTT;   // 32 loads in flight per thread
+            const int nrows = min(kDdRows, d - rb * kDdRows), nq = nrows / 4, nel = T * nq;
+            int off[kRedPer];
+            f32x4 a[kRedPer];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        v[k] = ld_dev16(pr, (unsigned)((size_t)min(k0 + k, ES - 1) * T * d + off) * 4u);
+            for (int q = 0; q < kRedPer; ++q) {
+                const int i = min(tid + kDdThreads * q, nel - 1), tk = i / nq;
+                off[q] = tk * d + rb * kDdRows + 4 * (i - tk * nq);
+                a[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+            for (int k0 = 0; k0 < ES; k0 += kRedChunks) {
+                f32x4 v[kRedChunks][kRedPer];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        if (k0 + k < ES) a += v[k];
+                for (int k = 0; k < kRedChunks; ++k) {
+                    const size_t base = (size_t)min(k0 + k, ES - 1) * T * d;
+#pragma unroll
+                    for (int q = 0; q < kRedPer; ++q)
+                        v[k][q] = ld_dev16(pr, (unsigned)(base + off[q]) * 4u);
                 }
-                if (P.bproj) a += *reinterpret_cast<const f32x4 *>(P.bproj + off % d);
-                *reinterpret_cast<f32x4 *>(P.y + off) = a;
+#pragma unroll
+                for (int k = 0; k < kRedChunks; ++k)
+                    if (k0 + k < ES)
+#pragma unroll
+                        for (int q = 0; q < kRedPer; ++q) a[q] += v[k][q];
+            }
+#pragma unroll
+            for (int q = 0; q < kRedPer; ++q) {
+                if (tid + kDdThreads * q < nel) {
+                    if (P.bproj) a[q] += *reinterpret_cast<const f32x4 *>(P.bproj + off[q] % d);
+                    *reinterpret_cast<f32x4 *>(P.y + off[q]) = a[q];
+                }
             }
         }
         __syncthreads();  // the unit's LDS buffers and flag are free again
