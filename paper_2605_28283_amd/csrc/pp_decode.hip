@@ -708,34 +708,37 @@ __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
 }
 
 
-// ---- every token keeps every expert (dense decode, up to 32 tokens): group u
+// ---- every token keeps every expert (dense decode, up to 64 tokens): group u
 // is expert u with all T tokens, its h rows u T .. u T + T - 1 in token order,
 // so the outputs of a unit accumulate in registers across its groups with no
-// per-group read-modify-write.  Unit = (128 rows of d, chunk of groups);
-// wavefront w owns row tiles 2 w and 2 w + 1 (each h fragment read from LDS
-// feeds both).  Group u + 2's h fragments (copied into one of three LDS
-// buffers by buffer loads to LDS) and weights (into a three-group register
-// ring) are issued together at the start of group u, so every wait is for
-// loads issued two groups earlier; one barrier per group.  Chunk partials are
-// summed in chunk order by the last chunk to arrive, as in the dense-group
-// mode above.
-constexpr int kDdThreads = 256;
-constexpr int kDdRows = 128;
-static_assert(kDdThreads / 64 * 2 * 16 == kDdRows, "four wavefronts of two row tiles");
+// per-group read-modify-write.  Unit = (32 NW rows of d, chunk of groups) on
+// NW wavefronts; wavefront w owns row tiles 2 w and 2 w + 1 (each h fragment
+// read from LDS feeds both).  Group u + 2's h fragments (copied into one of
+// three LDS buffers by buffer loads to LDS) and weights (into a three-group
+// register ring) are issued together at the start of group u, so every wait
+// is for loads issued two groups earlier; one barrier per group.  Chunk
+// partials are summed in chunk order by the last chunk to arrive, as in the
+// dense-group mode above.  Up to 32 tokens: four wavefronts (128 rows), two
+// workgroups per CU; 64 tokens (three 32 KiB h buffers): eight wavefronts
+// (256 rows), one workgroup per CU.
+template <int NTT>
+constexpr int dd_waves() { return NTT <= 2 ? 4 : 8; }
 
 // Copies group u's h B fragments into hb: fragment f = (token tile f / 8,
-// piece f % 8 = hi K-steps 0..3, lo K-steps 0..3); wavefront w copies
-// fragments w, w + 4, ...  Token slots past T read zeros.
+// piece f % 8 = hi K-steps 0..3, lo K-steps 0..3); wavefront w of NW copies
+// fragments w, w + NW, ...  Token slots past T read zeros.
 template <int NTT>
 __device__ __forceinline__ void dd_copy_h(const DNParams &P, uint4 (&hb)[NTT][8][64], int u,
                                           int wv, int lane) {
+    constexpr int NW = dd_waves<NTT>();
+    static_assert((8 * NTT) % NW == 0, "whole fragments per wavefront");
     const unsigned bytes = (unsigned)P.T * kExpertWidth * 2u;
     const size_t row0 = (size_t)u * P.T * kExpertWidth;
     const auto rh = buf_rsrc(P.h_hi + row0, bytes);
     const auto rl = buf_rsrc(P.h_lo + row0, bytes);
 #pragma unroll
-    for (int i = 0; i < 2 * NTT; ++i) {
-        const int f = wv + 4 * i, j = f >> 3, pc = f & 7;
+    for (int i = 0; i < 8 * NTT / NW; ++i) {
+        const int f = wv + NW * i, j = f >> 3, pc = f & 7;
         const unsigned off =
             ((unsigned)(16 * j + (lane & 15)) * kExpertWidth + kKStep * (pc & 3) + 8 * (lane >> 4)) * 2u;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -769,8 +772,11 @@ __device__ __forceinline__ void dd_group(const DNParams &P, const uint4 (&cur)[N
                                          int rt0, int RT, int wv, int lane, const uint4 (&wu)[2][4],
                                          uint4 (&wl)[2][4], f32x4 (&acc)[2][NTT]) {
     {
-        // the last of this wavefront's copies into cur; they complete in order
-        const uint4 own = cur[NTT - 1][4 + wv][lane];
+        // the last of this wavefront's copies into cur (fragment 8 NTT - NW + wv);
+        // they complete in order
+        constexpr int NW = dd_waves<NTT>();
+        const int f = 8 * NTT - NW + wv;
+        const uint4 own = cur[f >> 3][f & 7][lane];
         asm volatile("" ::"v"(own.x));
     }
     __syncthreads();
@@ -798,7 +804,9 @@ __device__ __forceinline__ void dd_group(const DNParams &P, const uint4 (&cur)[N
 
 // NTT: token tiles the kernel holds (T <= 16 NTT).
 template <int NTT>
-__global__ __launch_bounds__(kDdThreads, 2) void down_dense_k(DNParams P) {
+__global__ __launch_bounds__(64 * dd_waves<NTT>(), 8 / dd_waves<NTT>()) void down_dense_k(DNParams P) {
+    constexpr int kDdThreads = 64 * dd_waves<NTT>();
+    constexpr int kDdRows = 32 * dd_waves<NTT>();
     __shared__ uint4 hb0[NTT][8][64];
     __shared__ uint4 hb1[NTT][8][64];
     __shared__ uint4 hb2[NTT][8][64];
@@ -863,7 +871,7 @@ __global__ __launch_bounds__(kDdThreads, 2) void down_dense_k(DNParams P) {
             // chunks read in-range elements and are not added), so the sum
             // takes ES / kRedChunks round trips instead of one per piece and
             // chunk batch.
-            constexpr int kRedPer = 2 * NTT;                  // 16 NTT tokens x 32 pieces / 256 threads
+            constexpr int kRedPer = 2 * NTT;                  // 16 NTT tokens x 8 NW pieces / 64 NW threads
             constexpr int kRedChunks = kDecodeChunks / NTT;   // 32 loads in flight per thread
             const int nrows = min(kDdRows, d - rb * kDdRows), nq = nrows / 4, nel = T * nq;
             int off[kRedPer];
@@ -967,11 +975,14 @@ hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, bo
     dp.plan = plan_view(L, false);
     prof_mark(L, PP_KERNEL_DOWN, s, true);
     if (dense && T <= 16) {
-        static const int occ = resident(down_dense_k<1>, kDdThreads);
-        hipLaunchKernelGGL(down_dense_k<1>, dim3(occ * L->num_cu), dim3(kDdThreads), 0, s, dp);
+        static const int occ = resident(down_dense_k<1>, 64 * dd_waves<1>());
+        hipLaunchKernelGGL(down_dense_k<1>, dim3(occ * L->num_cu), dim3(64 * dd_waves<1>()), 0, s, dp);
     } else if (dense && T <= 32) {
-        static const int occ = resident(down_dense_k<2>, kDdThreads);
-        hipLaunchKernelGGL(down_dense_k<2>, dim3(occ * L->num_cu), dim3(kDdThreads), 0, s, dp);
+        static const int occ = resident(down_dense_k<2>, 64 * dd_waves<2>());
+        hipLaunchKernelGGL(down_dense_k<2>, dim3(occ * L->num_cu), dim3(64 * dd_waves<2>()), 0, s, dp);
+    } else if (dense) {
+        static const int occ = resident(down_dense_k<4>, 64 * dd_waves<4>());
+        hipLaunchKernelGGL(down_dense_k<4>, dim3(occ * L->num_cu), dim3(64 * dd_waves<4>()), 0, s, dp);
     } else if (T <= 16)
         launch_down_dec_tb<16>(dp, L->num_cu, s);
     else if (T <= 32)

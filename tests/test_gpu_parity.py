@@ -141,9 +141,10 @@ def test_comparison_rules_llama8b_decode(oracle_mod, llama8b):
 
 
 def test_decode_down_modes_ragged_rows(oracle_mod):
-    """d = 576 is not a multiple of 128: the decode down projection's last
-    128-row block has 64 rows.  tau = 0.3 gives sparse groups (row-tile
-    path), tau = 1 dense groups (shared-h path, several expert chunks)."""
+    """d = 576 is not a multiple of 128 or 256: the decode down projection's
+    last row block has 64 rows.  tau = 0.3 gives sparse groups (row-tile
+    path), tau = 1 keeps every expert (the dense kernel: 128-row units at
+    T = 24, 256-row units at T = 64, several expert chunks)."""
     L = make_layer(576, 40 * 128, 40, 31)
     for T in (24, 64):
         x, _ = make_tokens(T, 576, 32 + T)
