@@ -12,8 +12,9 @@
 //                 fill the resident workgroups exactly, one round.  Sparse
 //                 batches (groups of up to 32 tokens) with one to one and a
 //                 half 16-neuron tiles per workgroup use neuron-tile units:
-//                 one tile over all of K per half workgroup, its K quarters
-//                 summed in LDS, so no partial sums pass between workgroups.
+//                 one tile over all of K per two wavefronts (a K half each),
+//                 the halves summed in LDS, so no partial sums pass between
+//                 workgroups.
 //   down_dec_k  : sparse groups (<= 8 tokens per group on average): unit = one
 //                 16-row tile of d over all groups; each of the 8 wavefronts
 //                 takes every eighth group, tile by tile of 16 tokens (three
@@ -52,20 +53,22 @@ struct DNParams {
 // ------------------------------------------------------------------ gate/up
 
 // Neuron-tile units (sparse groups): unit = one 16-neuron tile of one group's
-// expert over all of K, taken by PARTS wavefronts of the workgroup --
-// four (half a workgroup) when the union fills the chip, all eight for a
-// small union; wavefront q of the unit takes K part q, its token B
-// fragments straight from x (a few tokens, cache resident), the weights PF
-// steps ahead in two register buffers.  The parts' (a, b) are added in LDS
-// in part order and the unit writes h for its 16 neurons: no partial sums
-// leave the workgroup, so no hand-off between workgroups.
-constexpr int kTileHalves = 2;      // units per workgroup at a time (four-part units)
-constexpr int kTileQuarters = 4;    // wavefronts per unit (K parts) when the union fills the chip
+// expert over all of K, taken by PARTS wavefronts of the workgroup -- two
+// when the union fills the chip (each wavefront then streams half of the
+// tile's K: long streams keep more of HBM busy than more, shorter ones), all
+// eight for a small union (a latency-bound unit is done sooner in eight
+// parts); wavefront q of the unit takes K part q, its token B fragments
+// straight from x (a few tokens, cache resident), the weights PF steps ahead
+// in two register buffers.  The parts' (a, b) are added in LDS in part order
+// and the unit writes h for its 16 neurons: no partial sums leave the
+// workgroup, so no hand-off between workgroups.
+constexpr int kTileSlots = 4;       // units per workgroup at a time (two-part units)
+constexpr int kTileParts = 2;       // wavefronts per unit (K parts) when the union fills the chip
 constexpr int kTilePF = 2;          // K-steps per register buffer (two buffers)
 constexpr int kTileMaxNT = 2;       // token tiles per unit (batches of up to 32 tokens)
-static_assert(kTileHalves * kTileQuarters * 64 == kGuThreads, "two halves of four wavefronts");
-static_assert(kTileHalves * kTileMaxNT * 2 * kTileQuarters * 64 * 16 <= kXBufBytes,
-              "the quarters' (a, b) of both halves fit in the token staging buffer");
+static_assert(kTileSlots * kTileParts * 64 == kGuThreads, "four slots of two wavefronts");
+static_assert(kTileSlots * kTileMaxNT * 2 * kTileParts * 64 * 16 <= kXBufBytes,
+              "the parts' (a, b) of all slots fit in the token staging buffer");
 
 template <int NT, bool GATED, int PF, bool STREAM>
 __device__ __forceinline__ void tile_load(const uint16_t *wb, const uint16_t *const (&xr)[NT],
@@ -200,25 +203,25 @@ __device__ __forceinline__ int nth_set_bit(unsigned long long w, int n) {
 // kept experts before it) is a wavefront sum of mask popcounts at the end,
 // and workgroup 0 stores the batch plan for the down projection after its
 // units.  A unit takes PARTS wavefronts (K parts), so a workgroup holds
-// 8 / PARTS units at a time: part h of workgroup b takes units b + h * grid,
+// 8 / PARTS units at a time: slot h of workgroup b takes units b + h * grid,
 // then the next (8 / PARTS) * grid, ... (every workgroup one unit before any
-// takes two); barriers stay outside the per-unit work, so every part meets
-// them whether or not it holds a unit.  A unit of a group with more than 16
+// takes two); barriers stay outside the per-unit work, so every wavefront
+// meets them whether or not it holds a unit.  A unit of a group with more than 16
 // tokens takes two token tiles (and one K-step per register buffer, which
 // keeps the kernel within its registers).
 template <bool GATED, int PARTS, bool STREAM>
 __device__ void tile_units_bits(const GUParams &P, DecodePlan &D, unsigned long long m_own,
                                 const unsigned long long *s_mask,
                                 const unsigned long long *kept, int nG, int *tokh, float4 *red) {
-    constexpr int HALVES = (kGuThreads / 64) / PARTS;  // units per workgroup at a time
-    static_assert(HALVES * PARTS == kGuThreads / 64 && HALVES <= kTileHalves, "whole wavefronts");
+    constexpr int SLOTS = (kGuThreads / 64) / PARTS;  // units per workgroup at a time
+    static_assert(SLOTS * PARTS == kGuThreads / 64 && SLOTS <= kTileSlots, "whole wavefronts");
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int half = wv / PARTS, q = wv % PARTS;
+    const int slot = wv / PARTS, q = wv % PARTS;
     const int units = nG * 8, grid = (int)gridDim.x;
-    int *tok = tokh + half * kGroupTokens;
-    float4 *rh = red + half * (kTileMaxNT * 2 * PARTS * 64);
-    for (int base = 0; base < units; base += HALVES * grid) {
-        const int u = base + half * grid + (int)blockIdx.x;
+    int *tok = tokh + slot * kGroupTokens;
+    float4 *rh = red + slot * (kTileMaxNT * 2 * PARTS * 64);
+    for (int base = 0; base < units; base += SLOTS * grid) {
+        const int u = base + slot * grid + (int)blockIdx.x;
         const bool act = u < units;
         int g = act ? u >> 3 : 0, wi = 0;
         while (wi < kMaxExperts / 64 - 1 && g >= __popcll(kept[wi])) g -= __popcll(kept[wi++]);
@@ -256,7 +259,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         SelLds<1> sel;  // the single-token selection, before any token is staged
     } U;
     uint4 *const xf = U.xf;
-    __shared__ int stok[kTileHalves * kGroupTokens];
+    __shared__ int stok[kTileSlots * kGroupTokens];
     __shared__ int s_flag;
     __shared__ DecodePlan D;
     __shared__ unsigned long long s_mask[kMaxExperts];
@@ -301,7 +304,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         const int nG = packed & 1023, npairs = packed >> 10;
         const int tiles = nG * 8;
         if (!over32 && tiles >= grid && 2 * tiles <= 3 * grid && npairs <= 4 * nG) {
-            tile_units_bits<GATED, kTileQuarters, true>(P, D, m_own, s_mask, s_kept, nG, stok,
+            tile_units_bits<GATED, kTileParts, true>(P, D, m_own, s_mask, s_kept, nG, stok,
                                                         reinterpret_cast<float4 *>(xf));
             return;
         }
