@@ -10,8 +10,8 @@
 //                 projection, bias and GELU; code shared with prefill); the
 //                 K-split (one slice more for some groups) makes the units
 //                 fill the resident workgroups exactly, one round.  Sparse
-//                 batches (groups of up to 32 tokens) with one to one and a
-//                 half 16-neuron tiles per workgroup use neuron-tile units:
+//                 batches (groups of up to 32 tokens) with at least one
+//                 16-neuron tile per workgroup use neuron-tile units:
 //                 one tile over all of K per two wavefronts (a K half each),
 //                 the halves summed in LDS, so no partial sums pass between
 //                 workgroups.
@@ -291,11 +291,13 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         if (tid < kMaxExperts && (tid & 63) == 0) s_kept[tid >> 6] = kb;
     }
     const int grid = (int)gridDim.x;
-    // Sparse groups (at most 4 tokens per group on average) and between one
-    // and one and a half neuron tiles per workgroup: neuron-tile units, no K
-    // split (with more tiles, workgroups holding two units form a tail).
-    // At most two token tiles per group (groups of up to 32 tokens), read from
-    // x directly.
+    // Sparse groups (at most 4 tokens per group on average) and at least one
+    // neuron tile per workgroup: neuron-tile units, no K split, every unit of
+    // the call in flight at once (up to kTileSlots per workgroup).  At most
+    // two token tiles per group (groups of up to 32 tokens), read from x
+    // directly.  (With fewer tiles than workgroups, the units' long streams
+    // would leave most of the chip idle: small unions take eight-part units
+    // below, larger ones the K split.)
     {
         // kept experts and pairs in one block sum: (pairs << 10) + experts,
         // and whether a group spans more than two token tiles
@@ -303,7 +305,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         const int packed = block_sum((m_own != 0ull ? 1 : 0) + (__popcll(m_own) << 10), s_sum);
         const int nG = packed & 1023, npairs = packed >> 10;
         const int tiles = nG * 8;
-        if (!over32 && tiles >= grid && 2 * tiles <= 3 * grid && npairs <= 4 * nG) {
+        if (!over32 && tiles >= grid && tiles <= kTileSlots * grid && npairs <= 4 * nG) {
             tile_units_bits<GATED, kTileParts, true>(P, D, m_own, s_mask, s_kept, nG, stok,
                                                         reinterpret_cast<float4 *>(xf));
             return;
