@@ -9,9 +9,9 @@
 //                 SiLU product of one group (or the non-gated layer's input
 //                 projection, bias and GELU; code shared with prefill); the
 //                 K-split (one slice more for some groups) makes the units
-//                 fill the resident workgroups exactly, one round.  Sparse
-//                 batches (groups of up to 32 tokens) with at least one
-//                 16-neuron tile per workgroup use neuron-tile units:
+//                 fill the resident workgroups exactly, one round.  Batches
+//                 whose groups hold at most 32 tokens, with at least one
+//                 16-neuron tile per workgroup, use neuron-tile units:
 //                 one tile over all of K per two wavefronts (a K half each),
 //                 the halves summed in LDS, so no partial sums pass between
 //                 workgroups.
@@ -291,13 +291,12 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         if (tid < kMaxExperts && (tid & 63) == 0) s_kept[tid >> 6] = kb;
     }
     const int grid = (int)gridDim.x;
-    // Sparse groups (at most 4 tokens per group on average) and at least one
-    // neuron tile per workgroup: neuron-tile units, no K split, every unit of
-    // the call in flight at once (up to kTileSlots per workgroup).  At most
-    // two token tiles per group (groups of up to 32 tokens), read from x
-    // directly.  (With fewer tiles than workgroups, the units' long streams
-    // would leave most of the chip idle: small unions take eight-part units
-    // below, larger ones the K split.)
+    // Groups of up to 32 tokens (at most two token tiles, read from x
+    // directly) and at least one neuron tile per workgroup: neuron-tile
+    // units, no K split, every unit of the call in flight at once (up to
+    // kTileSlots per workgroup).  (With fewer tiles than workgroups, the
+    // units' long streams would leave most of the chip idle: small unions
+    // take eight-part units below, larger ones the K split.)
     {
         // kept experts and pairs in one block sum: (pairs << 10) + experts,
         // and whether a group spans more than two token tiles
@@ -305,7 +304,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         const int packed = block_sum((m_own != 0ull ? 1 : 0) + (__popcll(m_own) << 10), s_sum);
         const int nG = packed & 1023, npairs = packed >> 10;
         const int tiles = nG * 8;
-        if (!over32 && tiles >= grid && tiles <= kTileSlots * grid && npairs <= 4 * nG) {
+        if (!over32 && tiles >= grid && tiles <= kTileSlots * grid) {
             tile_units_bits<GATED, kTileParts, true>(P, D, m_own, s_mask, s_kept, nG, stok,
                                                         reinterpret_cast<float4 *>(xf));
             return;
