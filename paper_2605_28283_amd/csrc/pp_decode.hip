@@ -208,27 +208,41 @@ __device__ __forceinline__ int nth_set_bit(unsigned long long w, int n) {
 // takes two); barriers stay outside the per-unit work, so every wavefront
 // meets them whether or not it holds a unit.  A unit of a group with more than 16
 // tokens takes two token tiles (and one K-step per register buffer, which
-// keeps the kernel within its registers).
+// keeps the kernel within its registers).  Units 8 nG .. 8 (nG + nBig) - 1
+// take the tokens past the first 32 of the nBig experts kept by more than 32
+// tokens (bitmask words `big`): u - 8 nG is tile (u - 8 nG) % 8 of the
+// ((u - 8 nG) / 8)-th of them, so no unit holds more than 32 tokens.
 template <bool GATED, int PARTS, bool STREAM>
 __device__ void tile_units_bits(const GUParams &P, DecodePlan &D, unsigned long long m_own,
                                 const unsigned long long *s_mask,
-                                const unsigned long long *kept, int nG, int *tokh, float4 *red) {
+                                const unsigned long long *kept, int nG, int *tokh, float4 *red,
+                                const unsigned long long *big, int nBig) {
     constexpr int SLOTS = (kGuThreads / 64) / PARTS;  // units per workgroup at a time
     static_assert(SLOTS * PARTS == kGuThreads / 64 && SLOTS <= kTileSlots, "whole wavefronts");
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int slot = wv / PARTS, q = wv % PARTS;
-    const int units = nG * 8, grid = (int)gridDim.x;
+    const int units = (nG + nBig) * 8, grid = (int)gridDim.x;
     int *tok = tokh + slot * kGroupTokens;
     float4 *rh = red + slot * (kTileMaxNT * 2 * PARTS * 64);
     for (int base = 0; base < units; base += SLOTS * grid) {
         const int u = base + slot * grid + (int)blockIdx.x;
         const bool act = u < units;
-        int g = act ? u >> 3 : 0, wi = 0;
-        while (wi < kMaxExperts / 64 - 1 && g >= __popcll(kept[wi])) g -= __popcll(kept[wi++]);
-        const int e = act ? 64 * wi + nth_set_bit(kept[wi], g) : 0, nt = u & 7;
-        const unsigned long long m = s_mask[e];
-        const int n = __popcll(m);
-        if (act && q == 0 && ((m >> lane) & 1ull)) tok[__popcll(m & ((1ull << lane) - 1ull))] = lane;
+        // units past 8 nG: the tokens past the first 32 of the experts kept by
+        // more than 32 tokens (words `big`), in expert order
+        const bool second = u >= nG * 8;
+        const unsigned long long *words = second ? big : kept;
+        int g = act ? (second ? u - nG * 8 : u) >> 3 : 0, wi = 0;
+        while (wi < kMaxExperts / 64 - 1 && g >= __popcll(words[wi])) g -= __popcll(words[wi++]);
+        const int e = act ? 64 * wi + nth_set_bit(words[wi], g) : 0, nt = u & 7;
+        const unsigned long long mall = s_mask[e];
+        // the unit's tokens: the first 32 of the expert's (all, for 32 or
+        // fewer), or those past them
+        const int nall = __popcll(mall), t0 = second ? 32 : 0;
+        const int n = second ? nall - 32 : min(nall, 32);
+        if (act && q == 0 && ((mall >> lane) & 1ull)) {
+            const int r = __popcll(mall & ((1ull << lane) - 1ull)) - t0;
+            if (r >= 0 && r < 32) tok[r] = lane;
+        }
         __syncthreads();
         if (act) {
             if (n <= 16)
@@ -240,7 +254,7 @@ __device__ void tile_units_bits(const GUParams &P, DecodePlan &D, unsigned long 
         if (act && q < ((n + 15) >> 4)) {
             int c = 0;
             for (int e2 = lane; e2 < e; e2 += 64) c += __popcll(s_mask[e2]);
-            const int p0 = __builtin_amdgcn_readlane(wave_scan_i32(c), 63);
+            const int p0 = __builtin_amdgcn_readlane(wave_scan_i32(c), 63) + t0;
             if (n <= 16)
                 tile_epilogue<1, GATED, PARTS>(P, e, nt, n, p0, tok, q, lane, rh);
             else
@@ -264,6 +278,7 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     __shared__ DecodePlan D;
     __shared__ unsigned long long s_mask[kMaxExperts];
     __shared__ unsigned long long s_kept[kMaxExperts / 64];
+    __shared__ unsigned long long s_big[kMaxExperts / 64];
     __shared__ __align__(16) int s_sum[kGuThreads / 64];
     __shared__ float s_gsig[kMaxExperts];
     const int tid = threadIdx.x;
@@ -288,25 +303,33 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     if (tid < kMaxExperts) s_mask[tid] = m_own;
     {
         const unsigned long long kb = __ballot(m_own != 0ull);
-        if (tid < kMaxExperts && (tid & 63) == 0) s_kept[tid >> 6] = kb;
+        const unsigned long long bb = __ballot(__popcll(m_own) > 32);
+        if (tid < kMaxExperts && (tid & 63) == 0) {
+            s_kept[tid >> 6] = kb;
+            s_big[tid >> 6] = bb;
+        }
     }
     const int grid = (int)gridDim.x;
-    // Groups of up to 32 tokens (at most two token tiles, read from x
-    // directly) and at least one neuron tile per workgroup: neuron-tile
-    // units, no K split, every unit of the call in flight at once (up to
-    // kTileSlots per workgroup).  (With fewer tiles than workgroups, the
+    // At least one neuron tile per workgroup: neuron-tile units, no K split,
+    // every unit of the call in flight at once (up to kTileSlots per
+    // workgroup).  A unit takes at most 32 tokens (two token tiles, read from
+    // x directly): an expert kept by more has a second set of tile units for
+    // its tokens past the first 32.  (With fewer tiles than workgroups, the
     // units' long streams would leave most of the chip idle: small unions
     // take eight-part units below, larger ones the K split.)
     {
         // kept experts and pairs in one block sum: (pairs << 10) + experts,
-        // and whether a group spans more than two token tiles
+        // whether a group spans more than two token tiles, and how many do
         const int over32 = NTMAX > 2 ? __syncthreads_or(__popcll(m_own) > 32) : 0;
         const int packed = block_sum((m_own != 0ull ? 1 : 0) + (__popcll(m_own) << 10), s_sum);
         const int nG = packed & 1023, npairs = packed >> 10;
-        const int tiles = nG * 8;
-        if (!over32 && tiles >= grid && tiles <= kTileSlots * grid) {
+        int nBig = 0;
+#pragma unroll
+        for (int i = 0; i < kMaxExperts / 64; ++i) nBig += __popcll(s_big[i]);
+        const int tiles = (nG + nBig) * 8;
+        if (tiles >= grid && tiles <= kTileSlots * grid) {
             tile_units_bits<GATED, kTileParts, true>(P, D, m_own, s_mask, s_kept, nG, stok,
-                                                        reinterpret_cast<float4 *>(xf));
+                                                     reinterpret_cast<float4 *>(xf), s_big, nBig);
             return;
         }
         // A small union (at most kSmallUnion kept experts, at most one tile
@@ -317,10 +340,10 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
             float4 *red = reinterpret_cast<float4 *>(xf);
             if (GATED && nG >= kStreamGroups)
                 tile_units_bits<GATED, kGuThreads / 64, true>(P, D, m_own, s_mask, s_kept, nG,
-                                                              stok, red);
+                                                              stok, red, s_big, 0);
             else
                 tile_units_bits<GATED, kGuThreads / 64, false>(P, D, m_own, s_mask, s_kept, nG,
-                                                               stok, red);
+                                                               stok, red, s_big, 0);
             return;
         }
     }
