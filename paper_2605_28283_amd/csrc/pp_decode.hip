@@ -315,8 +315,8 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
     // workgroup).  A unit takes at most 32 tokens (two token tiles, read from
     // x directly): an expert kept by more has a second set of tile units for
     // its tokens past the first 32.  (With fewer tiles than workgroups, the
-    // units' long streams would leave most of the chip idle: small unions
-    // take eight-part units below, larger ones the K split.)
+    // units' long streams would leave most of the chip idle: such calls take
+    // four-part units, and small unions eight-part units, below.)
     {
         // kept experts and pairs in one block sum: (pairs << 10) + experts,
         // whether a group spans more than two token tiles, and how many do
@@ -330,6 +330,14 @@ __global__ __launch_bounds__(kGuThreads, 4) void gateup_dec_k(GUParams P) {
         if (tiles >= grid && tiles <= kTileSlots * grid) {
             tile_units_bits<GATED, kTileParts, true>(P, D, m_own, s_mask, s_kept, nG, stok,
                                                      reinterpret_cast<float4 *>(xf), s_big, nBig);
+            return;
+        }
+        // Between half a tile and one tile per workgroup, past the small
+        // unions: the same units in four parts (each wavefront a K quarter),
+        // which keeps twice the wavefronts streaming
+        if (nG > kSmallUnion && 2 * tiles >= grid && tiles < grid) {
+            tile_units_bits<GATED, 2 * kTileParts, true>(P, D, m_own, s_mask, s_kept, nG, stok,
+                                                         reinterpret_cast<float4 *>(xf), s_big, nBig);
             return;
         }
         // A small union (at most kSmallUnion kept experts, at most one tile
