@@ -987,7 +987,11 @@ hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, bo
                              false);
     }
     prof_mark(L, PP_KERNEL_GATEUP, s, true);
-    if (dense)
+    // dense batches of more than 24 tokens: the grouped kernel, which stages
+    // the tokens in LDS once per group; up to 24 tokens the neuron-tile units
+    // (tokens read from x per unit) stream faster (T = 16 / 24, tau 1: 49.6 /
+    // 51.3 -> 42.9 / 47.6 us; at 32 tokens 51.5 -> 57.4 us)
+    if (dense && T > 24)
         launch_gateup_dense_dec(L, x, T, s);
     else if (L->gated)
         launch_gateup_dec_t<true>(gp, T, L->num_cu, s);
