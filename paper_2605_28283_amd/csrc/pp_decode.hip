@@ -5,16 +5,17 @@
 // every gate/up workgroup derives it from the router's per-expert token masks
 // and workgroup 0 stores it for the down projection.
 //
-//   gateup_dec_k: unit = (group, K-slice), the gate/up projections and the
-//                 SiLU product of one group (or the non-gated layer's input
-//                 projection, bias and GELU; code shared with prefill); the
-//                 K-split (one slice more for some groups) makes the units
-//                 fill the resident workgroups exactly, one round.  Batches
-//                 whose groups hold at most 32 tokens, with at least one
-//                 16-neuron tile per workgroup, use neuron-tile units:
-//                 one tile over all of K per two wavefronts (a K half each),
-//                 the halves summed in LDS, so no partial sums pass between
-//                 workgroups.
+//   gateup_dec_k: the gate/up projections and the SiLU product of every
+//                 group (or the non-gated layer's input projection, bias and
+//                 GELU).  Neuron-tile units: unit = one 16-neuron tile of one
+//                 kept expert over all of K (at most 32 of its tokens), its K
+//                 in 2, 4 or 8 parts on as many wavefronts (more parts the
+//                 fewer tiles the call has), the parts summed in LDS, so no
+//                 partial sums pass between workgroups.  Small unions with
+//                 many tokens per group: unit = (group, K-slice) with the
+//                 tokens staged in LDS (code shared with prefill); the K-split
+//                 (one slice more for some groups) makes the units fill the
+//                 resident workgroups exactly, one round.
 //   down_dec_k  : sparse groups (<= 8 tokens per group on average): unit = one
 //                 16-row tile of d over all groups; each of the 8 wavefronts
 //                 takes every eighth group, tile by tile of 16 tokens (three
