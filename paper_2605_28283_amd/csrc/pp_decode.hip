@@ -752,13 +752,26 @@ __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
 // read from LDS feeds both).  Group u + 2's h fragments (copied into one of
 // three LDS buffers by buffer loads to LDS) and weights (into a three-group
 // register ring) are issued together at the start of group u, so every wait
-// is for loads issued two groups earlier; one barrier per group.  Chunk
-// partials are summed in chunk order by the last chunk to arrive, as in the
-// dense-group mode above.  Up to 32 tokens: four wavefronts (128 rows), two
+// is for loads issued two groups earlier; one barrier per group.  The
+// chunks store their partials and a second launch (dense_sum_k) sums them in
+// chunk order on every CU.  Up to 32 tokens: four wavefronts (128 rows), two
 // workgroups per CU; 64 tokens (three 32 KiB h buffers): eight wavefronts
 // (256 rows), one workgroup per CU.
 template <int NTT>
 constexpr int dd_waves() { return NTT <= 2 ? 4 : 8; }
+
+// Expert chunks of the dense kernel on `grid` workgroups over n_rb row
+// blocks of nU groups: as many as fill the workgroups, at most nU / 3 (three
+// groups per chunk) and kDecodeChunks; Uc groups per chunk.  The kernel and
+// the host (which sizes the chunk sum) take it from here.
+__host__ __device__ inline int dd_chunks(int grid, int nU, int n_rb, int *Uc) {
+    int ES = grid / n_rb;
+    if (ES > nU / 3) ES = nU / 3;
+    if (ES > kDecodeChunks) ES = kDecodeChunks;
+    if (ES < 1) ES = 1;
+    *Uc = (nU + ES - 1) / ES;
+    return (nU + *Uc - 1) / *Uc;
+}
 
 // Copies group u's h B fragments into hb: fragment f = (token tile f / 8,
 // piece f % 8 = hi K-steps 0..3, lo K-steps 0..3); wavefront w of NW copies
@@ -846,19 +859,14 @@ __global__ __launch_bounds__(64 * dd_waves<NTT>(), 8 / dd_waves<NTT>()) void dow
     __shared__ uint4 hb0[NTT][8][64];
     __shared__ uint4 hb1[NTT][8][64];
     __shared__ uint4 hb2[NTT][8][64];
-    __shared__ int s_flag;
     // the wavefront index in a scalar register: the copies' descriptors and LDS
     // addresses derive from it and must be known uniform
     const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int T = P.T, d = P.d, RT = d / 16, nt = (T + 15) >> 4;
     const int nU = P.E;  // every expert is a group
     const int n_rb = (d + kDdRows - 1) / kDdRows;
-    int ES = (int)gridDim.x / n_rb;
-    if (ES > nU / 3) ES = nU / 3;
-    if (ES > kDecodeChunks) ES = kDecodeChunks;
-    if (ES < 1) ES = 1;
-    const int Uc = (nU + ES - 1) / ES;
-    ES = (nU + Uc - 1) / Uc;
+    int Uc;
+    const int ES = dd_chunks((int)gridDim.x, nU, n_rb, &Uc);
     const auto pr = buf_rsrc(P.ypart, (unsigned)((size_t)kDecodeChunks * T * d * 4u));
     for (int unit = blockIdx.x; unit < ES * n_rb; unit += gridDim.x) {
         const int c = unit / n_rb, rb = unit - c * n_rb;
@@ -899,49 +907,43 @@ __global__ __launch_bounds__(64 * dd_waves<NTT>(), 8 / dd_waves<NTT>()) void dow
                 }
             }
         }
-        if (ES > 1 && arrive_last(&P.dn_cnt[rb], (unsigned)ES, &s_flag)) {
-            // last chunk to arrive: y = sum of the chunk partials in chunk
-            // order (+ the output bias).  A thread owns kRedPer 16-byte
-            // pieces of the row block; its loads of kRedChunks chunks of all
-            // of them are in flight at once (loads past the block or the
-            // chunks read in-range elements and are not added), so the sum
-            // takes ES / kRedChunks round trips instead of one per piece and
-            // chunk batch.
-            constexpr int kRedPer = 2 * NTT;                  // 16 NTT tokens x 8 NW pieces / 64 NW threads
-            constexpr int kRedChunks = kDecodeChunks / NTT;   // 32 loads in flight per thread
-            const int nrows = min(kDdRows, d - rb * kDdRows), nq = nrows / 4, nel = T * nq;
-            int off[kRedPer];
-            f32x4 a[kRedPer];
+        __syncthreads();  // the unit's LDS buffers are free again
+    }
+}
+
+// y of a dense batch split into ES expert chunks: y = sum of the chunk
+// partials in chunk order (+ the output bias), one 16-byte piece per thread,
+// all of its ES loads in flight at once.  A launch of its own after the
+// chunks: every CU sums, where the last chunk to arrive of a row block
+// summed its whole block alone (the kernel's tail).
+__global__ __launch_bounds__(256) void dense_sum_k(DNParams P, int ES) {
+    const int n4 = P.T * (P.d / 4);
+    const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (i >= n4) return;
+    const size_t off = (size_t)i * 4, slab = (size_t)P.T * P.d;
+    f32x4 v[kDecodeChunks];
 #pragma unroll
-            for (int q = 0; q < kRedPer; ++q) {
-                const int i = min(tid + kDdThreads * q, nel - 1), tk = i / nq;
-                off[q] = tk * d + rb * kDdRows + 4 * (i - tk * nq);
-                a[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-            }
-            for (int k0 = 0; k0 < ES; k0 += kRedChunks) {
-                f32x4 v[kRedChunks][kRedPer];
+    for (int k = 0; k < kDecodeChunks; ++k)
+        v[k] = *reinterpret_cast<const f32x4 *>(P.ypart + (size_t)min(k, ES - 1) * slab + off);
+    f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int k = 0; k < kRedChunks; ++k) {
-                    const size_t base = (size_t)min(k0 + k, ES - 1) * T * d;
-#pragma unroll
-                    for (int q = 0; q < kRedPer; ++q)
-                        v[k][q] = ld_dev16(pr, (unsigned)(base + off[q]) * 4u);
-                }
-#pragma unroll
-                for (int k = 0; k < kRedChunks; ++k)
-                    if (k0 + k < ES)
-#pragma unroll
-                        for (int q = 0; q < kRedPer; ++q) a[q] += v[k][q];
-            }
-#pragma unroll
-            for (int q = 0; q < kRedPer; ++q) {
-                if (tid + kDdThreads * q < nel) {
-                    if (P.bproj) a[q] += *reinterpret_cast<const f32x4 *>(P.bproj + off[q] % d);
-                    *reinterpret_cast<f32x4 *>(P.y + off[q]) = a[q];
-                }
-            }
-        }
-        __syncthreads();  // the unit's LDS buffers and flag are free again
+    for (int k = 0; k < kDecodeChunks; ++k)
+        if (k < ES) a += v[k];
+    if (P.bproj) a += *reinterpret_cast<const f32x4 *>(P.bproj + off % P.d);
+    *reinterpret_cast<f32x4 *>(P.y + off) = a;
+}
+
+template <int NTT>
+void launch_down_dense(const DNParams &dp, int num_cu, hipStream_t s) {
+    constexpr int threads = 64 * dd_waves<NTT>(), rows = 32 * dd_waves<NTT>();
+    static const int occ = resident(down_dense_k<NTT>, threads);
+    const int grid = occ * num_cu;
+    hipLaunchKernelGGL(down_dense_k<NTT>, dim3(grid), dim3(threads), 0, s, dp);
+    int Uc;
+    const int ES = dd_chunks(grid, dp.E, (dp.d + rows - 1) / rows, &Uc);
+    if (ES > 1) {
+        const int n4 = dp.T * (dp.d / 4);
+        hipLaunchKernelGGL(dense_sum_k, dim3((n4 + 255) / 256), dim3(256), 0, s, dp, ES);
     }
 }
 
@@ -1014,16 +1016,13 @@ hipError_t launch_decode_ffn(pp_layer *L, const uint16_t *x, int T, float *y, bo
     dp.dn_cnt = L->counters + counters_for(L->dm, L->max_tokens).down_base();
     dp.plan = plan_view(L, false);
     prof_mark(L, PP_KERNEL_DOWN, s, true);
-    if (dense && T <= 16) {
-        static const int occ = resident(down_dense_k<1>, 64 * dd_waves<1>());
-        hipLaunchKernelGGL(down_dense_k<1>, dim3(occ * L->num_cu), dim3(64 * dd_waves<1>()), 0, s, dp);
-    } else if (dense && T <= 32) {
-        static const int occ = resident(down_dense_k<2>, 64 * dd_waves<2>());
-        hipLaunchKernelGGL(down_dense_k<2>, dim3(occ * L->num_cu), dim3(64 * dd_waves<2>()), 0, s, dp);
-    } else if (dense) {
-        static const int occ = resident(down_dense_k<4>, 64 * dd_waves<4>());
-        hipLaunchKernelGGL(down_dense_k<4>, dim3(occ * L->num_cu), dim3(64 * dd_waves<4>()), 0, s, dp);
-    } else if (T <= 16)
+    if (dense && T <= 16)
+        launch_down_dense<1>(dp, L->num_cu, s);
+    else if (dense && T <= 32)
+        launch_down_dense<2>(dp, L->num_cu, s);
+    else if (dense)
+        launch_down_dense<4>(dp, L->num_cu, s);
+    else if (T <= 16)
         launch_down_dec_tb<16>(dp, L->num_cu, s);
     else if (T <= 32)
         launch_down_dec_tb<32>(dp, L->num_cu, s);
