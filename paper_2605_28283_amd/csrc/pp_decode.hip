@@ -16,7 +16,7 @@
 //                 tokens staged in LDS (code shared with prefill); the K-split
 //                 (one slice more for some groups) makes the units fill the
 //                 resident workgroups exactly, one round.
-//   down_dec_k  : sparse groups (<= 8 tokens per group on average): unit = one
+//   down_dec_k  : sparse groups (<= 16 tokens per group on average): unit = one
 //                 16-row tile of d over all groups; each of the 8 wavefronts
 //                 takes every eighth group, tile by tile of 16 tokens (three
 //                 in flight), multiplies the 16x128 down block with the tokens'
@@ -719,10 +719,12 @@ __global__ __launch_bounds__(kDnThreads, 2) void down_dec_k(DNParams P) {
     } S;
     __shared__ int s_flag;
     const int nU = P.plan.head[0], npairs = P.plan.head[1];
-    // Dense groups (more than 8 tokens per group on average): reading h once
+    // Dense groups (more than 16 tokens per group on average): reading h once
     // per 16-row tile would cost more than the weights, so share it through
-    // LDS across 128-row units, with the groups split into chunks.
-    if (npairs > 8 * nU) {
+    // LDS across 128-row units, with the groups split into chunks.  (Measured
+    // crossover: at 6-16 tokens per group the row tiles are faster, at 28 the
+    // shared h.)
+    if (npairs > 16 * nU) {
         const int n_rb = (P.d + kShRows - 1) / kShRows;
         int ES = (int)gridDim.x / n_rb;
         if (ES > nU / 2) ES = nU / 2;

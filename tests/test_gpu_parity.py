@@ -144,7 +144,10 @@ def test_decode_down_modes_ragged_rows(oracle_mod):
     """d = 576 is not a multiple of 128 or 256: the decode down projection's
     last row block has 64 rows.  tau = 0.3 gives sparse groups (row-tile
     path), tau = 1 keeps every expert (the dense kernel: 128-row units at
-    T = 24, 256-row units at T = 64, several expert chunks)."""
+    T = 24, 256-row units at T = 64, several expert chunks, summed by their
+    own launch), and top-24 of 40 at T = 64 gives ~38 tokens per group
+    without keeping every expert (the shared-h dense-group mode, its chunks
+    summed by the last to arrive)."""
     L = make_layer(576, 40 * 128, 40, 31)
     for T in (24, 64):
         x, _ = make_tokens(T, 576, 32 + T)
@@ -153,6 +156,12 @@ def test_decode_down_modes_ragged_rows(oracle_mod):
                 a = parity(oracle_mod, dl, "decode", x, tau)
                 b = dl.run("decode", x, tau)
                 np.testing.assert_array_equal(a["y"], b[2])  # deterministic
+        if T == 64:
+            with DevLayer(L, 64, flags=TOPK) as dl:
+                a = parity(oracle_mod, dl, "decode", x, 24.0)
+                assert (a["cnt"] == 24).all()
+                b = dl.run("decode", x, 24.0)
+                np.testing.assert_array_equal(a["y"], b[2])
 
 
 @pytest.mark.parametrize("flags", [TOPK, TOPK | SIG])
