@@ -26,6 +26,10 @@
 //                 Dense groups: unit = (128 rows, chunk of groups), h staged
 //                 once in LDS for all 8 wavefronts, chunk partials summed in
 //                 chunk order by the last chunk to arrive.
+//   down_dense_k: every token keeps every expert (16-64 tokens): outputs
+//                 accumulate in registers across a unit's experts, h copied
+//                 into LDS two experts ahead; dense_sum_k (its own launch)
+//                 sums the expert chunks' partials in chunk order.
 //                 No float atomics: decode is deterministic.
 #include "pp_gateup.h"
 
