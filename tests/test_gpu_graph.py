@@ -1,4 +1,5 @@
-"""Decode and prefill calls captured in HIP graphs.
+"""Decode and prefill calls captured in HIP graphs, and two handles driven
+from two streams at once.
 
 The library's per-call state (router partials, token masks, the plan, the
 hand-off counters) lives in the handle and is rebuilt or reset by the calls
@@ -87,3 +88,40 @@ def test_graph_replays_match_eager(handle, mode, T, tau):
     torch.cuda.synchronize()
     for a, b in zip(eager, ref):
         assert a.cpu().numpy().tobytes() == b.tobytes()
+
+
+def test_two_handles_on_two_streams(handle):
+    """Each handle owns its partials, masks, plan and counters: two handles
+    driven from two streams at once (calls interleaved, no synchronisation
+    between them) give each handle's sequential results."""
+    import torch
+    W = make_layer_device(D, DFF, E, 0x6A12)
+    h2 = pp.prunepath_create(D, DFF, E, 2048, W["W_r"], W["W_gate"], W["W_up"], W["W_down"])
+    del W
+    try:
+        work = [(handle, "decode", 32, 0.7), (h2, "prefill", 700, 0.8),
+                (handle, "decode", 64, 1.0), (h2, "decode", 1, 0.5)]
+        xs = [to_dev(make_tokens(T, D, 500 + i)[0]) for i, (_, _, T, _) in enumerate(work)]
+        ref = []
+        for (h, mode, T, tau), x in zip(work, xs):
+            o = _outputs(torch, T)
+            _call(mode, h, x, T, tau, o)
+            torch.cuda.synchronize()
+            ref.append([a.cpu().numpy() for a in o])
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        outs = [_outputs(torch, T) for (_, _, T, _) in work]
+        torch.cuda.synchronize()
+        for rep in range(3):
+            for o in outs:
+                for a in o:
+                    a.fill_(-5)
+            torch.cuda.synchronize()
+            # handle's calls in order on s1, h2's on s2, issued alternately
+            for (h, mode, T, tau), x, o in zip(work, xs, outs):
+                _call(mode, h, x, T, tau, o, stream=s1 if h is handle else s2)
+            torch.cuda.synchronize()
+            for i, (o, r) in enumerate(zip(outs, ref)):
+                for a, b in zip(o, r):
+                    assert a.cpu().numpy().tobytes() == b.tobytes(), (rep, i)
+    finally:
+        pp.prunepath_destroy(h2)
